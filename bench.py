@@ -1,0 +1,248 @@
+"""Benchmark: DistillCache budgeted decode step on one MI355X.
+
+Workload (default): the Mistral-7B-shaped 32-layer KV stack — batch 16, 32
+layers, 32 query / 8 KV heads, head_dim 128, bf16, synthetic context 16384,
+budget 4096 (25 %), per-KV-head top-k.  One *step* is the whole hot path over
+every (batch, layer, KV head) unit: append the new K/V row, GQA decode
+attention, feature accumulation (alpha, windowed entropy, ||v||, position),
+policy-MLP scoring of every cached token, top-4096 keep and in-place
+compaction.  The first (compression) step 16385 -> 4096 runs before the warm-up
+and is reported separately; the timed steps are steady decode steps
+(4097 -> 4096 per unit).
+
+Prints one JSON line.  Inputs are resident in HBM before timing starts.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "decode steps/s + KV GB/s (% of 8 TB/s HBM) for attention+evict at 16k ctx, 25% budget"
+HBM_PEAK_GBPS = 8000.0
+
+
+def decode_alg_bytes(U, L, G, D, elt, append, retire):
+    """Algorithmic HBM bytes of one decode-step launch (every unit):
+    K/V rows read once (L - append rows from the cache; the appended row arrives
+    in k_new/v_new and is written once), feature state read+write (alpha f32,
+    num/den f64: 40 B/row; pos read 4 B/row when the window retires; vnorm
+    written 4 B/row), queries read, outputs written, the ring slot's queries read
+    (when retiring) and written, per-query statistics."""
+    row = 2 * D * elt
+    per_unit = (L - append) * row
+    per_unit += append * 2 * row                     # k_new/v_new read + cache write
+    per_unit += L * (40 + 4) + (L * 4 if retire else 0)
+    qbytes = G * D * elt
+    per_unit += 2 * qbytes + qbytes + (qbytes if retire else 0) + 2 * G * 3 * 4
+    return U * per_unit
+
+
+def evict_alg_bytes(U, L, moved, D, elt):
+    """score/select/compact: features read (alpha, vnorm f32, num/den f64, pos i32:
+    28 B/row), moved rows read+written (K/V + 28 B of state each)."""
+    return U * L * 28 + moved * 2 * (2 * D * elt + 28)
+
+
+def kv_bytes(U, L, D, elt, moved, append=1):
+    """KV bytes of a step: K/V read by attention, the appended row written, and the
+    K/V part of the compaction moves (read + write)."""
+    row = 2 * D * elt
+    return U * ((L - append) * row + append * 2 * row) + moved * 2 * row
+
+
+def run_oracle_baseline(wl, units, steps, seed_units=0):
+    """Time the CPU oracle on a bounded sample: `units` units, each brought to the
+    steady state (untimed compression step) and then stepped `steps` times."""
+    import numpy as np
+
+    from oracle import unit as ounit
+    from oracle import attention as oatt
+    from synth import workloads as W
+
+    params = W.policy_params(wl)
+    scale = oatt.default_scale(wl.head_dim)
+    total = 0.0
+    for k in range(units):
+        u = (k * 2654435761 + seed_units) % wl.units
+        pos = np.arange(wl.n0)
+        st = ounit.new_student(W.key_rows(wl, u, pos), W.value_rows(wl, u, pos), pos,
+                               G=wl.group, scale=scale, window=wl.ent_window, next_pos=wl.n0)
+        inputs = []
+        for t in range(steps + 1):
+            p = [wl.n0 + t]
+            inputs.append((W.queries(wl, t, u), W.key_rows(wl, u, p)[0], W.value_rows(wl, u, p)[0]))
+        ounit.decode_step(st, *inputs[0])
+        ounit.score_evict(st, params, wl.hidden, wl.budget)
+        t0 = time.perf_counter()
+        for t in range(1, steps + 1):
+            ounit.decode_step(st, *inputs[t])
+            ounit.score_evict(st, params, wl.hidden, wl.budget)
+        total += time.perf_counter() - t0
+    per_unit_step = total / (units * steps)
+    return per_unit_step, total
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=128)
+    ap.add_argument("--warmup", type=int, default=8)
+    ap.add_argument("--config", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-units", type=int, default=16)
+    ap.add_argument("--cpu-steps", type=int, default=48)
+    ap.add_argument("--calib-copy-mib", type=int, default=1024,
+                    help="size of the plain copy kernel run first (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the decode step shards by independent "
+              "(batch, layer, KV head) units with no exchange, and this build runs on a "
+              "single MI355X; run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2608_08878_amd.buffers import DecodeBuffers, make_policy
+    from synth import gpu as sg
+    from synth import workloads as W
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda")
+    wl = W.WORKLOADS[args.config]
+    U, G, D, elt = wl.units, wl.group, wl.head_dim, 2 if wl.dtype == "bf16" else 4
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+
+    # plain copy kernel of known size (HBM counter calibration under rocprofv3 --pmc)
+    if args.calib_copy_mib > 0:
+        a = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    cap = max(wl.n0 + 1, wl.budget + 1)
+    buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, D, cap, wl.dtype,
+                        wl.ent_window)
+    buf.reserve_workspace(cap)
+    t0 = time.time()
+    sg.init_cache(wl, buf.k, buf.v, U, cap)
+    buf.feat_init(wl.n0, 0)
+    params = torch.empty(wl.n_params, dtype=torch.float32, device=dev)
+    sg.fill_normal(params, wl, W.S_POLICY, 0, 0.1)
+    pol = make_policy(params, wl.hidden)
+    nsteps = 1 + args.warmup + args.steps
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    Q = torch.empty((nsteps, U, G, D), dtype=td, device=dev)
+    KN = torch.empty((nsteps, U, D), dtype=td, device=dev)
+    VN = torch.empty_like(KN)
+    for t in range(nsteps):
+        sg.queries(wl, t, Q[t])
+        sg.new_rows(wl, t, KN[t], VN[t], U)
+    out = torch.empty((U, G, D), dtype=td, device=dev)
+    torch.cuda.synchronize()
+    log(f"setup {time.time() - t0:.1f}s: {U} units, cache {buf.k.numel() * elt * 2 / 1e9:.1f} GB")
+
+    # step 0: compression n0+1 -> budget (reported separately)
+    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    e0.record()
+    buf.decode_step(Q[0], KN[0], VN[0], out)
+    e1.record()
+    buf.score_evict(pol, wl.budget)
+    e2.record()
+    torch.cuda.synchronize()
+    first = (e0.elapsed_time(e1), e1.elapsed_time(e2))
+    log(f"step 0 (L={wl.n0 + 1} -> {wl.budget}): decode {first[0]:.3f} ms, evict {first[1]:.3f} ms")
+
+    for t in range(1, 1 + args.warmup):
+        buf.decode_step(Q[t], KN[t], VN[t], out)
+        buf.score_evict(pol, wl.budget)
+    torch.cuda.synchronize()
+
+    L_steady = buf.kv.len + 1
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for i in range(args.steps):
+        t = 1 + args.warmup + i
+        a, b, c = ev[i]
+        a.record()
+        buf.decode_step(Q[t], KN[t], VN[t], out)
+        b.record()
+        buf.score_evict(pol, wl.budget)
+        c.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    dec_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
+    evi_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
+    gpu_ms = float(np.sum([a.elapsed_time(c) for a, _, c in ev])) / args.steps
+    ms_per_step = wall * 1e3 / args.steps
+    log(f"steady: {ms_per_step:.3f} ms/step (events {gpu_ms:.3f}); decode {dec_ms:.3f} ms, "
+        f"evict {evi_ms:.3f} ms")
+
+    # moved rows per steady step (one untimed extra step with the slot map)
+    kept = torch.empty((U, wl.budget), dtype=torch.int32, device=dev)
+    t = nsteps - 1
+    buf.decode_step(Q[t], KN[t], VN[t], out)
+    buf.score_evict(pol, wl.budget, kept_out=kept)
+    torch.cuda.synchronize()
+    moved = int((kept != torch.arange(wl.budget, device=dev, dtype=torch.int32)[None, :]).sum())
+
+    retire = True
+    dec_bytes = decode_alg_bytes(U, L_steady, G, D, elt, 1, retire)
+    evi_bytes = evict_alg_bytes(U, L_steady, moved, D, elt)
+    kvb = kv_bytes(U, L_steady, D, elt, moved)
+    steps_per_s = 1e3 / ms_per_step
+    dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
+    result = {
+        "metric": METRIC,
+        "value": round(steps_per_s, 3),
+        "unit": "decode steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded Philox; Mistral-7B-shaped K/V with log-normal key norms)",
+        "config": {"workload": wl.name, "batch": wl.batch, "layers": wl.n_layers,
+                   "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "head_dim": D,
+                   "context": wl.n0, "budget": wl.budget, "units": U,
+                   "steady_len": L_steady, "policy": "4->%s->1 ReLU MLP" % "->".join(map(str, wl.hidden))},
+        "kv_gbps": round(kvb / (ms_per_step * 1e-3) / 1e9, 1),
+        "kv_frac_of_8TBps": round(kvb / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "kv_bytes_per_step": kvb,
+        "all_bytes_gbps": round((dec_bytes + evi_bytes) / (ms_per_step * 1e-3) / 1e9, 1),
+        "moved_rows_per_step": moved,
+        "decode_ms": round(dec_ms, 4),
+        "evict_ms": round(evi_ms, 4),
+        "first_step_ms": {"decode": round(first[0], 3), "evict": round(first[1], 3)},
+        "roofline": {"bound": "hbm", "kernel": "decode_unit_kernel (attention + features)",
+                     "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "alg_bytes_per_launch": dec_bytes},
+    }
+    if not args.no_cpu_baseline:
+        del buf, Q, KN, VN
+        torch.cuda.empty_cache()
+        per_unit_step, total = run_oracle_baseline(wl, args.cpu_units, args.cpu_steps)
+        cpu_sps = 1.0 / (per_unit_step * U)
+        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        result["cpu_baseline"] = {
+            "value": cpu_sps, "unit": "decode steps/s", "cores": threads, "kind": "oracle",
+            "sample": f"{args.cpu_units} units x {args.cpu_steps} steady steps "
+                      f"({total:.1f} s), scaled by {U} units per step; numpy float64"}
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

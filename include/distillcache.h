@@ -1,0 +1,193 @@
+/*
+ * distillcache.h — C ABI of the DistillCache budgeted decode step for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The method (DistillCache: KL-guided adaptive KV-cache eviction) keeps, at
+ * every decode step, a subset C'_t of the cache C_t with |C'_t| <= B (problem
+ * formulation, Sec. 3.1).  One step (Algorithm 1, "DistillCache Inference"):
+ *   1. the forward pass appends the new key/value pair and attends over the
+ *      cache that now contains it;
+ *   2. per-token features x_i are built from that step's attention and the
+ *      cache (state space, Sec. 3.1.1);
+ *   3. a small MLP scores every cached token, s_i = f_phi(x_i) (Sec. 3.1.2);
+ *   4. the top-B tokens are kept and the pruned cache serves the next step.
+ * Training adds the per-step reward R_t = -KL(P_t || P^_t) between the
+ * full-cache (teacher) and pruned-cache (student) next-token distributions
+ * (reward, Sec. 3.1.4; teacher/student caches, Sec. 3.1.3).
+ *
+ * Terms used below
+ *   unit   one (batch b, layer l, KV head g) cache; units are numbered
+ *          u = (b * n_layers + l) * n_kv_heads + g and are fully independent.
+ *   G      n_q_heads / n_kv_heads query heads per unit (grouped-query
+ *          attention); query head h = g * G + j, j < G, reads KV head g.
+ *   T      tokens seen so far; a token's position p is its 0-based index.
+ *
+ * Conventions for every entry point
+ *   - Pointers are DEVICE memory owned by the caller unless marked "host".
+ *     The library allocates and frees nothing; scratch comes from the
+ *     caller's workspace (dc_workspace_bytes).
+ *   - Arguments are validated on the host before any launch; an invalid call
+ *     returns an error status and leaves every buffer and host field untouched.
+ *   - Work is enqueued on the given HIP stream (NULL = default stream) and is
+ *     asynchronous; outputs are valid once the stream reaches that point.  A
+ *     failed launch returns DC_ERR_HIP.
+ *   - Host bookkeeping fields (dc_kv.len, dc_feat.step/next_pos/ring_pmax) are
+ *     updated at enqueue time; nothing is read back from the device.
+ *   - Results are deterministic: the same inputs give the same bits (no
+ *     floating-point atomics).
+ *   - Calls on the same buffers must be ordered on one stream; calls on
+ *     disjoint buffers and workspaces may run concurrently.
+ */
+#ifndef DISTILLCACHE_H
+#define DISTILLCACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  DC_OK = 0,
+  DC_ERR_NULL = 1,         /* a required pointer is NULL */
+  DC_ERR_SHAPE = 2,        /* inconsistent sizes (e.g. len > capacity, empty cache) */
+  DC_ERR_UNSUPPORTED = 3,  /* valid but not implemented (head_dim, G, len limits) */
+  DC_ERR_CAPACITY = 4,     /* appending would exceed the capacity */
+  DC_ERR_BUDGET = 5,       /* budget < 1 */
+  DC_ERR_WORKSPACE = 6,    /* workspace missing or smaller than dc_workspace_bytes */
+  DC_ERR_HIP = 7           /* a HIP launch failed */
+} dc_status;
+
+typedef enum { DC_F32 = 0, DC_BF16 = 1 } dc_dtype;
+
+#define DC_MAX_WINDOW 64
+
+/* Shapes.  Supported: head_dim in {64, 128}; G = n_q_heads / n_kv_heads in
+ * {1, 2, 4, 8}; dtype DC_F32 or DC_BF16. */
+typedef struct {
+  int32_t batch, n_layers, n_q_heads, n_kv_heads, head_dim;
+  int32_t capacity;    /* rows allocated per unit in every per-row buffer */
+  int32_t dtype;       /* dc_dtype of q, k, v, out and the query ring */
+  int32_t ent_window;  /* entropy window w in decode steps, 1..64; 0 = unbounded */
+  float scale;         /* logit scale; 0 selects 1/sqrt(head_dim) */
+} dc_dims;
+
+/* The student (or teacher) KV cache C_t.  Row i < len of unit u lives at
+ * k[(u * capacity + i) * head_dim ...], likewise v.  Slot order is not token
+ * order: eviction fills holes (see dc_score_evict). */
+typedef struct {
+  void *k, *v;         /* [units][capacity][head_dim], dtype */
+  int32_t len;         /* host: valid rows per unit (identical for all units) */
+} dc_kv;
+
+/* Per-token feature state of the student cache (Sec. 3.1.1, state space).
+ * The feature vector is x_i = [alpha_i, ||v_i||_2, H_i, pos_i]:
+ *   alpha_i  attention mass token i received, averaged over the G query heads
+ *            of its unit and accumulated over decode steps;
+ *   H_i      = ent_num_i / ent_den_i (0 when ent_den_i = 0), where over the
+ *            queries q of the last w steps (each (step, query head) pair)
+ *            ent_den_i = sum_q a_q(i) and ent_num_i = sum_q a_q(i) H(a_q),
+ *            H(a) = -sum a ln a the entropy of the query's attention;
+ *   pos_i    = pos[i] / T.
+ * Row arrays are [units][capacity] and follow the K/V slots.  The query ring
+ * keeps, for each of the last w steps (slot = step mod w), the G queries and
+ * their softmax statistics so that the contribution of step t - w can be
+ * recomputed and removed from ent_num/ent_den at step t. */
+typedef struct {
+  float   *alpha;      /* [units][capacity] */
+  double  *ent_num;    /* [units][capacity] */
+  double  *ent_den;    /* [units][capacity] */
+  int32_t *pos;        /* [units][capacity] absolute position of the token in the slot */
+  float   *vnorm;      /* [units][capacity] ||v_i||_2, rewritten by every decode step */
+  void    *qring;      /* [units][w][G][head_dim], dtype: queries of the last w steps */
+  float   *qstat;      /* [units][w][G][3]: (m, 1/l, H) of each query, where
+                          m = max_i s_i, l = sum_i exp(s_i - m), s_i = scale * q.k_i */
+  int32_t step;        /* host: decode steps done since the state was initialised */
+  int32_t next_pos;    /* host: T, the position the next appended token receives */
+  int32_t ring_pmax[DC_MAX_WINDOW]; /* host: per ring slot, largest position present (T - 1) */
+} dc_feat;
+
+/* Policy MLP f_phi (Sec. 3.1.2; a small ReLU MLP per App. D).  params is a
+ * packed float32 blob, row-major:
+ *   W1[hidden[0]][n_in], b1[hidden[0]],
+ *   (W2[hidden[1]][hidden[0]], b2[hidden[1]]),   -- only if n_hidden_layers == 2
+ *   w_out[hidden[last]], b_out
+ * h = relu(W1 x + b1) [, h = relu(W2 h + b2)], s = w_out . h + b_out.
+ * Supported: n_in = 4, n_hidden_layers in {1, 2}, hidden widths 1..128 (the
+ * first width at most 64 when there are two hidden layers). */
+typedef struct {
+  int32_t n_in;
+  int32_t n_hidden_layers;
+  int32_t hidden[2];
+  const float *params;  /* device */
+} dc_policy;
+
+/* Bytes of caller workspace the entry points need for caches of up to max_len
+ * rows per unit (dc_decode_step, dc_score_evict) and for a KL reward over
+ * kl_rows rows of a kl_vocab-entry vocabulary (dc_kl_reward).  Pass 0 for the
+ * parts not used.  Returns 0 for invalid dims. */
+size_t dc_workspace_bytes(const dc_dims *dims, int32_t max_len, int32_t kl_rows, int32_t kl_vocab);
+
+/* Initialise the feature state of a cache holding kv->len rows per unit whose
+ * slot i holds the token at position first_pos + i (a freshly filled cache):
+ * alpha = ent_num = ent_den = 0, pos, vnorm from the value rows; host fields
+ * step = 0, next_pos = first_pos + kv->len. */
+dc_status dc_feat_init(const dc_dims *dims, const dc_kv *kv, dc_feat *feat, int32_t first_pos,
+                       void *hip_stream);
+
+/* One decode-step forward over every unit (Algorithm 1, forward pass and
+ * feature extraction; Sec. 3.1.1).
+ *   q      [batch][n_layers][n_q_heads][head_dim], dtype
+ *   k_new, v_new  [batch][n_layers][n_kv_heads][head_dim], dtype, or both NULL
+ *          for no append.  The pair is written to slot len, its features are
+ *          zeroed, pos = T, then len += 1 and T += 1 (host fields).
+ *   out    [batch][n_layers][n_q_heads][head_dim], dtype: o_j = sum_i a_{j,i} v_i
+ *          over the len rows (after the append), a_j = softmax_i(scale q_j.k_i).
+ *   feat   NULL => plain attention (the never-pruned teacher cache of
+ *          Sec. 3.1.3); otherwise alpha += (1/G) sum_j a_j(i), this step's
+ *          queries enter the entropy window, step t - w leaves it, vnorm is
+ *          rewritten, the ring slot (step mod w) is overwritten, step += 1.
+ * Errors: DC_ERR_NULL, DC_ERR_SHAPE (len == 0 without append, len > capacity),
+ * DC_ERR_CAPACITY (len + 1 > capacity), DC_ERR_UNSUPPORTED, DC_ERR_WORKSPACE. */
+dc_status dc_decode_step(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const void *q,
+                         const void *k_new, const void *v_new, void *out, void *ws,
+                         size_t ws_bytes, void *hip_stream);
+
+/* Score every cached token with the policy and keep the top `budget` per unit
+ * (Algorithm 1 scoring, argtop_B and prune; Sec. 3.1.2 deterministic top-B).
+ * Order: higher score first; equal scores keep the earlier token (smaller
+ * pos); -0 equals +0; NaN ranks below every number.  If budget >= len nothing
+ * moves.  Otherwise the kept rows end in slots 0..budget-1: a kept row already
+ * there stays in place, and the evicted slots below budget ("holes", in
+ * ascending order) receive the kept rows from slots >= budget (ascending),
+ * carrying k, v, alpha, ent_num, ent_den, pos and vnorm.  len = budget (host).
+ *   scores_out  [units][len] float32 scores in pre-eviction slot order, or NULL.
+ *   kept_out    [units][min(budget, len)] int32: pre-eviction slot of the row
+ *               that ends in each slot, or NULL.
+ * Errors: DC_ERR_NULL, DC_ERR_BUDGET (budget < 1), DC_ERR_UNSUPPORTED (policy
+ * shape, len > 40960), DC_ERR_SHAPE, DC_ERR_WORKSPACE (len > 8192 needs
+ * dc_workspace_bytes scratch). */
+dc_status dc_score_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const dc_policy *policy,
+                         int32_t budget, float *scores_out, int32_t *kept_out, void *ws,
+                         size_t ws_bytes, void *hip_stream);
+
+/* Per-step KL reward (Sec. 3.1.4): for each row r,
+ *   kl_out[r] = KL(P || Q) = sum_v P_v (ln P_v - ln Q_v)   (nats),
+ * P = softmax(h_full[r] W^T), Q = softmax(h_comp[r] W^T) over the whole vocab.
+ *   h_full, h_comp  [rows][hidden] bfloat16
+ *   w_lm            [vocab][hidden] bfloat16 (the lm-head weight)
+ *   kl_out          [rows] float32; the reward is R = -kl_out.
+ * Supported: hidden % 128 == 0, vocab % 64 == 0, 1 <= rows <= 64.
+ * Errors: DC_ERR_NULL, DC_ERR_SHAPE, DC_ERR_UNSUPPORTED, DC_ERR_WORKSPACE. */
+dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void *h_full,
+                       const void *h_comp, const void *w_lm, float *kl_out, void *ws,
+                       size_t ws_bytes, void *hip_stream);
+
+/* Static string naming a status. */
+const char *dc_status_str(dc_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DISTILLCACHE_H */

@@ -1,0 +1,130 @@
+"""ctypes binding of libdistillcache.so: the C-ABI structs and entry points
+under the same names (argument marshalling only; all work runs in the HIP
+kernels).  Tensors are passed as device pointers (``Tensor.data_ptr()``)."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libdistillcache.so")
+
+MAX_WINDOW = 64
+DC_F32, DC_BF16 = 0, 1
+STATUS = {0: "DC_OK", 1: "DC_ERR_NULL", 2: "DC_ERR_SHAPE", 3: "DC_ERR_UNSUPPORTED",
+          4: "DC_ERR_CAPACITY", 5: "DC_ERR_BUDGET", 6: "DC_ERR_WORKSPACE", 7: "DC_ERR_HIP"}
+
+
+class dc_dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("capacity", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("ent_window", ctypes.c_int32),
+                ("scale", ctypes.c_float)]
+
+
+class dc_kv(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("len", ctypes.c_int32)]
+
+
+class dc_feat(ctypes.Structure):
+    _fields_ = [("alpha", ctypes.c_void_p), ("ent_num", ctypes.c_void_p),
+                ("ent_den", ctypes.c_void_p), ("pos", ctypes.c_void_p),
+                ("vnorm", ctypes.c_void_p), ("qring", ctypes.c_void_p),
+                ("qstat", ctypes.c_void_p), ("step", ctypes.c_int32),
+                ("next_pos", ctypes.c_int32), ("ring_pmax", ctypes.c_int32 * MAX_WINDOW)]
+
+
+class dc_policy(ctypes.Structure):
+    _fields_ = [("n_in", ctypes.c_int32), ("n_hidden_layers", ctypes.c_int32),
+                ("hidden", ctypes.c_int32 * 2), ("params", ctypes.c_void_p)]
+
+
+EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
+           "dc_kl_reward", "dc_status_str")
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load the HIP library; raises if it has not been built (there is no fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "python -m paper_2608_08878_amd.build (or __graft_entry__.build())")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        L.dc_workspace_bytes.argtypes = [ctypes.POINTER(dc_dims), i32, i32, i32]
+        L.dc_workspace_bytes.restype = sz
+        L.dc_feat_init.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                   ctypes.POINTER(dc_feat), i32, vp]
+        L.dc_feat_init.restype = ctypes.c_int
+        L.dc_decode_step.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                     ctypes.POINTER(dc_feat), vp, vp, vp, vp, vp, sz, vp]
+        L.dc_decode_step.restype = ctypes.c_int
+        L.dc_score_evict.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                     ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
+                                     vp, vp, vp, sz, vp]
+        L.dc_score_evict.restype = ctypes.c_int
+        L.dc_kl_reward.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.dc_kl_reward.restype = ctypes.c_int
+        L.dc_status_str.argtypes = [ctypes.c_int]
+        L.dc_status_str.restype = ctypes.c_char_p
+        _lib = L
+    return _lib
+
+
+class DCError(RuntimeError):
+    def __init__(self, status: int):
+        self.status = status
+        super().__init__(dc_status_str(status))
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _check(st: int) -> None:
+    if st != 0:
+        raise DCError(st)
+
+
+def _ref(x):
+    return None if x is None else ctypes.byref(x)
+
+
+def dc_status_str(status: int) -> str:
+    return lib().dc_status_str(status).decode()
+
+
+def dc_workspace_bytes(dims: dc_dims, max_len: int, kl_rows: int = 0, kl_vocab: int = 0) -> int:
+    return int(lib().dc_workspace_bytes(ctypes.byref(dims), max_len, kl_rows, kl_vocab))
+
+
+def dc_feat_init(dims, kv, feat, first_pos: int, stream=None) -> None:
+    _check(lib().dc_feat_init(ctypes.byref(dims), ctypes.byref(kv), ctypes.byref(feat),
+                              first_pos, stream))
+
+
+def dc_decode_step(dims, kv, feat, q, k_new, v_new, out, ws=None, ws_bytes: int = 0,
+                   stream=None) -> None:
+    _check(lib().dc_decode_step(ctypes.byref(dims), ctypes.byref(kv), _ref(feat), _ptr(q),
+                                _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_score_evict(dims, kv, feat, policy, budget: int, scores_out=None, kept_out=None,
+                   ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_score_evict(ctypes.byref(dims), ctypes.byref(kv), _ref(feat),
+                                _ref(policy), budget, _ptr(scores_out), _ptr(kept_out),
+                                _ptr(ws), ws_bytes, stream))
+
+
+def dc_kl_reward(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_out, ws=None,
+                 ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_kl_reward(rows, hidden, vocab, _ptr(h_full), _ptr(h_comp), _ptr(w_lm),
+                              _ptr(kl_out), _ptr(ws), ws_bytes, stream))

@@ -1,0 +1,83 @@
+"""Device buffers for the C-ABI structs, allocated with torch (device memory and
+streams only; no computation happens here)."""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import binding as B
+
+TORCH_DTYPE = {"f32": torch.float32, "bf16": torch.bfloat16}
+DC_DTYPE = {"f32": B.DC_F32, "bf16": B.DC_BF16}
+
+
+def stream_handle(stream=None):
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+class DecodeBuffers:
+    """K/V cache and (optionally) feature state for `units` caches of `capacity` rows."""
+
+    def __init__(self, batch, n_layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype="bf16",
+                 ent_window=64, scale=0.0, features=True, device="cuda"):
+        self.G = n_q_heads // n_kv_heads
+        self.U = batch * n_layers * n_kv_heads
+        self.D = head_dim
+        self.cap = capacity
+        self.dtype = dtype
+        self.window = ent_window
+        td = TORCH_DTYPE[dtype]
+        self.dims = B.dc_dims(batch, n_layers, n_q_heads, n_kv_heads, head_dim, capacity,
+                              DC_DTYPE[dtype], ent_window, scale)
+        self.k = torch.zeros((self.U, capacity, head_dim), dtype=td, device=device)
+        self.v = torch.zeros((self.U, capacity, head_dim), dtype=td, device=device)
+        self.kv = B.dc_kv(self.k.data_ptr(), self.v.data_ptr(), 0)
+        self.feat = None
+        if features:
+            self.alpha = torch.zeros((self.U, capacity), dtype=torch.float32, device=device)
+            self.num = torch.zeros((self.U, capacity), dtype=torch.float64, device=device)
+            self.den = torch.zeros((self.U, capacity), dtype=torch.float64, device=device)
+            self.pos = torch.zeros((self.U, capacity), dtype=torch.int32, device=device)
+            self.vnorm = torch.zeros((self.U, capacity), dtype=torch.float32, device=device)
+            w = max(ent_window, 1)
+            self.qring = torch.zeros((self.U, w, self.G, head_dim), dtype=td, device=device)
+            self.qstat = torch.zeros((self.U, w, self.G, 3), dtype=torch.float32, device=device)
+            self.feat = B.dc_feat(self.alpha.data_ptr(), self.num.data_ptr(), self.den.data_ptr(),
+                                  self.pos.data_ptr(), self.vnorm.data_ptr(),
+                                  self.qring.data_ptr(), self.qstat.data_ptr(), 0, 0)
+        self.ws = None
+        self.ws_bytes = 0
+
+    @property
+    def len(self) -> int:
+        return self.kv.len
+
+    def reserve_workspace(self, max_len: int, kl_rows: int = 0, kl_vocab: int = 0):
+        need = B.dc_workspace_bytes(self.dims, max_len, kl_rows, kl_vocab)
+        if need > self.ws_bytes:
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.k.device)
+            self.ws_bytes = need
+        return self.ws
+
+    def feat_init(self, length: int, first_pos: int = 0, stream=None):
+        self.kv.len = length
+        B.dc_feat_init(self.dims, self.kv, self.feat, first_pos, stream_handle(stream))
+
+    def decode_step(self, q, k_new=None, v_new=None, out=None, stream=None, features=True):
+        if out is None:
+            out = torch.empty_like(q)
+        B.dc_decode_step(self.dims, self.kv, self.feat if features else None, q, k_new, v_new,
+                         out, self.ws, self.ws_bytes, stream_handle(stream))
+        return out
+
+    def score_evict(self, policy, budget, scores_out=None, kept_out=None, stream=None):
+        B.dc_score_evict(self.dims, self.kv, self.feat, policy, budget, scores_out, kept_out,
+                         self.ws, self.ws_bytes, stream_handle(stream))
+
+
+def make_policy(params: torch.Tensor, hidden) -> B.dc_policy:
+    hidden = tuple(hidden)
+    h = (ctypes.c_int32 * 2)(hidden[0], hidden[1] if len(hidden) > 1 else 0)
+    return B.dc_policy(4, len(hidden), h, params.data_ptr())

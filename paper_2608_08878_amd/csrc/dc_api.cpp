@@ -1,0 +1,274 @@
+// Host side of the C ABI: argument validation (no HIP call before it passes),
+// workspace sizing, path selection and host bookkeeping.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <string.h>
+
+#include "../../include/distillcache.h"
+#include "dc_kernels.hpp"
+
+namespace {
+
+constexpr int EVICT_REG_ROWS = 8192;
+
+int64_t units_of(const dc_dims* d) { return (int64_t)d->batch * d->n_layers * d->n_kv_heads; }
+int group_of(const dc_dims* d) { return d->n_q_heads / d->n_kv_heads; }
+
+dc_status check_dims(const dc_dims* d) {
+  if (!d) return DC_ERR_NULL;
+  if (d->batch < 1 || d->n_layers < 1 || d->n_q_heads < 1 || d->n_kv_heads < 1 || d->capacity < 1 ||
+      d->head_dim < 1)
+    return DC_ERR_SHAPE;
+  if (d->n_q_heads % d->n_kv_heads) return DC_ERR_SHAPE;
+  const int G = group_of(d);
+  if (G != 1 && G != 2 && G != 4 && G != 8) return DC_ERR_UNSUPPORTED;
+  if (d->head_dim != 64 && d->head_dim != 128) return DC_ERR_UNSUPPORTED;
+  if (d->dtype != DC_F32 && d->dtype != DC_BF16) return DC_ERR_UNSUPPORTED;
+  if (d->ent_window < 0 || d->ent_window > DC_MAX_WINDOW) return DC_ERR_SHAPE;
+  if (!(d->scale >= 0.0f) || isinf(d->scale)) return DC_ERR_SHAPE;
+  if (units_of(d) > (1 << 24) || d->capacity > (1 << 26)) return DC_ERR_UNSUPPORTED;
+  return DC_OK;
+}
+
+float scale_of(const dc_dims* d) { return d->scale > 0.0f ? d->scale : 1.0f / sqrtf((float)d->head_dim); }
+
+size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+int nchunks_of(int L) { return (L + dc::decode_chunk_rows() - 1) / dc::decode_chunk_rows(); }
+
+// Scratch of the chunked decode path for caches of L rows.
+size_t split_bytes(const dc_dims* d, int L) {
+  const size_t U = (size_t)units_of(d), G = group_of(d), D = d->head_dim;
+  const size_t rows = U * (size_t)L * (G + 3) * sizeof(float);
+  const size_t parts = U * (size_t)nchunks_of(L) * (3 * G + G * D) * sizeof(float);
+  return align256(rows) + align256(parts);
+}
+
+bool use_split(const dc_dims* d, int L, bool feat) {
+  const int G = group_of(d);
+  if (feat && !dc::decode_fits_lds(L, G, d->head_dim)) return true;
+  // few units: spread one unit's rows over several workgroups
+  return units_of(d) < 128 && L > 2 * dc::decode_chunk_rows();
+}
+
+size_t evict_bytes(const dc_dims* d, int L) { return align256(dc::evict_ws_bytes((int)units_of(d), L)); }
+
+size_t kl_bytes(int rows, int vocab) {
+  return align256((size_t)rows * (size_t)(vocab / dc::kl_tile_cols()) * 4 * sizeof(float));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dc_status_str(dc_status s) {
+  switch (s) {
+    case DC_OK: return "DC_OK";
+    case DC_ERR_NULL: return "DC_ERR_NULL: a required pointer is NULL";
+    case DC_ERR_SHAPE: return "DC_ERR_SHAPE: inconsistent sizes";
+    case DC_ERR_UNSUPPORTED: return "DC_ERR_UNSUPPORTED: shape or option not implemented";
+    case DC_ERR_CAPACITY: return "DC_ERR_CAPACITY: append exceeds the cache capacity";
+    case DC_ERR_BUDGET: return "DC_ERR_BUDGET: budget must be >= 1";
+    case DC_ERR_WORKSPACE: return "DC_ERR_WORKSPACE: workspace missing or too small";
+    case DC_ERR_HIP: return "DC_ERR_HIP: a HIP launch failed";
+  }
+  return "unknown dc_status";
+}
+
+size_t dc_workspace_bytes(const dc_dims* dims, int32_t max_len, int32_t kl_rows, int32_t kl_vocab) {
+  size_t need = 0;
+  if (max_len > 0) {
+    if (check_dims(dims) != DC_OK) return 0;
+    const size_t a = split_bytes(dims, max_len), b = evict_bytes(dims, max_len);
+    need = a > b ? a : b;
+  }
+  if (kl_rows > 0 && kl_vocab > 0) {
+    const size_t c = kl_bytes(kl_rows, kl_vocab);
+    need = c > need ? c : need;
+  }
+  return need;
+}
+
+dc_status dc_feat_init(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, int32_t first_pos,
+                       void* hip_stream) {
+  dc_status st = check_dims(dims);
+  if (st != DC_OK) return st;
+  if (!kv || !feat || !kv->v || !feat->alpha || !feat->ent_num || !feat->ent_den || !feat->pos ||
+      !feat->vnorm)
+    return DC_ERR_NULL;
+  if (kv->len < 0 || kv->len > dims->capacity || first_pos < 0) return DC_ERR_SHAPE;
+  if (kv->len > 0) {
+    dc::DecodeArgs a;
+    memset(&a, 0, sizeof(a));
+    a.v = kv->v;
+    a.alpha = feat->alpha;
+    a.num = feat->ent_num;
+    a.den = feat->ent_den;
+    a.pos = feat->pos;
+    a.vnorm = feat->vnorm;
+    a.cap = dims->capacity;
+    a.units = (int)units_of(dims);
+    a.L = kv->len;
+    if (dc::launch_feat_init(a, dims->dtype, dims->head_dim, first_pos, hip_stream) != 0)
+      return DC_ERR_HIP;
+  }
+  feat->step = 0;
+  feat->next_pos = first_pos + kv->len;
+  memset(feat->ring_pmax, 0, sizeof(feat->ring_pmax));
+  return DC_OK;
+}
+
+dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const void* q,
+                         const void* k_new, const void* v_new, void* out, void* ws,
+                         size_t ws_bytes, void* hip_stream) {
+  dc_status st = check_dims(dims);
+  if (st != DC_OK) return st;
+  if (!kv || !kv->k || !kv->v || !q || !out) return DC_ERR_NULL;
+  if ((k_new == nullptr) != (v_new == nullptr)) return DC_ERR_NULL;
+  const int W = dims->ent_window;
+  if (feat) {
+    if (!feat->alpha || !feat->ent_num || !feat->ent_den || !feat->pos || !feat->vnorm)
+      return DC_ERR_NULL;
+    if (W > 0 && (!feat->qring || !feat->qstat)) return DC_ERR_NULL;
+    if (feat->step < 0 || feat->next_pos < 0) return DC_ERR_SHAPE;
+  }
+  const int len = kv->len;
+  const int append = k_new != nullptr;
+  if (len < 0 || len > dims->capacity) return DC_ERR_SHAPE;
+  if (append && len + 1 > dims->capacity) return DC_ERR_CAPACITY;
+  if (!append && len == 0) return DC_ERR_SHAPE;
+  const int L = len + append;
+  const bool split = use_split(dims, L, feat != nullptr);
+  const size_t need = split ? split_bytes(dims, L) : 0;
+  if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
+
+  const int G = group_of(dims), D = dims->head_dim;
+  const int U = (int)units_of(dims);
+  dc::DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = q;
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.out = out;
+  a.k = kv->k;
+  a.v = kv->v;
+  a.cap = dims->capacity;
+  a.units = U;
+  a.len_old = len;
+  a.L = L;
+  a.append = append;
+  a.scale = scale_of(dims);
+  int slot = 0;
+  if (feat) {
+    a.alpha = feat->alpha;
+    a.num = feat->ent_num;
+    a.den = feat->ent_den;
+    a.pos = feat->pos;
+    a.vnorm = feat->vnorm;
+    a.qring = feat->qring;
+    a.qstat = feat->qstat;
+    a.T = feat->next_pos + append;
+    a.window = W;
+    if (W > 0) {
+      slot = feat->step % W;
+      a.slot = slot;
+      a.retire = feat->step >= W;
+      a.pmax_ret = a.retire ? feat->ring_pmax[slot] : 0;
+    }
+  }
+  if (split) {
+    const size_t rows = (size_t)U * L;
+    float* base = (float*)ws;
+    a.lmax = L;
+    a.chunk = dc::decode_chunk_rows();
+    a.nchunks = nchunks_of(L);
+    a.ws_s = base;
+    a.ws_r = base + rows * G;
+    a.ws_v = base + rows * (G + 2);
+    a.ws_part = (float*)((char*)ws + align256(rows * (G + 3) * sizeof(float)));
+  }
+  if (dc::launch_decode(a, dims->dtype, D, G, feat != nullptr, split, hip_stream) != 0)
+    return DC_ERR_HIP;
+  kv->len = L;
+  if (feat) {
+    feat->next_pos += append;
+    if (W > 0) feat->ring_pmax[slot] = feat->next_pos - 1;
+    feat->step += 1;
+  }
+  return DC_OK;
+}
+
+dc_status dc_score_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,
+                         int32_t budget, float* scores_out, int32_t* kept_out, void* ws,
+                         size_t ws_bytes, void* hip_stream) {
+  dc_status st = check_dims(dims);
+  if (st != DC_OK) return st;
+  if (!kv || !kv->k || !kv->v || !feat || !policy || !policy->params) return DC_ERR_NULL;
+  if (!feat->alpha || !feat->ent_num || !feat->ent_den || !feat->pos || !feat->vnorm)
+    return DC_ERR_NULL;
+  if (policy->n_in != 4 || (policy->n_hidden_layers != 1 && policy->n_hidden_layers != 2))
+    return DC_ERR_UNSUPPORTED;
+  if (policy->hidden[0] < 1 || policy->hidden[0] > 128) return DC_ERR_UNSUPPORTED;
+  if (policy->n_hidden_layers == 2 &&
+      (policy->hidden[0] > 64 || policy->hidden[1] < 1 || policy->hidden[1] > 128))
+    return DC_ERR_UNSUPPORTED;
+  if (budget < 1) return DC_ERR_BUDGET;
+  const int L = kv->len;
+  if (L < 1 || L > dims->capacity) return DC_ERR_SHAPE;
+  if (L > dc::evict_max_len()) return DC_ERR_UNSUPPORTED;
+  if (feat->next_pos < 1) return DC_ERR_SHAPE;
+  const int evict = budget < L;
+  const int B = evict ? budget : L;
+  const size_t need = L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0;
+  if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
+
+  dc::EvictArgs a;
+  memset(&a, 0, sizeof(a));
+  a.k = kv->k;
+  a.v = kv->v;
+  a.alpha = feat->alpha;
+  a.num = feat->ent_num;
+  a.den = feat->ent_den;
+  a.pos = feat->pos;
+  a.vnorm = feat->vnorm;
+  a.params = policy->params;
+  a.scores_out = scores_out;
+  a.kept_out = kept_out;
+  a.cap = dims->capacity;
+  a.units = (int)units_of(dims);
+  a.L = L;
+  a.budget = B;
+  a.T = feat->next_pos;
+  a.nh = policy->n_hidden_layers;
+  a.h1 = policy->hidden[0];
+  a.h2 = policy->n_hidden_layers == 2 ? policy->hidden[1] : 0;
+  a.evict = evict;
+  a.ws_keys = (uint64_t*)ws;
+  if (dc::launch_evict(a, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
+  kv->len = B;
+  return DC_OK;
+}
+
+dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
+                       const void* h_comp, const void* w_lm, float* kl_out, void* ws,
+                       size_t ws_bytes, void* hip_stream) {
+  if (!h_full || !h_comp || !w_lm || !kl_out) return DC_ERR_NULL;
+  if (rows < 1 || hidden < 1 || vocab < 1) return DC_ERR_SHAPE;
+  if (rows > 64 || hidden % 128 || vocab % dc::kl_tile_cols()) return DC_ERR_UNSUPPORTED;
+  const size_t need = kl_bytes(rows, vocab);
+  if (!ws || ws_bytes < need) return DC_ERR_WORKSPACE;
+  dc::KLArgs a;
+  a.h_full = h_full;
+  a.h_comp = h_comp;
+  a.w = w_lm;
+  a.out = kl_out;
+  a.part = (float*)ws;
+  a.rows = rows;
+  a.hidden = hidden;
+  a.vocab = vocab;
+  a.ntiles = vocab / dc::kl_tile_cols();
+  if (dc::launch_kl(a, hip_stream) != 0) return DC_ERR_HIP;
+  return DC_OK;
+}
+
+}  // extern "C"

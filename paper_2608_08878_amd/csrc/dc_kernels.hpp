@@ -1,0 +1,88 @@
+// Internal launch interface between the host C-ABI layer and the HIP kernels.
+#pragma once
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dc {
+
+// Everything one decode-step launch needs (device pointers and host-derived scalars).
+struct DecodeArgs {
+  const void* q;        // [units][G][D]
+  const void* k_new;    // [units][D] or null
+  const void* v_new;
+  void* out;            // [units][G][D]
+  void* k;              // [units][cap][D]
+  void* v;
+  float* alpha;         // feature state, [units][cap]; null for the plain (teacher) step
+  double* num;
+  double* den;
+  int32_t* pos;
+  float* vnorm;
+  void* qring;          // [units][w][G][D]
+  float* qstat;         // [units][w][G][3]
+  int64_t cap;
+  int units;
+  int len_old;          // valid rows before the append
+  int L;                // valid rows after the append
+  int append;
+  float scale;
+  int T;                // tokens seen after the append
+  int window;           // w (0 = unbounded)
+  int slot;             // ring slot written by this step
+  int retire;           // the step leaving the window has a ring record
+  int pmax_ret;         // largest position present at that step
+  // chunked (split) path scratch
+  float* ws_s;          // [units][lmax][G] logits
+  float* ws_r;          // [units][lmax][2] retired contributions
+  float* ws_v;          // [units][lmax] value norms
+  float* ws_part;       // [units][nchunks][3G + G*D] per-chunk softmax partials
+  int lmax;
+  int chunk;
+  int nchunks;
+};
+
+struct EvictArgs {
+  void* k;
+  void* v;
+  float* alpha;
+  double* num;
+  double* den;
+  int32_t* pos;
+  float* vnorm;
+  const float* params;
+  float* scores_out;
+  int32_t* kept_out;
+  int64_t cap;
+  int units;
+  int L;
+  int budget;           // kept rows after the call (min(budget, L))
+  int T;
+  int nh;               // hidden layers (1 or 2)
+  int h1, h2;
+  int evict;            // 1 if rows are removed
+  uint64_t* ws_keys;    // [units][kstride] row keys (long caches only)
+};
+
+struct KLArgs {
+  const void* h_full;
+  const void* h_comp;
+  const void* w;
+  float* out;
+  float* part;          // [rows][ntiles][4]
+  int rows, hidden, vocab, ntiles;
+};
+
+// Launchers return a hipError_t value (0 on success).
+int launch_decode(const DecodeArgs& a, int dtype, int D, int G, bool feat, bool split,
+                  void* stream);
+int launch_feat_init(const DecodeArgs& a, int dtype, int D, int first_pos, void* stream);
+size_t decode_lds_bytes(int L, int G, int D, bool feat);
+bool decode_fits_lds(int L, int G, int D);
+int decode_chunk_rows();
+int launch_evict(const EvictArgs& a, int dtype, int D, void* stream);
+int evict_max_len();
+size_t evict_ws_bytes(int units, int L);
+int launch_kl(const KLArgs& a, void* stream);
+int kl_tile_cols();
+
+}  // namespace dc

@@ -1,0 +1,229 @@
+// Per-step KL reward, KL(P || Q) with P = softmax(h_full W^T), Q = softmax(h_comp W^T)
+// (reward R_t = -KL of Sec. 3.1.4), on gfx950 matrix cores.
+//
+// Numerics.  With delta_v = l_v - l^_v (full minus compressed logit) and
+// mu = E_P[delta],
+//     KL = E_P[delta] + ln E_P[exp(-delta)] = ln E_P[exp(mu - delta)]
+//        = log1p( E_P[ g(mu - delta) ] ),   g(y) = e^y - 1 - y >= 0,
+// since E_P[mu - delta] = 0.  Every term is non-negative, so nothing cancels
+// even when KL is tiny (a direct "sum P (log P - log Q)" in float32 loses the
+// answer to the rounding of the two log-sum-exps), and identical rows give
+// exactly 0.  Q's normaliser never appears.
+//
+// Kernel 1 (one workgroup per 64 vocabulary columns): MFMA 16x16x32 bf16 over
+// the hidden dimension for a 16-row A = [8 full rows; the 8 matching compressed
+// rows], then per (row, tile) the local statistics
+//     m_t = max l,  s_t = sum e^{l - m_t},  mu_t = E_{P_t}[delta],
+//     A_t = E_{P_t}[g(mu_t - delta)]
+// where P_t is P restricted to the tile.  Kernel 2 merges the tiles exactly:
+//     w_t = s_t e^{m_t - M} / S,  mu = sum w_t mu_t,  x_t = mu - mu_t,
+//     KL = log1p( sum_t w_t (g(x_t) + e^{x_t} A_t) ).
+#include "dc_device.hpp"
+#include "dc_kernels.hpp"
+
+#pragma clang fp contract(off)
+
+namespace dc {
+
+constexpr int KL_WAVES = 4;
+constexpr int KL_TILE = 16 * KL_WAVES;   // vocabulary columns per workgroup
+constexpr int KL_KSTEP = 128;            // hidden elements per main-loop iteration
+
+// g(y) = e^y - 1 - y without cancellation.
+__device__ __forceinline__ float gfun(float y) {
+  const float ay = fabsf(y);
+  if (ay < 0.5f) {
+    // y^2/2 * (1 + y/3 (1 + y/4 (1 + y/5 (1 + y/6 (1 + y/7 (1 + y/8 (1 + y/9)))))))
+    float t = 1.0f + y * (1.0f / 9.0f);
+    t = 1.0f + (y * (1.0f / 8.0f)) * t;
+    t = 1.0f + (y * (1.0f / 7.0f)) * t;
+    t = 1.0f + (y * (1.0f / 6.0f)) * t;
+    t = 1.0f + (y * (1.0f / 5.0f)) * t;
+    t = 1.0f + (y * (1.0f / 4.0f)) * t;
+    t = 1.0f + (y * (1.0f / 3.0f)) * t;
+    return (0.5f * y * y) * t;
+  }
+  return expm1f(y) - y;
+}
+
+__device__ __forceinline__ float sum16(float x) {   // over the 16 lanes of a DPP row
+  x += dpp<DPP_XOR1>(x);
+  x += dpp<DPP_XOR2>(x);
+  x += dpp<DPP_HALF_MIRROR>(x);
+  x += dpp<DPP_MIRROR>(x);
+  return x;
+}
+__device__ __forceinline__ float max16(float x) {
+  x = fmaxf(x, dpp<DPP_XOR1>(x));
+  x = fmaxf(x, dpp<DPP_XOR2>(x));
+  x = fmaxf(x, dpp<DPP_HALF_MIRROR>(x));
+  x = fmaxf(x, dpp<DPP_MIRROR>(x));
+  return x;
+}
+
+// grid: (vocab / 64, ceil(rows / 8)); block: 256 threads (4 waves).
+__global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
+  __shared__ float red[KL_WAVES][8][4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int tile = blockIdx.x, rb = blockIdx.y;
+  const int n0 = tile * KL_TILE + wave * 16;      // this wave's 16 columns
+  const int i = lane & 15, kg = lane >> 4;        // MFMA row/col index, k group
+  // A row i: rows 0..7 full, 8..15 compressed, of kl rows rb*8 + (i & 7)
+  const int krow = rb * 8 + (i & 7);
+  const bool avalid = krow < a.rows;
+  const char* arow = (const char*)(i < 8 ? a.h_full : a.h_comp) + (size_t)(avalid ? krow : 0) * a.hidden * 2;
+  const char* brow = (const char*)a.w + (size_t)(n0 + i) * a.hidden * 2;
+  f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  // lane's k range within an iteration: [32*kg, 32*kg + 32) = 4 MFMA slices of 8
+  for (int k0 = 0; k0 < a.hidden; k0 += KL_KSTEP) {
+    const int off = (k0 + 32 * kg) * 2;
+    uint4 av[4], bv[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      av[t] = avalid ? ldg16(arow + off + 16 * t) : make_uint4(0, 0, 0, 0);
+      bv[t] = ldg16_nt(brow + off + 16 * t);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av[t]),
+                                                    __builtin_bit_cast(bf16x8_t, bv[t]), acc, 0, 0, 0);
+  }
+  // lane holds C[4*kg + r][i] for r < 4: kg 0,1 full rows 0..7, kg 2,3 compressed rows 0..7
+  float lf[4], lc[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float x = acc[r];
+    const float y = __shfl_xor(x, 32);
+    lf[r] = x;   // meaningful in lanes 0..31
+    lc[r] = y;
+  }
+  // per kl row rho = 4*kg + r (lanes 0..31): statistics over this workgroup's 64 columns
+  float m[4], s[4], mu[4], At[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) m[r] = max16(lf[r]);
+  if (lane < 32 && i == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][0] = m[r];
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int rho = 4 * (kg & 1) + r;
+    float M = red[0][rho][0];
+    for (int w = 1; w < KL_WAVES; ++w) M = fmaxf(M, red[w][rho][0]);
+    m[r] = M;
+    const float p = __expf(lf[r] - M);
+    s[r] = sum16(p);
+    mu[r] = sum16(p * (lf[r] - lc[r]));
+  }
+  if (lane < 32 && i == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      red[wave][4 * kg + r][1] = s[r];
+      red[wave][4 * kg + r][2] = mu[r];
+    }
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int rho = 4 * (kg & 1) + r;
+    float S = 0.0f, T = 0.0f;
+    for (int w = 0; w < KL_WAVES; ++w) {
+      S = S + red[w][rho][1];
+      T = T + red[w][rho][2];
+    }
+    s[r] = S;
+    mu[r] = T / S;
+    const float p = __expf(lf[r] - m[r]);
+    At[r] = sum16(p * gfun(mu[r] - (lf[r] - lc[r])));
+  }
+  if (lane < 32 && i == 0)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][3] = At[r];
+  __syncthreads();
+  if (wave == 0 && lane < 32 && i == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rho = 4 * kg + r;
+      const int row = rb * 8 + rho;
+      if (row < a.rows) {
+        float A = 0.0f;
+        for (int w = 0; w < KL_WAVES; ++w) A = A + red[w][rho][3];
+        float* p = a.part + ((size_t)row * a.ntiles + tile) * 4;
+        p[0] = m[r];
+        p[1] = s[r];
+        p[2] = mu[r];
+        p[3] = A / s[r];
+      }
+    }
+  }
+}
+
+// One workgroup per row: merge the tile statistics (fixed reduction order).
+__global__ void __launch_bounds__(256) kl_merge_kernel(KLArgs a) {
+  __shared__ float red[256];
+  __shared__ float bc[2];
+  const int row = blockIdx.x, t = threadIdx.x;
+  const float* P = a.part + (size_t)row * a.ntiles * 4;
+  float M = NEG_BIG;
+  for (int j = t; j < a.ntiles; j += 256) M = fmaxf(M, P[4 * j]);
+  red[t] = M;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = fmaxf(red[t], red[t + w]);
+    __syncthreads();
+  }
+  M = red[0];
+  __syncthreads();
+  float S = 0.0f, U = 0.0f;
+  for (int j = t; j < a.ntiles; j += 256) {
+    const float w = P[4 * j + 1] * __expf(P[4 * j] - M);
+    S = S + w;
+    U = U + w * P[4 * j + 2];
+  }
+  red[t] = S;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = red[t] + red[t + w];
+    __syncthreads();
+  }
+  S = red[0];
+  __syncthreads();
+  red[t] = U;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = red[t] + red[t + w];
+    __syncthreads();
+  }
+  if (t == 0) {
+    bc[0] = S;
+    bc[1] = red[0] / S;
+  }
+  __syncthreads();
+  S = bc[0];
+  const float mu = bc[1];
+  float acc = 0.0f;
+  for (int j = t; j < a.ntiles; j += 256) {
+    const float w = P[4 * j + 1] * __expf(P[4 * j] - M) / S;
+    const float x = mu - P[4 * j + 2];
+    acc = acc + w * (gfun(x) + __expf(x) * P[4 * j + 3]);
+  }
+  __syncthreads();
+  red[t] = acc;
+  __syncthreads();
+  for (int w = 128; w > 0; w >>= 1) {
+    if (t < w) red[t] = red[t] + red[t + w];
+    __syncthreads();
+  }
+  if (t == 0) a.out[row] = log1pf(red[0]);
+}
+
+int kl_tile_cols() { return KL_TILE; }
+
+int launch_kl(const KLArgs& a, void* stream) {
+  hipStream_t s = (hipStream_t)stream;
+  dim3 g1(a.vocab / KL_TILE, (a.rows + 7) / 8);
+  hipLaunchKernelGGL(kl_tile_kernel, g1, dim3(64 * KL_WAVES), 0, s, a);
+  hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
+  return (int)hipGetLastError();
+}
+
+}  // namespace dc

@@ -150,6 +150,14 @@ def det_exp(x):
 def uniform(seed: int, stream: int, step: int, idx) -> np.ndarray:
     """Uniform (0,1) binary64 values for element indices ``idx``."""
     idx = np.asarray(idx, np.uint64)
+    if idx.size >= FAST_MIN and _fast() is not None:
+        return _fast_values(idx, seed, stream, step, 1)
+    return uniform_np(seed, stream, step, idx)
+
+
+def uniform_np(seed: int, stream: int, step: int, idx) -> np.ndarray:
+    """numpy evaluation of ``uniform`` (the readable definition)."""
+    idx = np.asarray(idx, np.uint64)
     w = _words(seed, stream, step, idx >> np.uint64(2))
     lane = (idx & np.uint64(3)).astype(np.int64)
     x = np.select([lane == 0, lane == 1, lane == 2], [w[0], w[1], w[2]], w[3])
@@ -158,6 +166,14 @@ def uniform(seed: int, stream: int, step: int, idx) -> np.ndarray:
 
 def normal(seed: int, stream: int, step: int, idx) -> np.ndarray:
     """Standard normal binary64 values for element indices ``idx``."""
+    idx = np.asarray(idx, np.uint64)
+    if idx.size >= FAST_MIN and _fast() is not None:
+        return _fast_values(idx, seed, stream, step, 0)
+    return normal_np(seed, stream, step, idx)
+
+
+def normal_np(seed: int, stream: int, step: int, idx) -> np.ndarray:
+    """numpy evaluation of ``normal`` (the readable definition)."""
     idx = np.asarray(idx, np.uint64)
     w = _words(seed, stream, step, idx >> np.uint64(2))
     pair = ((idx >> np.uint64(1)) & np.uint64(1)).astype(bool)
@@ -194,3 +210,45 @@ def narrow(x, dtype: str) -> np.ndarray:
     if dtype == "bf16":
         return bf16_bits_to_f32(f32_to_bf16_bits(f))
     raise ValueError(dtype)
+
+
+# ---------------------------------------------------------------------------
+# Bulk evaluation through the host build of the generator library (the same
+# binary64 operations compiled as C++ for the CPU); tests check it against the
+# numpy evaluation above, element by element.
+FAST_MIN = 1 << 14
+_FAST = None
+_FAST_TRIED = False
+
+
+def _fast():
+    global _FAST, _FAST_TRIED
+    if not _FAST_TRIED:
+        _FAST_TRIED = True
+        import ctypes
+        import os
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libdcsynth.so")
+        if os.path.exists(path):
+            try:
+                L = ctypes.CDLL(path)
+                L.synth_cpu_values.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                               ctypes.c_uint64, ctypes.c_int, ctypes.c_int,
+                                               ctypes.c_int, ctypes.c_int]
+                L.synth_cpu_values.restype = None
+                _FAST = L
+            except OSError:
+                _FAST = None
+    return _FAST
+
+
+def _threads() -> int:
+    import os
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _fast_values(idx, seed, stream, step, kind):
+    idx = np.ascontiguousarray(idx, np.uint64)
+    out = np.empty(idx.shape, np.float64)
+    _fast().synth_cpu_values(out.ctypes.data, idx.ctypes.data, idx.size, seed, stream, step, kind,
+                             _threads())
+    return out
