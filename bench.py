@@ -95,8 +95,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=8)
     ap.add_argument("--config", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-units", type=int, default=16)
-    ap.add_argument("--cpu-steps", type=int, default=48)
+    ap.add_argument("--cpu-units", type=int, default=64)
+    ap.add_argument("--cpu-steps", type=int, default=96)
     ap.add_argument("--calib-copy-mib", type=int, default=1024,
                     help="size of the plain copy kernel run first (counter calibration)")
     args = ap.parse_args()
@@ -150,57 +150,47 @@ def main():
     log(f"setup {time.time() - t0:.1f}s: {U} units, cache {buf.k.numel() * elt * 2 / 1e9:.1f} GB")
 
     # step 0: compression n0+1 -> budget (reported separately)
-    e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+    e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
     e0.record()
-    buf.decode_step(Q[0], KN[0], VN[0], out)
+    buf.decode_evict(pol, wl.budget, Q[0], KN[0], VN[0], out)
     e1.record()
-    buf.score_evict(pol, wl.budget)
-    e2.record()
     torch.cuda.synchronize()
-    first = (e0.elapsed_time(e1), e1.elapsed_time(e2))
-    log(f"step 0 (L={wl.n0 + 1} -> {wl.budget}): decode {first[0]:.3f} ms, evict {first[1]:.3f} ms")
+    first_ms = e0.elapsed_time(e1)
+    log(f"step 0 (L={wl.n0 + 1} -> {wl.budget}): {first_ms:.3f} ms")
 
     for t in range(1, 1 + args.warmup):
-        buf.decode_step(Q[t], KN[t], VN[t], out)
-        buf.score_evict(pol, wl.budget)
+        buf.decode_evict(pol, wl.budget, Q[t], KN[t], VN[t], out)
     torch.cuda.synchronize()
 
     L_steady = buf.kv.len + 1
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
-           torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
         t = 1 + args.warmup + i
-        a, b, c = ev[i]
+        a, b = ev[i]
         a.record()
-        buf.decode_step(Q[t], KN[t], VN[t], out)
+        buf.decode_evict(pol, wl.budget, Q[t], KN[t], VN[t], out)
         b.record()
-        buf.score_evict(pol, wl.budget)
-        c.record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
-    dec_ms = float(np.mean([a.elapsed_time(b) for a, b, _ in ev]))
-    evi_ms = float(np.mean([b.elapsed_time(c) for _, b, c in ev]))
-    gpu_ms = float(np.sum([a.elapsed_time(c) for a, _, c in ev])) / args.steps
+    step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     ms_per_step = wall * 1e3 / args.steps
-    log(f"steady: {ms_per_step:.3f} ms/step (events {gpu_ms:.3f}); decode {dec_ms:.3f} ms, "
-        f"evict {evi_ms:.3f} ms")
+    log(f"steady: {ms_per_step:.3f} ms/step wall; fused step kernel {step_ms:.3f} ms (events)")
 
     # moved rows per steady step (one untimed extra step with the slot map)
     kept = torch.empty((U, wl.budget), dtype=torch.int32, device=dev)
     t = nsteps - 1
-    buf.decode_step(Q[t], KN[t], VN[t], out)
-    buf.score_evict(pol, wl.budget, kept_out=kept)
+    buf.decode_evict(pol, wl.budget, Q[t], KN[t], VN[t], out, kept_out=kept)
     torch.cuda.synchronize()
     moved = int((kept != torch.arange(wl.budget, device=dev, dtype=torch.int32)[None, :]).sum())
 
     retire = True
-    dec_bytes = decode_alg_bytes(U, L_steady, G, D, elt, 1, retire)
-    evi_bytes = evict_alg_bytes(U, L_steady, moved, D, elt)
+    step_bytes = decode_alg_bytes(U, L_steady, G, D, elt, 1, retire) + moved * 2 * (2 * D * elt + 28)
     kvb = kv_bytes(U, L_steady, D, elt, moved)
     steps_per_s = 1e3 / ms_per_step
-    dec_gbps = dec_bytes / (dec_ms * 1e-3) / 1e9
+    step_gbps = step_bytes / (step_ms * 1e-3) / 1e9
     result = {
         "metric": METRIC,
         "value": round(steps_per_s, 3),
@@ -221,15 +211,13 @@ def main():
         "kv_gbps": round(kvb / (ms_per_step * 1e-3) / 1e9, 1),
         "kv_frac_of_8TBps": round(kvb / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
         "kv_bytes_per_step": kvb,
-        "all_bytes_gbps": round((dec_bytes + evi_bytes) / (ms_per_step * 1e-3) / 1e9, 1),
         "moved_rows_per_step": moved,
-        "decode_ms": round(dec_ms, 4),
-        "evict_ms": round(evi_ms, 4),
-        "first_step_ms": {"decode": round(first[0], 3), "evict": round(first[1], 3)},
-        "roofline": {"bound": "hbm", "kernel": "decode_unit_kernel (attention + features)",
-                     "achieved": round(dec_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(dec_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "alg_bytes_per_launch": dec_bytes},
+        "step_kernel_ms": round(step_ms, 4),
+        "first_step_ms": round(first_ms, 3),
+        "roofline": {"bound": "hbm", "kernel": "step_unit_kernel (attention + features + score + select + compact)",
+                     "achieved": round(step_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(step_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "alg_bytes_per_launch": step_bytes},
     }
     if not args.no_cpu_baseline:
         del buf, Q, KN, VN

@@ -99,7 +99,8 @@ typedef struct {
   double  *ent_num;    /* [units][capacity] */
   double  *ent_den;    /* [units][capacity] */
   int32_t *pos;        /* [units][capacity] absolute position of the token in the slot */
-  float   *vnorm;      /* [units][capacity] ||v_i||_2, rewritten by every decode step */
+  float   *vnorm;      /* [units][capacity] ||v_i||_2, set when the row is appended (or by
+                          dc_feat_init) and carried with the row */
   void    *qring;      /* [units][w][G][head_dim], dtype: queries of the last w steps */
   float   *qstat;      /* [units][w][G][3]: (m, 1/l, H) of each query, where
                           m = max_i s_i, l = sum_i exp(s_i - m), s_i = scale * q.k_i */
@@ -171,6 +172,21 @@ dc_status dc_decode_step(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const vo
 dc_status dc_score_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const dc_policy *policy,
                          int32_t budget, float *scores_out, int32_t *kept_out, void *ws,
                          size_t ws_bytes, void *hip_stream);
+
+/* One whole decode step (Algorithm 1): dc_decode_step followed by
+ * dc_score_evict with the same policy, budget and outputs.  Results and host
+ * bookkeeping are bit-identical to the two calls in sequence; where the cache
+ * fits on chip (bf16, up to about 5000 rows per unit) it runs as a single
+ * launch that streams K/V once and compacts before it exits.
+ *   scores_out  [units][len + appended] float32 or NULL (pre-eviction slot order)
+ *   kept_out    [units][min(budget, len + appended)] int32 or NULL
+ * Errors: those of dc_decode_step and dc_score_evict (feat must not be NULL);
+ * nothing is enqueued unless both validate.  Workspace: dc_workspace_bytes for
+ * the post-append length. */
+dc_status dc_decode_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const dc_policy *policy,
+                          int32_t budget, const void *q, const void *k_new, const void *v_new,
+                          void *out, float *scores_out, int32_t *kept_out, void *ws,
+                          size_t ws_bytes, void *hip_stream);
 
 /* Per-step KL reward (Sec. 3.1.4): for each row r,
  *   kl_out[r] = KL(P || Q) = sum_v P_v (ln P_v - ln Q_v)   (nats),

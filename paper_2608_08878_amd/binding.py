@@ -41,7 +41,7 @@ class dc_policy(ctypes.Structure):
 
 
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
-           "dc_kl_reward", "dc_status_str")
+           "dc_decode_evict", "dc_kl_reward", "dc_status_str")
 
 _lib = None
 
@@ -67,6 +67,10 @@ def lib() -> ctypes.CDLL:
                                      ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
                                      vp, vp, vp, sz, vp]
         L.dc_score_evict.restype = ctypes.c_int
+        L.dc_decode_evict.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                      ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
+                                      vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.dc_decode_evict.restype = ctypes.c_int
         L.dc_kl_reward.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
         L.dc_kl_reward.restype = ctypes.c_int
         L.dc_status_str.argtypes = [ctypes.c_int]
@@ -122,6 +126,13 @@ def dc_score_evict(dims, kv, feat, policy, budget: int, scores_out=None, kept_ou
     _check(lib().dc_score_evict(ctypes.byref(dims), ctypes.byref(kv), _ref(feat),
                                 _ref(policy), budget, _ptr(scores_out), _ptr(kept_out),
                                 _ptr(ws), ws_bytes, stream))
+
+
+def dc_decode_evict(dims, kv, feat, policy, budget: int, q, k_new, v_new, out, scores_out=None,
+                    kept_out=None, ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_decode_evict(ctypes.byref(dims), ctypes.byref(kv), _ref(feat), _ref(policy),
+                                 budget, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
+                                 _ptr(scores_out), _ptr(kept_out), _ptr(ws), ws_bytes, stream))
 
 
 def dc_kl_reward(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_out, ws=None,

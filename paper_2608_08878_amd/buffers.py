@@ -72,6 +72,14 @@ class DecodeBuffers:
                          out, self.ws, self.ws_bytes, stream_handle(stream))
         return out
 
+    def decode_evict(self, policy, budget, q, k_new=None, v_new=None, out=None, scores_out=None,
+                     kept_out=None, stream=None):
+        if out is None:
+            out = torch.empty_like(q)
+        B.dc_decode_evict(self.dims, self.kv, self.feat, policy, budget, q, k_new, v_new, out,
+                          scores_out, kept_out, self.ws, self.ws_bytes, stream_handle(stream))
+        return out
+
     def score_evict(self, policy, budget, scores_out=None, kept_out=None, stream=None):
         B.dc_score_evict(self.dims, self.kv, self.feat, policy, budget, scores_out, kept_out,
                          self.ws, self.ws_bytes, stream_handle(stream))

@@ -118,9 +118,14 @@ dc_status dc_feat_init(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, int3
   return DC_OK;
 }
 
-dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const void* q,
-                         const void* k_new, const void* v_new, void* out, void* ws,
-                         size_t ws_bytes, void* hip_stream) {
+}  // extern "C"
+
+namespace {
+
+// Validate a decode step and fill its launch arguments; no side effects.
+dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat, const void* q,
+                      const void* k_new, const void* v_new, void* out, void* ws, size_t ws_bytes,
+                      dc::DecodeArgs& a, bool& split, size_t& need) {
   dc_status st = check_dims(dims);
   if (st != DC_OK) return st;
   if (!kv || !kv->k || !kv->v || !q || !out) return DC_ERR_NULL;
@@ -138,13 +143,15 @@ dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const vo
   if (append && len + 1 > dims->capacity) return DC_ERR_CAPACITY;
   if (!append && len == 0) return DC_ERR_SHAPE;
   const int L = len + append;
-  const bool split = use_split(dims, L, feat != nullptr);
-  const size_t need = split ? split_bytes(dims, L) : 0;
-  if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
-
   const int G = group_of(dims), D = dims->head_dim;
   const int U = (int)units_of(dims);
-  dc::DecodeArgs a;
+  if (dims->dtype == DC_BF16)
+    split = !dc::step_fits(L, G, D, feat != nullptr, 0) || (U < 128 && L > 2 * dc::step_chunk_rows());
+  else
+    split = use_split(dims, L, feat != nullptr);
+  need = split ? split_bytes(dims, L) : 0;
+  if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
+
   memset(&a, 0, sizeof(a));
   a.q = q;
   a.k_new = k_new;
@@ -158,7 +165,6 @@ dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const vo
   a.L = L;
   a.append = append;
   a.scale = scale_of(dims);
-  int slot = 0;
   if (feat) {
     a.alpha = feat->alpha;
     a.num = feat->ent_num;
@@ -170,10 +176,9 @@ dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const vo
     a.T = feat->next_pos + append;
     a.window = W;
     if (W > 0) {
-      slot = feat->step % W;
-      a.slot = slot;
+      a.slot = feat->step % W;
       a.retire = feat->step >= W;
-      a.pmax_ret = a.retire ? feat->ring_pmax[slot] : 0;
+      a.pmax_ret = a.retire ? feat->ring_pmax[a.slot] : 0;
     }
   }
   if (split) {
@@ -187,20 +192,30 @@ dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const vo
     a.ws_v = base + rows * (G + 2);
     a.ws_part = (float*)((char*)ws + align256(rows * (G + 3) * sizeof(float)));
   }
-  if (dc::launch_decode(a, dims->dtype, D, G, feat != nullptr, split, hip_stream) != 0)
-    return DC_ERR_HIP;
-  kv->len = L;
-  if (feat) {
-    feat->next_pos += append;
-    if (W > 0) feat->ring_pmax[slot] = feat->next_pos - 1;
-    feat->step += 1;
-  }
   return DC_OK;
 }
 
-dc_status dc_score_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,
-                         int32_t budget, float* scores_out, int32_t* kept_out, void* ws,
-                         size_t ws_bytes, void* hip_stream) {
+dc_status launch_decode_any(const dc_dims* dims, const dc::DecodeArgs& a, bool feat, bool split,
+                            void* stream) {
+  const int G = group_of(dims), D = dims->head_dim;
+  const int rc = dims->dtype == DC_BF16 ? dc::launch_step(a, nullptr, D, G, feat, split, stream)
+                                        : dc::launch_decode(a, dims->dtype, D, G, feat, split, stream);
+  return rc == 0 ? DC_OK : DC_ERR_HIP;
+}
+
+void commit_decode(dc_kv* kv, dc_feat* feat, const dc::DecodeArgs& a, int W) {
+  kv->len = a.L;
+  if (feat) {
+    feat->next_pos += a.append;
+    if (W > 0) feat->ring_pmax[a.slot] = feat->next_pos - 1;
+    feat->step += 1;
+  }
+}
+
+// Validate a score/evict call on a cache of L rows with T tokens seen.
+dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
+                     const dc_policy* policy, int32_t budget, float* scores_out, int32_t* kept_out,
+                     void* ws, size_t ws_bytes, int L, int T, dc::EvictArgs& e, size_t& need) {
   dc_status st = check_dims(dims);
   if (st != DC_OK) return st;
   if (!kv || !kv->k || !kv->v || !feat || !policy || !policy->params) return DC_ERR_NULL;
@@ -213,39 +228,94 @@ dc_status dc_score_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc
       (policy->hidden[0] > 64 || policy->hidden[1] < 1 || policy->hidden[1] > 128))
     return DC_ERR_UNSUPPORTED;
   if (budget < 1) return DC_ERR_BUDGET;
-  const int L = kv->len;
   if (L < 1 || L > dims->capacity) return DC_ERR_SHAPE;
   if (L > dc::evict_max_len()) return DC_ERR_UNSUPPORTED;
-  if (feat->next_pos < 1) return DC_ERR_SHAPE;
+  if (T < 1) return DC_ERR_SHAPE;
   const int evict = budget < L;
-  const int B = evict ? budget : L;
-  const size_t need = L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0;
+  need = L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0;
   if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
+  memset(&e, 0, sizeof(e));
+  e.k = kv->k;
+  e.v = kv->v;
+  e.alpha = feat->alpha;
+  e.num = feat->ent_num;
+  e.den = feat->ent_den;
+  e.pos = feat->pos;
+  e.vnorm = feat->vnorm;
+  e.params = policy->params;
+  e.scores_out = scores_out;
+  e.kept_out = kept_out;
+  e.cap = dims->capacity;
+  e.units = (int)units_of(dims);
+  e.L = L;
+  e.budget = evict ? budget : L;
+  e.T = T;
+  e.nh = policy->n_hidden_layers;
+  e.h1 = policy->hidden[0];
+  e.h2 = policy->n_hidden_layers == 2 ? policy->hidden[1] : 0;
+  e.evict = evict;
+  e.ws_keys = (uint64_t*)ws;
+  return DC_OK;
+}
 
-  dc::EvictArgs a;
-  memset(&a, 0, sizeof(a));
-  a.k = kv->k;
-  a.v = kv->v;
-  a.alpha = feat->alpha;
-  a.num = feat->ent_num;
-  a.den = feat->ent_den;
-  a.pos = feat->pos;
-  a.vnorm = feat->vnorm;
-  a.params = policy->params;
-  a.scores_out = scores_out;
-  a.kept_out = kept_out;
-  a.cap = dims->capacity;
-  a.units = (int)units_of(dims);
-  a.L = L;
-  a.budget = B;
-  a.T = feat->next_pos;
-  a.nh = policy->n_hidden_layers;
-  a.h1 = policy->hidden[0];
-  a.h2 = policy->n_hidden_layers == 2 ? policy->hidden[1] : 0;
-  a.evict = evict;
-  a.ws_keys = (uint64_t*)ws;
-  if (dc::launch_evict(a, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
-  kv->len = B;
+}  // namespace
+
+extern "C" {
+
+dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const void* q,
+                         const void* k_new, const void* v_new, void* out, void* ws,
+                         size_t ws_bytes, void* hip_stream) {
+  dc::DecodeArgs a;
+  bool split = false;
+  size_t need = 0;
+  dc_status st = prep_decode(dims, kv, feat, q, k_new, v_new, out, ws, ws_bytes, a, split, need);
+  if (st != DC_OK) return st;
+  st = launch_decode_any(dims, a, feat != nullptr, split, hip_stream);
+  if (st != DC_OK) return st;
+  commit_decode(kv, feat, a, dims->ent_window);
+  return DC_OK;
+}
+
+dc_status dc_score_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,
+                         int32_t budget, float* scores_out, int32_t* kept_out, void* ws,
+                         size_t ws_bytes, void* hip_stream) {
+  if (!kv || !feat) return DC_ERR_NULL;
+  dc::EvictArgs e;
+  size_t need = 0;
+  dc_status st = prep_evict(dims, kv, feat, policy, budget, scores_out, kept_out, ws, ws_bytes,
+                            kv->len, feat->next_pos, e, need);
+  if (st != DC_OK) return st;
+  if (dc::launch_evict(e, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
+  kv->len = e.budget;
+  return DC_OK;
+}
+
+dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,
+                          int32_t budget, const void* q, const void* k_new, const void* v_new,
+                          void* out, float* scores_out, int32_t* kept_out, void* ws,
+                          size_t ws_bytes, void* hip_stream) {
+  if (!feat) return DC_ERR_NULL;
+  dc::DecodeArgs a;
+  bool split = false;
+  size_t need_d = 0, need_e = 0;
+  dc_status st = prep_decode(dims, kv, feat, q, k_new, v_new, out, ws, ws_bytes, a, split, need_d);
+  if (st != DC_OK) return st;
+  dc::EvictArgs e;
+  st = prep_evict(dims, kv, feat, policy, budget, scores_out, kept_out, ws, ws_bytes, a.L, a.T, e,
+                  need_e);
+  if (st != DC_OK) return st;
+  const int G = group_of(dims), D = dims->head_dim;
+  const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
+  const bool fused = dims->dtype == DC_BF16 && !split && dc::step_fits(a.L, G, D, true, nm);
+  if (fused) {
+    if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
+  } else {
+    st = launch_decode_any(dims, a, true, split, hip_stream);
+    if (st != DC_OK) return st;
+    if (dc::launch_evict(e, dims->dtype, D, hip_stream) != 0) return DC_ERR_HIP;
+  }
+  commit_decode(kv, feat, a, dims->ent_window);
+  kv->len = e.budget;
   return DC_OK;
 }
 

@@ -195,8 +195,9 @@ __device__ __forceinline__ void wave_combine(Acc<G, EPL>& acc) {
 }
 
 // Combine the waves of a workgroup.  On return every thread holds the final
-// (m, l, u) per head in fin, and each wave's rescale factor cw[j]; stat is LDS
-// scratch of NWAVE * 3G floats.
+// (m, l, u) per head in fm/fl/fu, and its wave's rescale factor cw[j]; stat is
+// LDS scratch of NWAVE * 3G + 3G floats.  A few threads merge the per-wave
+// partials (fixed order) and broadcast the result through LDS.
 template <int G>
 __device__ __forceinline__ void block_stats(float (&m)[G], float (&l)[G], float (&u)[G],
                                             float* stat, float (&fm)[G], float (&fl)[G],
@@ -211,18 +212,25 @@ __device__ __forceinline__ void block_stats(float (&m)[G], float (&l)[G], float 
     }
   }
   __syncthreads();
-#pragma unroll
-  for (int j = 0; j < G; ++j) {
+  if (threadIdx.x < G) {
+    const int j = threadIdx.x;
     float M = stat[j * 3], Lx = stat[j * 3 + 1], U = stat[j * 3 + 2];
     for (int w = 1; w < NWAVE; ++w) {
       float c1, c2;
       merge_stats(M, Lx, U, stat[(w * G + j) * 3], stat[(w * G + j) * 3 + 1],
                   stat[(w * G + j) * 3 + 2], c1, c2);
     }
-    fm[j] = M;
-    fl[j] = Lx;
-    fu[j] = U;
-    cw[j] = __builtin_amdgcn_exp2f((m[j] - M) * LOG2E);
+    stat[NWAVE * 3 * G + 3 * j] = M;
+    stat[NWAVE * 3 * G + 3 * j + 1] = Lx;
+    stat[NWAVE * 3 * G + 3 * j + 2] = U;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    fm[j] = stat[NWAVE * 3 * G + 3 * j];
+    fl[j] = stat[NWAVE * 3 * G + 3 * j + 1];
+    fu[j] = stat[NWAVE * 3 * G + 3 * j + 2];
+    cw[j] = __builtin_amdgcn_exp2f((m[j] - fm[j]) * LOG2E);
   }
 }
 
@@ -329,8 +337,8 @@ __global__ void __launch_bounds__(NTH) decode_unit_kernel(DecodeArgs a) {
   using Q = Geo<DTYPE, D, G>;
   extern __shared__ float lds[];
   const int u = blockIdx.x;
-  float* stat = lds;                          // NWAVE * 3G
-  float* sbuf = lds + NWAVE * 3 * G;          // L * G
+  float* stat = lds;                          // NWAVE * 3G + 3G
+  float* sbuf = lds + NWAVE * 3 * G + 3 * G;  // L * G
   float* rbuf = sbuf + (FEAT ? a.L * G : 0);  // L * 2
   float* vbuf = rbuf + (FEAT ? a.L * 2 : 0);  // L
   float* obuf = sbuf;                         // NWAVE * G * D, after the feature pass
@@ -373,9 +381,9 @@ __global__ void __launch_bounds__(NTH) decode_unit_kernel(DecodeArgs a) {
 template <int DTYPE, int D, int G, bool FEAT>
 __global__ void __launch_bounds__(NTH) decode_split1_kernel(DecodeArgs a) {
   using Q = Geo<DTYPE, D, G>;
-  __shared__ float lds[NWAVE * 3 * G + NWAVE * G * D];
+  __shared__ float lds[NWAVE * 3 * G + 3 * G + NWAVE * G * D];
   float* stat = lds;
-  float* obuf = lds + NWAVE * 3 * G;
+  float* obuf = lds + NWAVE * 3 * G + 3 * G;
   const int c = blockIdx.x, u = blockIdx.y;
   const int r0 = c * a.chunk, r1 = min(a.L, r0 + a.chunk);
   if (c == 0 && a.append) write_append<DTYPE, D>(a, u);
@@ -486,7 +494,7 @@ __global__ void __launch_bounds__(256) feat_init_kernel(DecodeArgs a, int first_
 
 // ---------------------------------------------------------------- dispatch
 size_t decode_lds_bytes(int L, int G, int D, bool feat) {
-  size_t stat = (size_t)NWAVE * 3 * G;
+  size_t stat = (size_t)NWAVE * 3 * G + 3 * G;
   size_t rows = feat ? (size_t)L * (G + 3) : 0;
   size_t ob = (size_t)NWAVE * G * D;
   return (stat + (rows > ob ? rows : ob)) * sizeof(float);

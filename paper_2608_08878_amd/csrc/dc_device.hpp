@@ -92,19 +92,34 @@ __device__ __forceinline__ float attn_weight(float s, float m, float invl) {
   return __builtin_amdgcn_exp2f((s - m) * LOG2E) * invl;
 }
 
-// Feature contributions of one row for one step:
-//   cz = sum_j a_j,  cn = sum_j a_j H_j   (j = 0..G-1 in order).
+// Feature contributions of one row for one step from its weights a_j:
+//   cz = sum_j a_j,  cn = sum_j a_j H_j,
+// summed in order within blocks of four heads, blocks added in order.
 template <int G>
-__device__ __forceinline__ void row_contrib(const float* s, const float* m, const float* invl,
-                                            const float* H, float& cz, float& cn) {
+__device__ __forceinline__ void contrib_from_weights(const float* a, const float* H, float& cz,
+                                                     float& cn) {
   cz = 0.0f;
   cn = 0.0f;
 #pragma unroll
-  for (int j = 0; j < G; ++j) {
-    float a = attn_weight(s[j], m[j], invl[j]);
-    cz = cz + a;
-    cn = cn + a * H[j];
+  for (int b = 0; b < G; b += 4) {
+    float z = 0.0f, n = 0.0f;
+#pragma unroll
+    for (int j = b; j < (b + 4 < G ? b + 4 : G); ++j) {
+      z = z + a[j];
+      n = n + a[j] * H[j];
+    }
+    cz = cz + z;
+    cn = cn + n;
   }
+}
+
+template <int G>
+__device__ __forceinline__ void row_contrib(const float* s, const float* m, const float* invl,
+                                            const float* H, float& cz, float& cn) {
+  float a[G];
+#pragma unroll
+  for (int j = 0; j < G; ++j) a[j] = attn_weight(s[j], m[j], invl[j]);
+  contrib_from_weights<G>(a, H, cz, cn);
 }
 
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }

@@ -83,6 +83,11 @@ int launch_evict(const EvictArgs& a, int dtype, int D, void* stream);
 int evict_max_len();
 size_t evict_ws_bytes(int units, int L);
 int launch_kl(const KLArgs& a, void* stream);
+// bf16 matrix-core step (dc_step.hip); e != nullptr fuses scoring and eviction.
+int launch_step(const DecodeArgs& a, const EvictArgs* e, int D, int G, bool feat, bool chunked,
+                void* stream);
+bool step_fits(int L, int G, int D, bool feat, int nmoves);
+int step_chunk_rows();
 int kl_tile_cols();
 
 }  // namespace dc

@@ -1,0 +1,356 @@
+// Scoring, top-B selection and hole-filling compaction shared by the
+// stand-alone score/evict kernels and the fused decode+evict kernel.
+#pragma once
+#include "dc_device.hpp"
+#include "dc_kernels.hpp"
+
+namespace dc {
+
+constexpr int ENT = 1024;            // threads of the per-unit select workgroup
+constexpr int ENW = ENT / 64;
+constexpr int REG_KPT = 8;           // rows per thread kept in registers (L <= 8192)
+constexpr int MAX_LEN = 40960;
+constexpr int MAX_H1_2L = 64;        // first hidden width supported with two hidden layers
+
+__device__ __forceinline__ uint32_t score_key(float s) {
+  uint32_t b = __float_as_uint(s);
+  if ((b & 0x7F800000u) == 0x7F800000u && (b & 0x007FFFFFu)) return 0u;  // NaN ranks lowest
+  if (b == 0x80000000u) b = 0u;                                           // -0 -> +0
+  return (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+}
+
+__device__ __forceinline__ uint64_t row_key(float s, int32_t pos) {
+  return ((uint64_t)score_key(s) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)pos);
+}
+
+// Feature vector x = [alpha, ||v||, H = num/den (0 if den = 0), pos / T].
+__device__ __forceinline__ void make_features(float alpha, float vnorm, double num, double den,
+                                              int32_t p, float invT, float x[4]) {
+  x[0] = alpha;
+  x[1] = vnorm;
+  x[2] = den > 0.0 ? (float)(num / den) : 0.0f;
+  x[3] = (float)p * invT;
+}
+
+__device__ __forceinline__ void load_features(const EvictArgs& a, size_t gi, float invT, float x[4],
+                                              int32_t& p) {
+  p = a.pos[gi];
+  make_features(a.alpha[gi], a.vnorm[gi], a.num[gi], a.den[gi], p, invT, x);
+}
+
+// s = f_phi(x), float32, fixed evaluation order.
+__device__ __forceinline__ float mlp1(const float* __restrict__ P, int h1, const float x[4]) {
+  const float* W1 = P;
+  const float* b1 = P + 4 * h1;
+  const float* wo = b1 + h1;
+  float out = wo[h1];
+  for (int h = 0; h < h1; ++h) {
+    float z = b1[h];
+    z = __builtin_fmaf(W1[4 * h + 0], x[0], z);
+    z = __builtin_fmaf(W1[4 * h + 1], x[1], z);
+    z = __builtin_fmaf(W1[4 * h + 2], x[2], z);
+    z = __builtin_fmaf(W1[4 * h + 3], x[3], z);
+    out = __builtin_fmaf(wo[h], fmaxf(z, 0.0f), out);
+  }
+  return out;
+}
+
+__device__ __forceinline__ float mlp2(const float* __restrict__ P, int h1, int h2, const float x[4]) {
+  const float* W1 = P;
+  const float* b1 = P + 4 * h1;
+  const float* W2 = b1 + h1;
+  const float* b2 = W2 + h2 * h1;
+  const float* wo = b2 + h2;
+  float hv[MAX_H1_2L];
+#pragma unroll
+  for (int h = 0; h < MAX_H1_2L; ++h) {
+    if (h < h1) {
+      float z = b1[h];
+      z = __builtin_fmaf(W1[4 * h + 0], x[0], z);
+      z = __builtin_fmaf(W1[4 * h + 1], x[1], z);
+      z = __builtin_fmaf(W1[4 * h + 2], x[2], z);
+      z = __builtin_fmaf(W1[4 * h + 3], x[3], z);
+      hv[h] = fmaxf(z, 0.0f);
+    } else {
+      hv[h] = 0.0f;
+    }
+  }
+  float out = wo[h2];
+  for (int o = 0; o < h2; ++o) {
+    const float* w = W2 + o * h1;
+    float z = b2[o];
+#pragma unroll
+    for (int h = 0; h < MAX_H1_2L; ++h)
+      if (h < h1) z = __builtin_fmaf(w[h], hv[h], z);
+    out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
+  }
+  return out;
+}
+
+__device__ __forceinline__ float policy_score(const EvictArgs& a, const float x[4]) {
+  return a.nh == 1 ? mlp1(a.params, a.h1, x) : mlp2(a.params, a.h1, a.h2, x);
+}
+
+// Scores of KP rows per thread.  Row slots k >= kact (uniform over the wave)
+// are skipped; the loops over the hidden units are uniform, so the weights are
+// read once per wave into scalar registers and reused for every row slot.  The
+// arithmetic (order of the fused multiply-adds) is that of mlp1 / mlp2.
+template <int KP, int NH>
+__device__ __forceinline__ void policy_scores(const EvictArgs& a, const float (&x)[KP][4],
+                                              float (&out)[KP], int kact) {
+  const float* __restrict__ P = a.params;
+  if constexpr (NH == 1) {
+    const int h1 = a.h1;
+    const float* W1 = P;
+    const float* b1 = P + 4 * h1;
+    const float* wo = b1 + h1;
+    const float bo = wo[h1];
+#pragma unroll
+    for (int k = 0; k < KP; ++k) out[k] = bo;
+    for (int h = 0; h < h1; ++h) {
+      const float w0 = W1[4 * h], w1 = W1[4 * h + 1], w2 = W1[4 * h + 2], w3 = W1[4 * h + 3];
+      const float bb = b1[h], ww = wo[h];
+#pragma unroll
+      for (int k = 0; k < KP; ++k) {
+        if (k < kact) {
+          float z = bb;
+          z = __builtin_fmaf(w0, x[k][0], z);
+          z = __builtin_fmaf(w1, x[k][1], z);
+          z = __builtin_fmaf(w2, x[k][2], z);
+          z = __builtin_fmaf(w3, x[k][3], z);
+          out[k] = __builtin_fmaf(ww, fmaxf(z, 0.0f), out[k]);
+        }
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < KP; ++k)
+      if (k < kact) out[k] = mlp2(P, a.h1, a.h2, x[k]);
+  }
+}
+
+// ---------------------------------------------------------------- key sources
+// Keys of row r = k * ENT + tid live in registers (fused path) ...
+template <int KPT>
+struct RegKeys {
+  static constexpr int KMAX = KPT;
+  uint64_t key[KPT];
+  __device__ uint64_t get(int k) const { return key[k]; }
+};
+// ... or in the workspace (long caches), written by score_kernel.
+struct MemKeys {
+  static constexpr int KMAX = MAX_LEN / ENT;
+  const uint64_t* key;
+  __device__ uint64_t get(int k) const { return key[k * ENT + threadIdx.x]; }
+};
+
+// ... or in LDS (fused decode+evict kernel).
+template <int KM>
+struct LdsKeys {
+  static constexpr int KMAX = KM;
+  const uint64_t* key;
+  __device__ uint64_t get(int k) const { return key[k * ENT + threadIdx.x]; }
+};
+
+template <typename T>
+__device__ __forceinline__ T wave_min(T x) {
+  for (int off = 32; off > 0; off >>= 1) {
+    T o = __shfl_xor(x, off);
+    x = o < x ? o : x;
+  }
+  return x;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x) {
+  const int lane = threadIdx.x & 63;
+  for (int off = 1; off < 64; off <<= 1) {
+    int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+// Shared-memory layout of the select workgroup.
+struct SelShared {
+  uint64_t wmin[ENW];
+  int hist[256];
+  int sel[4];            // digit, count below, count in digit, done flag
+  int wcnt[2][ENW];      // per-wave hole / mover counts
+  int nmoves;
+};
+
+// Block exclusive scans of two flags over rows k*ENT + tid (one k at a time).
+__device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, int& t0, int& t1,
+                                            SelShared& sh) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const uint64_t b0 = __ballot(f0), b1 = __ballot(f1);
+  const uint64_t below = lane ? (~0ull >> (64 - lane)) : 0ull;
+  const int p0 = __popcll(b0 & below), p1 = __popcll(b1 & below);
+  if (lane == 0) {
+    sh.wcnt[0][wave] = __popcll(b0);
+    sh.wcnt[1][wave] = __popcll(b1);
+  }
+  __syncthreads();
+  int o0 = 0, o1 = 0;
+  t0 = 0;
+  t1 = 0;
+  for (int w = 0; w < ENW; ++w) {
+    if (w < wave) {
+      o0 += sh.wcnt[0][w];
+      o1 += sh.wcnt[1][w];
+    }
+    t0 += sh.wcnt[0][w];
+    t1 += sh.wcnt[1][w];
+  }
+  __syncthreads();
+  r0 = o0 + p0;
+  r1 = o1 + p1;
+}
+
+// Select the E smallest keys and compact the unit.  `keys` holds the keys of
+// rows k*ENT + tid for k < kpt (invalid rows beyond L are ignored).
+template <typename Keys, int DTYPE, int D>
+__device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int kpt, SelShared& sh,
+                               int* mv) {
+  constexpr int ELT = DTYPE == 0 ? 4 : 2;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int L = a.L, B = a.budget, E = L - B;
+  const size_t ub = (size_t)u * a.cap;
+  // threshold: evicted rows are those with key <= thr
+  uint64_t thr;
+  if (E == 1) {
+    uint64_t m = ~0ull;
+#pragma unroll
+    for (int k = 0; k < Keys::KMAX; ++k) {
+      if (k >= kpt) break;
+      const int r = k * ENT + tid;
+      if (r < L) {
+        const uint64_t x = keys.get(k);
+        m = x < m ? x : m;
+      }
+    }
+    m = wave_min(m);
+    if (lane == 0) sh.wmin[wave] = m;
+    __syncthreads();
+    thr = sh.wmin[0];
+    for (int w = 1; w < ENW; ++w) thr = sh.wmin[w] < thr ? sh.wmin[w] : thr;
+    // one row leaves: if it sits below B, the row in slot B (the only slot >= B)
+    // fills it; no scans needed
+#pragma unroll
+    for (int k = 0; k < Keys::KMAX; ++k) {
+      if (k >= kpt) break;
+      const int r = k * ENT + tid;
+      if (r < L && keys.get(k) == thr) sh.sel[3] = r;
+    }
+    __syncthreads();
+    const int ev = sh.sel[3];
+    if (a.kept_out)
+      for (int r = tid; r < B; r += ENT) a.kept_out[(size_t)u * B + r] = r == ev ? B : r;
+    if (ev < B && tid < 64) {
+      const size_t gd = ub + ev, gs = ub + B;
+      constexpr int N16 = D * ELT / 16;
+      char* kb = (char*)a.k;
+      char* vb = (char*)a.v;
+      for (int c = tid; c < 2 * N16; c += 64) {
+        char* base = c < N16 ? kb : vb;
+        const int cc = c < N16 ? c : c - N16;
+        *reinterpret_cast<uint4*>(base + gd * D * ELT + cc * 16) = ldg16(base + gs * D * ELT + cc * 16);
+      }
+      if (tid == 0) {
+        a.alpha[gd] = a.alpha[gs];
+        a.num[gd] = a.num[gs];
+        a.den[gd] = a.den[gs];
+        a.pos[gd] = a.pos[gs];
+        a.vnorm[gd] = a.vnorm[gs];
+      }
+    }
+    return;
+  } else {
+    uint64_t prefix = 0;
+    int need = E;
+    int shift = 56;
+    for (;; shift -= 8) {
+      const uint64_t hmask = shift + 8 >= 64 ? 0ull : (~0ull << (shift + 8));
+      for (int i = tid; i < 256; i += ENT) sh.hist[i] = 0;
+      __syncthreads();
+#pragma unroll
+      for (int k = 0; k < Keys::KMAX; ++k) {
+        if (k >= kpt) break;
+        const int r = k * ENT + tid;
+        if (r < L) {
+          const uint64_t x = keys.get(k);
+          if ((x & hmask) == prefix) atomicAdd(&sh.hist[(int)((x >> shift) & 255u)], 1);
+        }
+      }
+      __syncthreads();
+      if (wave == 0) {
+        const int c0 = sh.hist[4 * lane], c1 = sh.hist[4 * lane + 1], c2 = sh.hist[4 * lane + 2],
+                  c3 = sh.hist[4 * lane + 3];
+        const int incl = wave_incl_scan(c0 + c1 + c2 + c3);
+        int below = incl - (c0 + c1 + c2 + c3);
+        const int cs[4] = {c0, c1, c2, c3};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          if (below < need && need <= below + cs[q]) {
+            sh.sel[0] = 4 * lane + q;
+            sh.sel[1] = below;
+            sh.sel[2] = cs[q];
+          }
+          below += cs[q];
+        }
+      }
+      __syncthreads();
+      const int digit = sh.sel[0], cbelow = sh.sel[1], cin = sh.sel[2];
+      __syncthreads();
+      need -= cbelow;
+      prefix |= (uint64_t)digit << shift;
+      if (cin == need || shift == 0) break;
+    }
+    // evicted: (key >> shift) <= (prefix >> shift)
+    thr = prefix | (shift ? ((1ull << shift) - 1) : 0ull);
+  }
+  // plan: holes (evicted, slot < B) take movers (kept, slot >= B) in order
+  if (tid == 0) sh.nmoves = 0;
+  int run0 = 0, run1 = 0;
+#pragma unroll
+  for (int k = 0; k < Keys::KMAX; ++k) {
+    if (k >= kpt || k * ENT >= L) break;
+    const int r = k * ENT + tid;
+    bool ev = false;
+    if (r < L) ev = keys.get(k) <= thr;
+    const bool hole = r < B && ev;
+    const bool mover = r >= B && r < L && !ev;
+    int rk0, rk1, t0, t1;
+    block_scan2(hole, mover, rk0, rk1, t0, t1, sh);
+    if (hole) mv[2 * (run0 + rk0)] = r;
+    if (mover) mv[2 * (run1 + rk1) + 1] = r;
+    if (a.kept_out && r < B && !ev) a.kept_out[(size_t)u * B + r] = r;
+    run0 += t0;
+    run1 += t1;
+  }
+  __syncthreads();
+  const int nm = run0;  // == run1
+  // copy rows: one 16-lane group per move
+  constexpr int N16 = D * ELT / 16;  // 16-byte chunks per row (8 or 16)
+  const int grp = tid / 16, gl = tid % 16, ngrp = ENT / 16;
+  for (int j = grp; j < nm; j += ngrp) {
+    const int dst = mv[2 * j], src = mv[2 * j + 1];
+    const size_t gd = ub + dst, gs = ub + src;
+    char* kb = (char*)a.k;
+    char* vb = (char*)a.v;
+    for (int c = gl; c < N16; c += 16) {
+      *reinterpret_cast<uint4*>(kb + gd * D * ELT + c * 16) = ldg16(kb + gs * D * ELT + c * 16);
+      *reinterpret_cast<uint4*>(vb + gd * D * ELT + c * 16) = ldg16(vb + gs * D * ELT + c * 16);
+    }
+    if (gl == 0) {
+      a.alpha[gd] = a.alpha[gs];
+      a.num[gd] = a.num[gs];
+      a.den[gd] = a.den[gs];
+      a.pos[gd] = a.pos[gs];
+      a.vnorm[gd] = a.vnorm[gs];
+      if (a.kept_out) a.kept_out[(size_t)u * B + dst] = src;
+    }
+  }
+}
+
+}  // namespace dc

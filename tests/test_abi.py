@@ -1,0 +1,138 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+the header declares, and rejects invalid calls on the host before any launch
+(status codes and untouched host fields)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_08878_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "distillcache.h")
+FAKE = 0x10000          # a non-NULL pointer that validation failures never dereference
+
+pytestmark = pytest.mark.skipif(not os.path.exists(B.LIB_PATH), reason="library not built")
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(dc_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_function():
+    names = declared_functions()
+    assert set(names) == set(B.EXPORTS), names
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _dims(**kw):
+    d = dict(batch=1, n_layers=2, n_q_heads=8, n_kv_heads=2, head_dim=128, capacity=100,
+             dtype=B.DC_BF16, ent_window=64, scale=0.0)
+    d.update(kw)
+    return B.dc_dims(*[d[f] for f, _ in B.dc_dims._fields_])
+
+
+def _feat(**kw):
+    f = B.dc_feat(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 5, 50)
+    for k, v in kw.items():
+        setattr(f, k, v)
+    return f
+
+
+def _decode(dims, kv, feat, q=FAKE, kn=FAKE, vn=FAKE, out=FAKE, ws=None, wsb=0):
+    L = B.lib()
+    return L.dc_decode_step(ctypes.byref(dims), ctypes.byref(kv),
+                            ctypes.byref(feat) if feat is not None else None, q, kn, vn, out, ws,
+                            wsb, None)
+
+
+def test_status_strings():
+    for code, name in B.STATUS.items():
+        assert B.dc_status_str(code).startswith(name)
+    assert "unknown" in B.dc_status_str(99)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(head_dim=96), 3), (dict(n_q_heads=6, n_kv_heads=4), 2), (dict(n_q_heads=48, n_kv_heads=2), 3),
+    (dict(dtype=7), 3), (dict(ent_window=65), 2), (dict(ent_window=-1), 2), (dict(batch=0), 2),
+    (dict(scale=-1.0), 2), (dict(scale=float("nan")), 2), (dict(capacity=0), 2)])
+def test_decode_rejects_bad_dims(kw, status):
+    kv = B.dc_kv(FAKE, FAKE, 10)
+    feat = _feat()
+    assert _decode(_dims(**kw), kv, feat) == status
+    assert kv.len == 10 and feat.step == 5 and feat.next_pos == 50
+
+
+def test_decode_rejects_bad_state():
+    d = _dims()
+    assert _decode(d, B.dc_kv(None, FAKE, 10), _feat()) == 1
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 10), _feat(), q=None) == 1
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 10), _feat(), kn=None) == 1          # k_new without v_new
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 10), _feat(alpha=None)) == 1
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 10), _feat(qring=None)) == 1         # window needs the ring
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 101), _feat()) == 2                  # len > capacity
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 100), _feat()) == 4                  # append beyond capacity
+    assert _decode(d, B.dc_kv(FAKE, FAKE, 0), _feat(), kn=None, vn=None) == 2  # empty, no append
+    big = _dims(capacity=50000)
+    kv = B.dc_kv(FAKE, FAKE, 40000)                                            # chunked path needs scratch
+    assert _decode(big, kv, _feat(), ws=None) == 6
+    assert _decode(big, kv, _feat(), ws=FAKE, wsb=10) == 6
+    assert kv.len == 40000
+
+
+def test_score_evict_rejects_bad_arguments():
+    L = B.lib()
+    d = _dims()
+    params = ctypes.c_void_p(FAKE)
+
+    def call(budget=10, kv=None, feat=None, pol=None, ws=None, wsb=0):
+        kv = kv or B.dc_kv(FAKE, FAKE, 50)
+        feat = feat or _feat()
+        pol = pol or B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)
+        return L.dc_score_evict(ctypes.byref(d), ctypes.byref(kv), ctypes.byref(feat),
+                                ctypes.byref(pol), budget, None, None, ws, wsb, None)
+
+    assert call(budget=0) == 5
+    assert call(budget=-3) == 5
+    assert call(pol=B.dc_policy(5, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 3, (ctypes.c_int32 * 2)(32, 32), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 2, (ctypes.c_int32 * 2)(65, 32), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 1, (ctypes.c_int32 * 2)(0, 0), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), None)) == 1
+    assert call(kv=B.dc_kv(FAKE, FAKE, 0)) == 2
+    assert call(feat=_feat(vnorm=None)) == 1
+    big = _dims(capacity=60000)
+    kv = B.dc_kv(FAKE, FAKE, 41000)
+    assert L.dc_score_evict(ctypes.byref(big), ctypes.byref(kv), ctypes.byref(_feat()),
+                            ctypes.byref(B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)),
+                            10, None, None, None, 0, None) == 3              # beyond 40960 rows
+    kv = B.dc_kv(FAKE, FAKE, 9000)                                            # long cache: key scratch
+    assert L.dc_score_evict(ctypes.byref(big), ctypes.byref(kv), ctypes.byref(_feat()),
+                            ctypes.byref(B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)),
+                            10, None, None, None, 0, None) == 6
+    assert kv.len == 9000
+
+
+def test_kl_reward_rejects_bad_arguments():
+    L = B.lib()
+    assert L.dc_kl_reward(8, 4096, 32768, None, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 1
+    assert L.dc_kl_reward(0, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 2
+    assert L.dc_kl_reward(65, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
+    assert L.dc_kl_reward(8, 4000, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
+    assert L.dc_kl_reward(8, 4096, 32700, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
+    assert L.dc_kl_reward(8, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == 6
+
+
+def test_workspace_sizes():
+    d = _dims(batch=16, n_layers=32, n_q_heads=32, n_kv_heads=8, capacity=16385)
+    assert B.dc_workspace_bytes(d, 0, 0, 0) == 0
+    big = B.dc_workspace_bytes(d, 16385, 0, 0)
+    assert big >= 4096 * 16385 * 7 * 4            # per-row logits, retired sums, norms
+    assert B.dc_workspace_bytes(d, 4097, 0, 0) < big
+    assert B.dc_workspace_bytes(d, 0, 8, 32768) >= 8 * 512 * 16
+    assert B.dc_workspace_bytes(_dims(head_dim=96), 100, 0, 0) == 0

@@ -369,3 +369,71 @@ def test_long_cache_selection_uses_workspace_keys():
         _check_decode(wl, outn[u], pre[u], st, att, u)
         s_or = ounit.scores(st, pnp, wl.hidden)
         _check_evict(wl, wl.budget, pre[u], sc[u], kp[u], H.download_unit(buf, u), s_or, u)
+
+
+@pytest.mark.parametrize("dtype,n0,head_dim", [("bf16", 1000, 128), ("bf16", 6000, 128),
+                                               ("bf16", 900, 64), ("f32", 1000, 128),
+                                               ("f32", 700, 64)])
+def test_retire_recomputes_the_added_weights_bit_exactly(dtype, n0, head_dim):
+    """Window w = 2, the same query every step, no appends: every step adds the
+    same per-row contribution c, and from step 2 on retires the one added two
+    steps earlier.  The window sums are then 2c after every step, bit for bit,
+    only if the retire reproduces the added weights exactly (the recomputed
+    logits, the stored max and 1/l, the same exp and the same head order)."""
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=2, n_q_heads=8, n0=n0, dtype=dtype, head_dim=head_dim,
+                               ent_window=2, append=False, steps=5)
+    U = wl.units
+    buf = _buffers(wl, capacity=n0)
+    buf.reserve_workspace(n0)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(n0, 0)
+    q = torch.empty((U, wl.group, head_dim), dtype=H.torch_dtype(wl), device="cuda")
+    sg.queries(wl, 0, q)
+    dens, nums = [], []
+    for t in range(5):
+        buf.decode_step(q)
+        torch.cuda.synchronize()
+        dens.append(buf.den[:, :n0].clone())
+        nums.append(buf.num[:, :n0].clone())
+    assert torch.all(dens[1] > 0)
+    for t in (2, 3, 4):
+        assert torch.equal(dens[t], dens[1]), t
+        assert torch.equal(nums[t], nums[1]), t
+    # and the first step's contribution is exactly half of the two-step window
+    assert torch.equal(dens[0] * 2, dens[1])
+
+
+@pytest.mark.parametrize("n0,budget", [(3000, 900), (6000, 1500)])
+def test_fused_step_equals_decode_then_evict(n0, budget):
+    """dc_decode_evict (one launch where the cache fits on chip; the chunked
+    decode plus the separate eviction otherwise) leaves every buffer, output,
+    score and slot map bit-identical to dc_decode_step + dc_score_evict."""
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=2, n_q_heads=8, n0=n0, budget=budget, steps=70)
+    U = wl.units
+    bufs = [_buffers(wl), _buffers(wl)]
+    for b in bufs:
+        b.reserve_workspace(wl.capacity)
+        sg.init_cache(wl, b.k, b.v, U, b.cap)
+        b.feat_init(wl.n0, 0)
+    params, pol = _policy(wl)
+    q, kn, vn = _step_tensors(wl)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        L = bufs[0].kv.len + 1
+        sc = [torch.empty((U, L), dtype=torch.float32, device="cuda") for _ in range(2)]
+        kp = [torch.empty((U, min(L, budget)), dtype=torch.int32, device="cuda") for _ in range(2)]
+        o0 = bufs[0].decode_step(q, kn, vn)
+        bufs[0].score_evict(pol, budget, sc[0], kp[0])
+        o1 = bufs[1].decode_evict(pol, budget, q, kn, vn, scores_out=sc[1], kept_out=kp[1])
+        torch.cuda.synchronize()
+        assert torch.equal(o0, o1), t
+        assert torch.equal(sc[0], sc[1]) and torch.equal(kp[0], kp[1]), t
+        assert bufs[0].kv.len == bufs[1].kv.len and bufs[0].feat.step == bufs[1].feat.step
+        n = bufs[0].kv.len
+        for name in ("k", "v", "alpha", "num", "den", "pos", "vnorm", "qring", "qstat"):
+            a0, a1 = getattr(bufs[0], name), getattr(bufs[1], name)
+            if name in ("qring", "qstat"):
+                assert torch.equal(a0, a1), (t, name)
+            else:
+                assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
