@@ -149,6 +149,9 @@ dc_status dc_feat_init(const dc_dims *dims, const dc_kv *kv, dc_feat *feat, int3
  *          Sec. 3.1.3); otherwise alpha += (1/G) sum_j a_j(i), this step's
  *          queries enter the entropy window, step t - w leaves it, vnorm is
  *          rewritten, the ring slot (step mod w) is overwritten, step += 1.
+ * Workspace: dc_workspace_bytes(dims, len + appended, 0, 0) bytes whenever feat is
+ * not NULL (per-row scratch between the key and feature passes), and for
+ * plain attention over caches longer than fit on chip.
  * Errors: DC_ERR_NULL, DC_ERR_SHAPE (len == 0 without append, len > capacity),
  * DC_ERR_CAPACITY (len + 1 > capacity), DC_ERR_UNSUPPORTED, DC_ERR_WORKSPACE. */
 dc_status dc_decode_step(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const void *q,

@@ -49,6 +49,8 @@ class DecodeBuffers:
                                   self.qring.data_ptr(), self.qstat.data_ptr(), 0, 0)
         self.ws = None
         self.ws_bytes = 0
+        if features:
+            self.reserve_workspace(capacity)
 
     @property
     def len(self) -> int:

@@ -149,7 +149,9 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
     split = !dc::step_fits(L, G, D, feat != nullptr, 0) || (U < 128 && L > 2 * dc::step_chunk_rows());
   else
     split = use_split(dims, L, feat != nullptr);
-  need = split ? split_bytes(dims, L) : 0;
+  // the matrix-core unit path parks each row's retired (cz, cn) in the workspace
+  const bool unit_scratch = dims->dtype == DC_BF16 && feat && !split;
+  need = split ? split_bytes(dims, L) : unit_scratch ? align256((size_t)U * L * 2 * sizeof(float)) : 0;
   if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
 
   memset(&a, 0, sizeof(a));
@@ -180,6 +182,10 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
       a.retire = feat->step >= W;
       a.pmax_ret = a.retire ? feat->ring_pmax[a.slot] : 0;
     }
+  }
+  if (unit_scratch) {
+    a.ws_r = (float*)ws;
+    a.lmax = L;
   }
   if (split) {
     const size_t rows = (size_t)U * L;

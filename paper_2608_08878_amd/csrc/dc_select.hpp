@@ -6,8 +6,8 @@
 
 namespace dc {
 
-constexpr int ENT = 1024;            // threads of the per-unit select workgroup
-constexpr int ENW = ENT / 64;
+constexpr int ENT = 1024;            // threads of the stand-alone select workgroup
+constexpr int ENW_MAX = 16;          // waves per workgroup, at most
 constexpr int REG_KPT = 8;           // rows per thread kept in registers (L <= 8192)
 constexpr int MAX_LEN = 40960;
 constexpr int MAX_H1_2L = 64;        // first hidden width supported with two hidden layers
@@ -145,11 +145,13 @@ struct MemKeys {
 };
 
 // ... or in LDS (fused decode+evict kernel).
-template <int KM>
+// Keys in LDS at a row stride of `stride` u64 (rows k * NT + tid).
+template <int KM, int NT>
 struct LdsKeys {
   static constexpr int KMAX = KM;
   const uint64_t* key;
-  __device__ uint64_t get(int k) const { return key[k * ENT + threadIdx.x]; }
+  int stride;
+  __device__ uint64_t get(int k) const { return key[(size_t)(k * NT + threadIdx.x) * stride]; }
 };
 
 template <typename T>
@@ -172,14 +174,15 @@ __device__ __forceinline__ int wave_incl_scan(int x) {
 
 // Shared-memory layout of the select workgroup.
 struct SelShared {
-  uint64_t wmin[ENW];
+  uint64_t wmin[ENW_MAX];
   int hist[256];
-  int sel[4];            // digit, count below, count in digit, done flag
-  int wcnt[2][ENW];      // per-wave hole / mover counts
+  int sel[4];            // digit, count below, count in digit, evicted slot
+  int wcnt[2][ENW_MAX];  // per-wave hole / mover counts
   int nmoves;
 };
 
-// Block exclusive scans of two flags over rows k*ENT + tid (one k at a time).
+// Block exclusive scans of two flags over rows k*NT + tid (one k at a time).
+template <int NT>
 __device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, int& t0, int& t1,
                                             SelShared& sh) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -194,7 +197,7 @@ __device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, 
   int o0 = 0, o1 = 0;
   t0 = 0;
   t1 = 0;
-  for (int w = 0; w < ENW; ++w) {
+  for (int w = 0; w < NT / 64; ++w) {
     if (w < wave) {
       o0 += sh.wcnt[0][w];
       o1 += sh.wcnt[1][w];
@@ -208,8 +211,9 @@ __device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, 
 }
 
 // Select the E smallest keys and compact the unit.  `keys` holds the keys of
-// rows k*ENT + tid for k < kpt (invalid rows beyond L are ignored).
-template <typename Keys, int DTYPE, int D>
+// rows k*NT + tid for k < kpt (invalid rows beyond L are ignored); NT is the
+// workgroup size.
+template <typename Keys, int DTYPE, int D, int NT = ENT>
 __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int kpt, SelShared& sh,
                                int* mv) {
   constexpr int ELT = DTYPE == 0 ? 4 : 2;
@@ -223,7 +227,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
 #pragma unroll
     for (int k = 0; k < Keys::KMAX; ++k) {
       if (k >= kpt) break;
-      const int r = k * ENT + tid;
+      const int r = k * NT + tid;
       if (r < L) {
         const uint64_t x = keys.get(k);
         m = x < m ? x : m;
@@ -233,19 +237,19 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
     if (lane == 0) sh.wmin[wave] = m;
     __syncthreads();
     thr = sh.wmin[0];
-    for (int w = 1; w < ENW; ++w) thr = sh.wmin[w] < thr ? sh.wmin[w] : thr;
+    for (int w = 1; w < NT / 64; ++w) thr = sh.wmin[w] < thr ? sh.wmin[w] : thr;
     // one row leaves: if it sits below B, the row in slot B (the only slot >= B)
     // fills it; no scans needed
 #pragma unroll
     for (int k = 0; k < Keys::KMAX; ++k) {
       if (k >= kpt) break;
-      const int r = k * ENT + tid;
+      const int r = k * NT + tid;
       if (r < L && keys.get(k) == thr) sh.sel[3] = r;
     }
     __syncthreads();
     const int ev = sh.sel[3];
     if (a.kept_out)
-      for (int r = tid; r < B; r += ENT) a.kept_out[(size_t)u * B + r] = r == ev ? B : r;
+      for (int r = tid; r < B; r += NT) a.kept_out[(size_t)u * B + r] = r == ev ? B : r;
     if (ev < B && tid < 64) {
       const size_t gd = ub + ev, gs = ub + B;
       constexpr int N16 = D * ELT / 16;
@@ -271,12 +275,12 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
     int shift = 56;
     for (;; shift -= 8) {
       const uint64_t hmask = shift + 8 >= 64 ? 0ull : (~0ull << (shift + 8));
-      for (int i = tid; i < 256; i += ENT) sh.hist[i] = 0;
+      for (int i = tid; i < 256; i += NT) sh.hist[i] = 0;
       __syncthreads();
 #pragma unroll
       for (int k = 0; k < Keys::KMAX; ++k) {
         if (k >= kpt) break;
-        const int r = k * ENT + tid;
+        const int r = k * NT + tid;
         if (r < L) {
           const uint64_t x = keys.get(k);
           if ((x & hmask) == prefix) atomicAdd(&sh.hist[(int)((x >> shift) & 255u)], 1);
@@ -314,14 +318,14 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
   int run0 = 0, run1 = 0;
 #pragma unroll
   for (int k = 0; k < Keys::KMAX; ++k) {
-    if (k >= kpt || k * ENT >= L) break;
-    const int r = k * ENT + tid;
+    if (k >= kpt || k * NT >= L) break;
+    const int r = k * NT + tid;
     bool ev = false;
     if (r < L) ev = keys.get(k) <= thr;
     const bool hole = r < B && ev;
     const bool mover = r >= B && r < L && !ev;
     int rk0, rk1, t0, t1;
-    block_scan2(hole, mover, rk0, rk1, t0, t1, sh);
+    block_scan2<NT>(hole, mover, rk0, rk1, t0, t1, sh);
     if (hole) mv[2 * (run0 + rk0)] = r;
     if (mover) mv[2 * (run1 + rk1) + 1] = r;
     if (a.kept_out && r < B && !ev) a.kept_out[(size_t)u * B + r] = r;
@@ -332,7 +336,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
   const int nm = run0;  // == run1
   // copy rows: one 16-lane group per move
   constexpr int N16 = D * ELT / 16;  // 16-byte chunks per row (8 or 16)
-  const int grp = tid / 16, gl = tid % 16, ngrp = ENT / 16;
+  const int grp = tid / 16, gl = tid % 16, ngrp = NT / 16;
   for (int j = grp; j < nm; j += ngrp) {
     const int dst = mv[2 * j], src = mv[2 * j + 1];
     const size_t gd = ub + dst, gs = ub + src;

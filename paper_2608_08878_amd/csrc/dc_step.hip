@@ -24,11 +24,12 @@
 
 namespace dc {
 
-constexpr int SNT = 1024;
+constexpr int SNT = 512;              // threads per workgroup (two workgroups per CU)
 constexpr int SNW = SNT / 64;
 constexpr int SCHUNK = 2048;          // rows per workgroup on the chunked path
-constexpr int S_KMAX = 5;             // fused step: rows per thread (L <= 5120)
-constexpr int S_LDS = 160 * 1024 - 8 * 1024;  // dynamic LDS budget (static LDS aside)
+constexpr int S_KMAX = 10;            // fused step: row slots per thread (L <= 5120)
+constexpr int S_KB = 3;               // row slots per thread handled per feature batch
+constexpr int S_LDS = 160 * 1024 - 4 * 1024;  // dynamic LDS budget (static LDS aside)
 
 template <int D>
 struct MG {
@@ -90,7 +91,7 @@ __device__ __forceinline__ void load_ret(RetStats<G>& r, const DecodeArgs& a, in
 // Rows [r0, r1) of unit u, 16-key tiles distributed over the waves.  Logits of
 // the current heads go to s_sink[(i - sink0) * G + j], retired contributions to
 // r_sink[2 (i - sink0)], running maxima per current head into mrun.
-template <int D, int G, bool FEAT>
+template <int D, int G, bool FEAT, int RS = G>
 __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r1, float* s_sink,
                                        float* r_sink, int sink0, const uint4 (&qa)[MG<D>::NT],
                                        bool retire, const RetStats<G>& rs, float (&mrun)[4]) {
@@ -106,8 +107,10 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
     int key = r0 + tile * 16 + i;
     key = key < r1 ? key : r1 - 1;
     const char* kp = key == newrow ? kn : kc + (size_t)key * D * 2;
+    // plain loads: instructions t and t+1 read the two halves of the same 128-byte
+    // line, so the second one should find it in the vector L1
 #pragma unroll
-    for (int t = 0; t < NT; ++t) kb[t] = ldg16_nt(kp + 16 * (4 * t + g));
+    for (int t = 0; t < NT; ++t) kb[t] = ldg16(kp + 16 * (4 * t + g));
   };
   auto process = [&](int tt, const uint4 (&kb)[NT]) {
     f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -126,7 +129,7 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
 #pragma unroll
       for (int r = 0; r < 4; ++r)
         if (4 * g + r < G) mrun[r] = fmaxf(mrun[r], s[r]);
-      float* dst = s_sink + (size_t)(key - sink0) * G + 4 * g;
+      float* dst = s_sink + (size_t)(key - sink0) * RS + 4 * g;
       if constexpr (G >= 4) {
         *reinterpret_cast<f32x4_t*>(dst) = f32x4_t{s[0], s[1], s[2], s[3]};
       } else {
@@ -204,7 +207,7 @@ __device__ __forceinline__ void block_max(const float (&mrun)[4], float* stat, f
 
 // pass P over LDS rows [0, n): p = exp(s - M) in place; returns the per-thread
 // partial sums of p and p (s - M).
-template <int G>
+template <int G, int RS = G>
 __device__ __forceinline__ void pass_p(float* sbuf, int n, const float (&M)[G], float (&ls)[G],
                                        float (&us)[G]) {
 #pragma unroll
@@ -215,9 +218,9 @@ __device__ __forceinline__ void pass_p(float* sbuf, int n, const float (&M)[G], 
   for (int i = threadIdx.x; i < n; i += SNT) {
 #pragma unroll
     for (int j = 0; j < G; ++j) {
-      const float d = sbuf[i * G + j] - M[j];
+      const float d = sbuf[i * RS + j] - M[j];
       const float p = __builtin_amdgcn_exp2f(d * LOG2E);
-      sbuf[i * G + j] = p;
+      sbuf[i * RS + j] = p;
       ls[j] = ls[j] + p;
       us[j] = us[j] + p * d;
     }
@@ -256,7 +259,7 @@ __device__ __forceinline__ void block_sum2(float (&x)[G], float (&y)[G], float* 
 
 // pass B: rows [r0, r1), p from pbuf[(i - p0) * G + j]; per-wave partial output
 // o[j][e] for the lane's 8 dims (lanes 0..LPR-1 hold the wave total).
-template <int D, int G>
+template <int D, int G, int RS = G>
 __device__ __forceinline__ void pass_b(const DecodeArgs& a, int u, int r0, int r1,
                                        const float* pbuf, int p0, float (&o)[G][8]) {
   constexpr int LPR = MG<D>::LPR, NG = SNT / LPR;
@@ -279,7 +282,7 @@ __device__ __forceinline__ void pass_b(const DecodeArgs& a, int u, int r0, int r
     const int rc = ok ? row : r1 - 1;
     float pj[G];
 #pragma unroll
-    for (int j = 0; j < G; ++j) pj[j] = ok ? pbuf[(size_t)(rc - p0) * G + j] : 0.0f;
+    for (int j = 0; j < G; ++j) pj[j] = ok ? pbuf[(size_t)(rc - p0) * RS + j] : 0.0f;
     float vf[8];
     unpack_slice<1>(vv, vf);
 #pragma unroll
@@ -402,21 +405,31 @@ __device__ __forceinline__ void append_rows(const DecodeArgs& a, int u) {
 }
 
 // ---------------------------------------------------------------- unit kernel
-// Dynamic LDS: [L*G logits -> weights][L*2 retired (cz, cn) -> u64 keys]
-//              [SNW*G*D output partials][2 ints per compaction move]
+// One workgroup per unit, sized so that two fit on a CU (one computes while the
+// other streams).  Dynamic LDS: [L * RS floats: logits -> weights -> u64 keys]
+// [SNW/2 * G * D output partials][2 ints per compaction move]; the retired
+// contributions (cz, cn) of pass A go to the workspace (ws_r) and come back in
+// the feature pass.
+template <int G>
+struct RowStride {
+  static constexpr int RS = G < 2 ? 2 : G;     // floats per row in LDS (a u64 key must fit)
+  static constexpr int KS = RS / 2;            // u64 per row
+};
+
 template <int D, int G, bool FEAT, bool EVICT, int NH>
-__global__ void __launch_bounds__(SNT) step_unit_kernel(DecodeArgs a, EvictArgs e) {
+__global__ void __launch_bounds__(SNT, 2) step_unit_kernel(DecodeArgs a, EvictArgs e) {
   constexpr int LPR = MG<D>::LPR;
+  constexpr int RS = RowStride<G>::RS, KS = RowStride<G>::KS;
   extern __shared__ float lds[];
   __shared__ SelShared sh;
   __shared__ float stat[SNW * 2 * G + 2 * G];
   __shared__ float newnorm_slot;
   const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int L = a.L;
-  float* sbuf = lds;
-  float* rbuf = lds + (size_t)L * G;
-  float* obuf = rbuf + (FEAT ? 2 * (size_t)L : 0);
-  int* mv = (int*)(obuf + SNW * G * D);
+  float* sbuf = lds;                                  // row stride RS
+  float* obuf = lds + (size_t)L * RS;                 // (SNW / 2) * G * D
+  int* mv = (int*)(obuf + (SNW / 2) * G * D);
+  float* rws = FEAT ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr;
   const size_t ub = (size_t)u * a.cap;
 
   if (a.append) append_rows<D>(a, u);
@@ -428,12 +441,12 @@ __global__ void __launch_bounds__(SNT) step_unit_kernel(DecodeArgs a, EvictArgs 
     RetStats<G> rs;
     if (retire) load_ret<G>(rs, a, u);
     float mrun[4];
-    pass_a<D, G, FEAT>(a, u, 0, L, sbuf, rbuf, 0, qa, retire, rs, mrun);
+    pass_a<D, G, FEAT, RS>(a, u, 0, L, sbuf, rws, 0, qa, retire, rs, mrun);
     block_max<G>(mrun, stat, M);
   }
   {
     float ls[G], us[G];
-    pass_p<G>(sbuf, L, M, ls, us);
+    pass_p<G, RS>(sbuf, L, M, ls, us);
     __syncthreads();
     block_sum2<G>(ls, us, stat);
 #pragma unroll
@@ -444,19 +457,30 @@ __global__ void __launch_bounds__(SNT) step_unit_kernel(DecodeArgs a, EvictArgs 
   }
   {
     float o[G][8];
-    pass_b<D, G>(a, u, 0, L, sbuf, 0, o);
-    if (lane < LPR) {
+    pass_b<D, G, RS>(a, u, 0, L, sbuf, 0, o);
+    // tree over the waves through SNW/2 partial slots
+    if (wave >= SNW / 2 && lane < LPR) {
 #pragma unroll
       for (int j = 0; j < G; ++j)
 #pragma unroll
-        for (int x = 0; x < 8; ++x) obuf[(wave * G + j) * D + lane * 8 + x] = o[j][x];
+        for (int x = 0; x < 8; ++x) obuf[((wave - SNW / 2) * G + j) * D + lane * 8 + x] = o[j][x];
+    }
+    __syncthreads();
+    if (wave < SNW / 2 && lane < LPR) {
+#pragma unroll
+      for (int j = 0; j < G; ++j)
+#pragma unroll
+        for (int x = 0; x < 8; ++x) {
+          float* slot = &obuf[(wave * G + j) * D + lane * 8 + x];
+          *slot = o[j][x] + *slot;
+        }
     }
   }
   __syncthreads();
   for (int t = tid; t < G * D; t += SNT) {
     const int j = t / D;
-    float acc = 0.0f;
-    for (int w = 0; w < SNW; ++w) acc = acc + obuf[w * G * D + t];
+    float acc = obuf[t];
+    for (int w = 1; w < SNW / 2; ++w) acc = acc + obuf[w * G * D + t];
     float il = invl[0];
 #pragma unroll
     for (int jj = 1; jj < G; ++jj) il = (jj == j) ? invl[jj] : il;
@@ -467,91 +491,109 @@ __global__ void __launch_bounds__(SNT) step_unit_kernel(DecodeArgs a, EvictArgs 
     const int newrow = a.append ? a.len_old : -1;
     const float invT = 1.0f / (float)a.T;
     constexpr float invG = 1.0f / G;
-    uint64_t* keys = reinterpret_cast<uint64_t*>(rbuf);   // row i's key replaces its (cz, cn)
-    constexpr int KP = S_KMAX;
-    // row slots k (rows k * SNT + tid) that hold a valid row somewhere in this wave
-    const int kact = L > wave * 64 ? (L - wave * 64 + SNT - 1) / SNT : 0;
-    // (1) issue every state load of the thread's rows at once
-    float al0[KP], vn0[KP];
-    double nu0[KP], de0[KP];
-    int32_t p0[KP];
+    uint64_t* keys = reinterpret_cast<uint64_t*>(sbuf);   // row i's key replaces its weights
+    const int nslots = (L + SNT - 1) / SNT;
+    struct Batch {
+      float al[S_KB], vn[S_KB], rz[S_KB], rn[S_KB];
+      double nu[S_KB], de[S_KB];
+      int32_t p[S_KB];
+    };
+    auto kact_of = [&](int kb) {
+      const int rem = L - kb * SNT - wave * 64;   // slots with a valid row in this wave
+      return rem > 0 ? min(S_KB, (rem + SNT - 1) / SNT) : 0;
+    };
+    auto load_batch = [&](int kb, Batch& b) {
+      const int kact = kact_of(kb);
 #pragma unroll
-    for (int k = 0; k < KP; ++k) {
-      if (k < kact) {
-        const int i = k * SNT + tid;
-        const size_t gi = ub + (i < L ? i : L - 1);
-        al0[k] = a.alpha[gi];
-        nu0[k] = a.num[gi];
-        de0[k] = a.den[gi];
-        p0[k] = a.pos[gi];
-        vn0[k] = a.vnorm[gi];
-      }
-    }
-    // (2) update the state from this step's weights
-    float x[KP][4];
-    int32_t pk[KP];
-#pragma unroll
-    for (int k = 0; k < KP; ++k) {
-      if (k < kact) {
-        const int i = k * SNT + tid;
-        const bool valid = i < L;
-        const int ic = valid ? i : L - 1;
-        const size_t gi = ub + ic;
-        float w[G];
-#pragma unroll
-        for (int j = 0; j < G; ++j) w[j] = sbuf[ic * G + j] * invl[j];
-        float cz, cn;
-        contrib_from_weights<G>(w, H, cz, cn);
-        float al, vn;
-        double nu, de;
-        int32_t ps;
-        if (ic == newrow) {
-          al = cz * invG;
-          de = (double)cz;
-          nu = (double)cn;
-          ps = a.T - 1;
-          vn = newnorm;
-        } else {
-          al = al0[k] + cz * invG;
-          de = de0[k] + (double)cz;
-          nu = nu0[k] + (double)cn;
-          ps = p0[k];
-          vn = vn0[k];
-          if (retire && ps <= a.pmax_ret) {
-            de = de - (double)rbuf[2 * ic];
-            nu = nu - (double)rbuf[2 * ic + 1];
+      for (int k = 0; k < S_KB; ++k) {
+        if (k < kact) {
+          const int i = (kb + k) * SNT + tid;
+          const int ic = i < L ? i : L - 1;
+          const size_t gi = ub + ic;
+          b.al[k] = a.alpha[gi];
+          b.nu[k] = a.num[gi];
+          b.de[k] = a.den[gi];
+          b.p[k] = a.pos[gi];
+          b.vn[k] = a.vnorm[gi];
+          if (retire) {
+            b.rz[k] = rws[2 * ic];
+            b.rn[k] = rws[2 * ic + 1];
           }
         }
-        if (valid) {
-          a.alpha[gi] = al;
-          a.den[gi] = de;
-          a.num[gi] = nu;
+      }
+    };
+    Batch cur, nxt;
+    load_batch(0, cur);
+    for (int kb = 0; kb < nslots; kb += S_KB) {
+      if (kb + S_KB < nslots) load_batch(kb + S_KB, nxt);
+      const int kact = kact_of(kb);
+      float x[S_KB][4];
+      int32_t pk[S_KB];
+#pragma unroll
+      for (int k = 0; k < S_KB; ++k) {
+        if (k < kact) {
+          const int i = (kb + k) * SNT + tid;
+          const bool valid = i < L;
+          const int ic = valid ? i : L - 1;
+          const size_t gi = ub + ic;
+          float w[G];
+#pragma unroll
+          for (int j = 0; j < G; ++j) w[j] = sbuf[ic * RS + j] * invl[j];
+          float cz, cn;
+          contrib_from_weights<G>(w, H, cz, cn);
+          float al, vn;
+          double nu, de;
+          int32_t ps;
           if (ic == newrow) {
-            a.pos[gi] = ps;
-            a.vnorm[gi] = vn;
+            al = cz * invG;
+            de = (double)cz;
+            nu = (double)cn;
+            ps = a.T - 1;
+            vn = newnorm;
+          } else {
+            al = cur.al[k] + cz * invG;
+            de = cur.de[k] + (double)cz;
+            nu = cur.nu[k] + (double)cn;
+            ps = cur.p[k];
+            vn = cur.vn[k];
+            if (retire && ps <= a.pmax_ret) {
+              de = de - (double)cur.rz[k];
+              nu = nu - (double)cur.rn[k];
+            }
+          }
+          if (valid) {
+            a.alpha[gi] = al;
+            a.den[gi] = de;
+            a.num[gi] = nu;
+            if (ic == newrow) {
+              a.pos[gi] = ps;
+              a.vnorm[gi] = vn;
+            }
+          }
+          make_features(al, vn, nu, de, ps, invT, x[k]);
+          pk[k] = ps;
+        }
+      }
+      if constexpr (EVICT) {
+        float sc[S_KB];
+        policy_scores<S_KB, NH>(e, x, sc, kact);
+#pragma unroll
+        for (int k = 0; k < S_KB; ++k) {
+          const int i = (kb + k) * SNT + tid;
+          if (k < kact && i < L) {
+            if (e.scores_out) e.scores_out[(size_t)u * L + i] = sc[k];
+            keys[(size_t)i * KS] = row_key(sc[k], pk[k]);
           }
         }
-        make_features(al, vn, nu, de, ps, invT, x[k]);
-        pk[k] = ps;
       }
+      cur = nxt;
     }
     if (a.window > 0) write_ring2<D, G>(a, u, M, invl, H);
     if constexpr (EVICT) {
-      // (3) policy scores and ranking keys
-      float sc[KP];
-      policy_scores<KP, NH>(e, x, sc, kact);
-#pragma unroll
-      for (int k = 0; k < KP; ++k) {
-        const int i = k * SNT + tid;
-        if (k < kact && i < L) {
-          if (e.scores_out) e.scores_out[(size_t)u * L + i] = sc[k];
-          keys[i] = row_key(sc[k], pk[k]);
-        }
-      }
       __syncthreads();
       if (e.evict) {
-        LdsKeys<S_KMAX> lk{keys};
-        select_compact<LdsKeys<S_KMAX>, 1, D>(e, u, lk, (L + SNT - 1) / SNT, sh, mv);
+        LdsKeys<S_KMAX, SNT> lk{keys, KS};
+        select_compact<LdsKeys<S_KMAX, SNT>, 1, D, SNT>(e, u, lk, nslots, sh, mv);
       } else if (e.kept_out) {
         for (int r = tid; r < L; r += SNT) e.kept_out[(size_t)u * L + r] = r;
       }
@@ -693,7 +735,8 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
 
 // ---------------------------------------------------------------- dispatch
 size_t step_lds_bytes(int L, int G, int D, bool feat, int nmoves) {
-  const size_t b = ((size_t)L * G + (feat ? 2 * (size_t)L : 0) + (size_t)SNW * G * D) * sizeof(float);
+  const size_t rs = G < 2 ? 2 : G;
+  const size_t b = ((size_t)L * rs + (size_t)(SNW / 2) * G * D) * sizeof(float);
   return b + (size_t)2 * (nmoves > 0 ? nmoves : 1) * sizeof(int);
 }
 
