@@ -17,6 +17,7 @@ from __future__ import annotations
 import argparse
 import json
 import os
+import re
 import sys
 import time
 
@@ -27,20 +28,20 @@ METRIC = "decode steps/s + KV GB/s (% of 8 TB/s HBM) for attention+evict at 16k 
 HBM_PEAK_GBPS = 8000.0
 
 
-def decode_alg_bytes(U, L, G, D, elt, append, retire):
-    """Algorithmic HBM bytes of one decode-step launch (every unit):
-    K/V rows read once (L - append rows from the cache; the appended row arrives
-    in k_new/v_new and is written once), feature state read+write (alpha f32,
-    num/den f64: 40 B/row; pos read 4 B/row when the window retires; vnorm
-    written 4 B/row), queries read, outputs written, the ring slot's queries read
-    (when retiring) and written, per-query statistics."""
+def step_alg_bytes(U, L, G, D, elt, retire, moved):
+    """Algorithmic HBM bytes of one fused decode step over U units of L rows
+    (after the append): every cached K/V row read once (L - 1 rows; the new row
+    arrives in k_new/v_new, read once and written to the cache once); per row the
+    feature state read and written (alpha f32 and num/den f64: 40 B) plus pos and
+    ||v|| read (8 B); the queries read and outputs written; the retiring ring
+    queries read and this step's queries written to the ring (1 KB each), the
+    per-query statistics; compaction moves read and write the K/V row and its
+    28 bytes of state."""
     row = 2 * D * elt
-    per_unit = (L - append) * row
-    per_unit += append * 2 * row                     # k_new/v_new read + cache write
-    per_unit += L * (40 + 4) + (L * 4 if retire else 0)
     qbytes = G * D * elt
-    per_unit += 2 * qbytes + qbytes + (qbytes if retire else 0) + 2 * G * 3 * 4
-    return U * per_unit
+    per_unit = (L - 1) * row + 2 * row + L * 48
+    per_unit += 2 * qbytes + (qbytes if retire else 0) + qbytes + 2 * G * 3 * 4
+    return U * per_unit + moved * 2 * (row + 28)
 
 
 def evict_alg_bytes(U, L, moved, D, elt):
@@ -54,6 +55,34 @@ def kv_bytes(U, L, D, elt, moved, append=1):
     K/V part of the compaction moves (read + write)."""
     row = 2 * D * elt
     return U * ((L - append) * row + append * 2 * row) + moved * 2 * row
+
+
+STEP_KERNEL_SOURCES = ("dc_step.hip", "dc_select.hpp", "dc_device.hpp", "dc_kernels.hpp")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "step_unit_kernel_c3_hbm_counters.md")
+
+
+def step_kernel_source_hash():
+    import hashlib
+    h = hashlib.sha256()
+    for f in STEP_KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2608_08878_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the fused step kernel from the committed
+    FETCH_SIZE/WRITE_SIZE counter runs (copy-kernel calibrated), or None when the
+    kernel sources changed after the counters were taken."""
+    try:
+        text = open(TRAFFIC_PROFILE).read()
+    except OSError:
+        return None
+    tb = re.search(r"traffic_bytes_per_launch: (\d+)", text)
+    hs = re.search(r"kernel source sha256\[:16\]: ([0-9a-f]+)", text)
+    if not tb or not hs or hs.group(1) != step_kernel_source_hash():
+        return None
+    return int(tb.group(1))
 
 
 def run_oracle_baseline(wl, units, steps, seed_units=0):
@@ -187,7 +216,7 @@ def main():
     moved = int((kept != torch.arange(wl.budget, device=dev, dtype=torch.int32)[None, :]).sum())
 
     retire = True
-    step_bytes = decode_alg_bytes(U, L_steady, G, D, elt, 1, retire) + moved * 2 * (2 * D * elt + 28)
+    step_bytes = step_alg_bytes(U, L_steady, G, D, elt, retire, moved)
     kvb = kv_bytes(U, L_steady, D, elt, moved)
     steps_per_s = 1e3 / ms_per_step
     step_gbps = step_bytes / (step_ms * 1e-3) / 1e9
@@ -216,7 +245,8 @@ def main():
         "first_step_ms": round(first_ms, 3),
         "roofline": {"bound": "hbm", "kernel": "step_unit_kernel (attention + features + score + select + compact)",
                      "achieved": round(step_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(step_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
+                     "traffic": measured_traffic() if wl.name == W.WORKLOADS[3].name else None,
                      "alg_bytes_per_launch": step_bytes},
     }
     if not args.no_cpu_baseline:
