@@ -36,10 +36,16 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int nchunks_of(int L) { return (L + dc::decode_chunk_rows() - 1) / dc::decode_chunk_rows(); }
 
+// Per-unit row stride of the decode scratch: L rows plus padding that takes the
+// stores of lanes past the last row (so those stores need no branch), rounded
+// to 32 rows so that every unit's rows start on a 256-byte boundary (a 16-row
+// tile of retired pairs is then exactly one 128-byte line).
+int scratch_rows(int L) { return (L + 8 + 31) / 32 * 32; }
+
 // Scratch of the chunked decode path for caches of L rows.
 size_t split_bytes(const dc_dims* d, int L) {
   const size_t U = (size_t)units_of(d), G = group_of(d), D = d->head_dim;
-  const size_t rows = U * (size_t)L * (G + 3) * sizeof(float);
+  const size_t rows = U * (size_t)scratch_rows(L) * (G + 3) * sizeof(float);
   const size_t parts = U * (size_t)nchunks_of(L) * (3 * G + G * D) * sizeof(float);
   return align256(rows) + align256(parts);
 }
@@ -151,7 +157,8 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
     split = use_split(dims, L, feat != nullptr);
   // the matrix-core unit path parks each row's retired (cz, cn) in the workspace
   const bool unit_scratch = dims->dtype == DC_BF16 && feat && !split;
-  need = split ? split_bytes(dims, L) : unit_scratch ? align256((size_t)U * L * 2 * sizeof(float)) : 0;
+  need = split ? split_bytes(dims, L)
+         : unit_scratch ? align256((size_t)U * scratch_rows(L) * 2 * sizeof(float)) : 0;
   if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
 
   memset(&a, 0, sizeof(a));
@@ -185,12 +192,12 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   }
   if (unit_scratch) {
     a.ws_r = (float*)ws;
-    a.lmax = L;
+    a.lmax = scratch_rows(L);
   }
   if (split) {
-    const size_t rows = (size_t)U * L;
+    const size_t rows = (size_t)U * scratch_rows(L);
     float* base = (float*)ws;
-    a.lmax = L;
+    a.lmax = scratch_rows(L);
     a.chunk = dc::decode_chunk_rows();
     a.nchunks = nchunks_of(L);
     a.ws_s = base;

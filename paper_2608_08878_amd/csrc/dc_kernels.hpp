@@ -36,7 +36,8 @@ struct DecodeArgs {
   float* ws_r;          // [units][lmax][2] retired contributions
   float* ws_v;          // [units][lmax] value norms
   float* ws_part;       // [units][nchunks][3G + G*D] per-chunk softmax partials
-  int lmax;
+  int lmax;             // row stride of the scratch per unit: L + 8 rounded up to 32 (rows
+                        // past L are padding that absorbs the stores of lanes without a row)
   int chunk;
   int nchunks;
 };

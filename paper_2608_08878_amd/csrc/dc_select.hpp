@@ -38,29 +38,24 @@ __device__ __forceinline__ void load_features(const EvictArgs& a, size_t gi, flo
   make_features(a.alpha[gi], a.vnorm[gi], a.num[gi], a.den[gi], p, invT, x);
 }
 
-// s = f_phi(x), float32, fixed evaluation order.
-__device__ __forceinline__ float mlp1(const float* __restrict__ P, int h1, const float x[4]) {
-  const float* W1 = P;
-  const float* b1 = P + 4 * h1;
-  const float* wo = b1 + h1;
-  float out = wo[h1];
-  for (int h = 0; h < h1; ++h) {
-    float z = b1[h];
-    z = __builtin_fmaf(W1[4 * h + 0], x[0], z);
-    z = __builtin_fmaf(W1[4 * h + 1], x[1], z);
-    z = __builtin_fmaf(W1[4 * h + 2], x[2], z);
-    z = __builtin_fmaf(W1[4 * h + 3], x[3], z);
-    out = __builtin_fmaf(wo[h], fmaxf(z, 0.0f), out);
-  }
-  return out;
+// Policy parameters are read through the constant address space: no kernel
+// writes them, so each load is a scalar load issued once per wave instead of a
+// vector load per lane (which would compete with the cache streams for the
+// vector memory pipeline).
+typedef __attribute__((address_space(4))) const float cfloat;
+
+__device__ __forceinline__ const cfloat* const_params(const float* p) {
+  return (const cfloat*)p;
 }
 
-__device__ __forceinline__ float mlp2(const float* __restrict__ P, int h1, int h2, const float x[4]) {
-  const float* W1 = P;
-  const float* b1 = P + 4 * h1;
-  const float* W2 = b1 + h1;
-  const float* b2 = W2 + h2 * h1;
-  const float* wo = b2 + h2;
+// s = f_phi(x) for a 4 -> h1 -> h2 -> 1 ReLU MLP (two hidden layers), float32,
+// fixed evaluation order (bias first, then the inputs in order).
+__device__ __forceinline__ float mlp2(const cfloat* P, int h1, int h2, const float x[4]) {
+  const cfloat* W1 = P;
+  const cfloat* b1 = P + 4 * h1;
+  const cfloat* W2 = b1 + h1;
+  const cfloat* b2 = W2 + h2 * h1;
+  const cfloat* wo = b2 + h2;
   float hv[MAX_H1_2L];
 #pragma unroll
   for (int h = 0; h < MAX_H1_2L; ++h) {
@@ -77,7 +72,7 @@ __device__ __forceinline__ float mlp2(const float* __restrict__ P, int h1, int h
   }
   float out = wo[h2];
   for (int o = 0; o < h2; ++o) {
-    const float* w = W2 + o * h1;
+    const cfloat* w = W2 + o * h1;
     float z = b2[o];
 #pragma unroll
     for (int h = 0; h < MAX_H1_2L; ++h)
@@ -87,41 +82,50 @@ __device__ __forceinline__ float mlp2(const float* __restrict__ P, int h1, int h
   return out;
 }
 
-__device__ __forceinline__ float policy_score(const EvictArgs& a, const float x[4]) {
-  return a.nh == 1 ? mlp1(a.params, a.h1, x) : mlp2(a.params, a.h1, a.h2, x);
+// One hidden unit of the one-hidden-layer MLP for KP rows.
+template <int KP>
+__device__ __forceinline__ void mlp1_unit(const cfloat* W1, const cfloat* b1, const cfloat* wo,
+                                          int h, const float (&x)[KP][4], float (&out)[KP],
+                                          int kact) {
+  const float w0 = W1[4 * h], w1 = W1[4 * h + 1], w2 = W1[4 * h + 2], w3 = W1[4 * h + 3];
+  const float bb = b1[h], ww = wo[h];
+#pragma unroll
+  for (int k = 0; k < KP; ++k) {
+    if (k < kact) {
+      float z = bb;
+      z = __builtin_fmaf(w0, x[k][0], z);
+      z = __builtin_fmaf(w1, x[k][1], z);
+      z = __builtin_fmaf(w2, x[k][2], z);
+      z = __builtin_fmaf(w3, x[k][3], z);
+      out[k] = __builtin_fmaf(ww, fmaxf(z, 0.0f), out[k]);
+    }
+  }
 }
 
-// Scores of KP rows per thread.  Row slots k >= kact (uniform over the wave)
-// are skipped; the loops over the hidden units are uniform, so the weights are
-// read once per wave into scalar registers and reused for every row slot.  The
-// arithmetic (order of the fused multiply-adds) is that of mlp1 / mlp2.
+// Scores of KP rows per thread, s = f_phi(x) in float32 with a fixed evaluation
+// order: out = b_out, then for every hidden unit h in order
+// out += w_out[h] relu(b1[h] + W1[h,0] x0 + W1[h,1] x1 + W1[h,2] x2 + W1[h,3] x3)
+// (for two hidden layers see mlp2).  Row slots k >= kact (uniform over the
+// wave) are skipped.  The loops over the hidden units are uniform, so every
+// weight is read once per wave and reused for all row slots.
 template <int KP, int NH>
 __device__ __forceinline__ void policy_scores(const EvictArgs& a, const float (&x)[KP][4],
                                               float (&out)[KP], int kact) {
-  const float* __restrict__ P = a.params;
+  const cfloat* P = const_params(a.params);
   if constexpr (NH == 1) {
     const int h1 = a.h1;
-    const float* W1 = P;
-    const float* b1 = P + 4 * h1;
-    const float* wo = b1 + h1;
+    const cfloat* W1 = P;
+    const cfloat* b1 = P + 4 * h1;
+    const cfloat* wo = b1 + h1;
     const float bo = wo[h1];
 #pragma unroll
     for (int k = 0; k < KP; ++k) out[k] = bo;
-    for (int h = 0; h < h1; ++h) {
-      const float w0 = W1[4 * h], w1 = W1[4 * h + 1], w2 = W1[4 * h + 2], w3 = W1[4 * h + 3];
-      const float bb = b1[h], ww = wo[h];
+    int h = 0;
+    for (; h + 4 <= h1; h += 4) {       // four units per trip: the scalar loads batch up
 #pragma unroll
-      for (int k = 0; k < KP; ++k) {
-        if (k < kact) {
-          float z = bb;
-          z = __builtin_fmaf(w0, x[k][0], z);
-          z = __builtin_fmaf(w1, x[k][1], z);
-          z = __builtin_fmaf(w2, x[k][2], z);
-          z = __builtin_fmaf(w3, x[k][3], z);
-          out[k] = __builtin_fmaf(ww, fmaxf(z, 0.0f), out[k]);
-        }
-      }
+      for (int q = 0; q < 4; ++q) mlp1_unit<KP>(W1, b1, wo, h + q, x, out, kact);
     }
+    for (; h < h1; ++h) mlp1_unit<KP>(W1, b1, wo, h, x, out, kact);
   } else {
 #pragma unroll
     for (int k = 0; k < KP; ++k)

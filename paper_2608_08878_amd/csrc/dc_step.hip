@@ -28,7 +28,6 @@ constexpr int SNT = 512;              // threads per workgroup (two workgroups p
 constexpr int SNW = SNT / 64;
 constexpr int SCHUNK = 2048;          // rows per workgroup on the chunked path
 constexpr int S_KMAX = 10;            // fused step: row slots per thread (L <= 5120)
-constexpr int S_KB = 3;               // row slots per thread handled per feature batch
 constexpr int S_LDS = 160 * 1024 - 4 * 1024;  // dynamic LDS budget (static LDS aside)
 
 template <int D>
@@ -88,14 +87,21 @@ __device__ __forceinline__ void load_ret(RetStats<G>& r, const DecodeArgs& a, in
 }
 
 // ---------------------------------------------------------------- pass A
-// Rows [r0, r1) of unit u, 16-key tiles distributed over the waves.  Logits of
-// the current heads go to s_sink[(i - sink0) * G + j], retired contributions to
-// r_sink[2 (i - sink0)], running maxima per current head into mrun.
-template <int D, int G, bool FEAT, int RS = G>
+// Rows [r0, r1) of unit u in 16-key tiles.  Logits of the current heads go to
+// s_sink[(i - sink0) * RS + j], running maxima per current head into mrun.  The
+// retired contributions (z, n) of each key are either stored to
+// r_sink[2 (i - sink0)] (tiles round-robin over the waves; chunked path) or, with
+// GROUPED, kept in registers: rows then go in groups of 64 (four tiles), group
+// b to wave b mod SNW, and after a group lane l of the wave holds the pair of
+// the group's row l, in zr[k] / nr[k] for the wave's k-th group.
+constexpr int S_GMAX = S_KMAX;        // 64-row groups per wave, at most (L <= 5120)
+
+template <int D, int G, bool FEAT, bool GROUPED, int RS = G>
 __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r1, float* s_sink,
                                        float* r_sink, int sink0, const uint4 (&qa)[MG<D>::NT],
-                                       bool retire, const RetStats<G>& rs, float (&mrun)[4]) {
-  constexpr int NT = MG<D>::NT, LB = MG<D>::LB;
+                                       bool retire, const RetStats<G>& rs, float (&mrun)[4],
+                                       float (&zr)[S_GMAX], float (&nr)[S_GMAX]) {
+  constexpr int NT = MG<D>::NT;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, i = lane & 15, g = lane >> 4;
   const char* kc = (const char*)a.k + (size_t)u * a.cap * D * 2;
   const char* kn = a.append ? (const char*)a.k_new + (size_t)u * D * 2 : nullptr;
@@ -103,6 +109,7 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
   const int ntiles = (r1 - r0 + 15) / 16;
 #pragma unroll
   for (int r = 0; r < 4; ++r) mrun[r] = NEG_BIG;
+  auto clamp_tile = [&](int t) { return t < ntiles ? t : ntiles - 1; };
   auto load_tile = [&](int tile, uint4 (&kb)[NT]) {
     int key = r0 + tile * 16 + i;
     key = key < r1 ? key : r1 - 1;
@@ -112,7 +119,9 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
 #pragma unroll
     for (int t = 0; t < NT; ++t) kb[t] = ldg16(kp + 16 * (4 * t + g));
   };
-  auto process = [&](int tt, const uint4 (&kb)[NT]) {
+  // logits of tile tt; returns the retired pair of key (tile row i) in lanes
+  // 32 + i (zero elsewhere or without a retiring step)
+  auto process = [&](int tt, const uint4 (&kb)[NT], float& z, float& n) {
     f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int t = 0; t < NT; ++t)
@@ -137,10 +146,11 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
         for (int r = 0; r < G; ++r) dst[r] = s[r];
       }
     }
+    z = 0.0f;
+    n = 0.0f;
     if constexpr (FEAT) {
       if (retire && g >= 2 && 4 * (g - 2) < G) {
         const bool hi = G > 4 && g == 3;        // heads 4..7 (only when G == 8)
-        float z = 0.0f, n = 0.0f;
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           constexpr int last = G - 1;
@@ -154,28 +164,89 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
             n = n + w * hh;
           }
         }
-        if constexpr (G > 4) {   // heads 4..7 live in group 3: add the blocks in order
-          const float z1 = __shfl_down(z, 16), n1 = __shfl_down(n, 16);
-          z = z + z1;
-          n = n + n1;
-        }
-        if (g == 2 && valid) {
-          r_sink[2 * (key - sink0)] = z;
-          r_sink[2 * (key - sink0) + 1] = n;
-        }
+      }
+      if constexpr (G > 4) {     // heads 4..7 live in group 3: add the blocks in order
+        const float z1 = __shfl_down(z, 16), n1 = __shfl_down(n, 16);
+        z = z + z1;
+        n = n + n1;
       }
     }
   };
-  // two tiles in flight per wave: consume a buffer, then refill it
-  uint4 kb0[NT], kb1[NT];
-  if (wave < ntiles) load_tile(wave, kb0);
-  if (wave + SNW < ntiles) load_tile(wave + SNW, kb1);
-  for (int tile = wave; tile < ntiles; tile += 2 * SNW) {
-    process(tile, kb0);
-    if (tile + 2 * SNW < ntiles) load_tile(tile + 2 * SNW, kb0);
-    if (tile + SNW < ntiles) {
-      process(tile + SNW, kb1);
-      if (tile + 3 * SNW < ntiles) load_tile(tile + 3 * SNW, kb1);
+  // Two tiles in flight per wave: consume a buffer, then refill it.  Every load
+  // is issued unconditionally (a tile past the end re-reads the last tile, which
+  // the cache serves), so the wait before a tile's MFMAs covers only that
+  // tile's loads and never drains the other buffer.
+  if constexpr (GROUPED) {
+    const int ngrp = (ntiles + 3) / 4;
+    const int ngw = wave < ngrp ? (ngrp - 1 - wave) / SNW + 1 : 0;
+#pragma unroll
+    for (int k = 0; k < S_GMAX; ++k) {
+      zr[k] = 0.0f;
+      nr[k] = 0.0f;
+    }
+    if (ngw > 0) {
+      uint4 kb0[NT], kb1[NT];
+      load_tile(4 * wave, kb0);
+      load_tile(clamp_tile(4 * wave + 1), kb1);
+      for (int k = 0; k < ngw; ++k) {
+        const int t0 = 4 * (wave + SNW * k), tn = t0 + 4 * SNW;
+        float zz = 0.0f, nn = 0.0f;
+        // tile j's pairs (lanes 32..47) move to lanes 16 j .. 16 j + 15
+        auto take = [&](int j, float z, float n) {
+          const float zj = __shfl(z, 32 + i), nj = __shfl(n, 32 + i);
+          zz = g == j ? zj : zz;
+          nn = g == j ? nj : nn;
+        };
+        float z, n;
+        process(t0, kb0, z, n);
+        if constexpr (FEAT) take(0, z, n);
+        load_tile(clamp_tile(t0 + 2), kb0);
+        process(t0 + 1, kb1, z, n);
+        if constexpr (FEAT) take(1, z, n);
+        load_tile(clamp_tile(t0 + 3), kb1);
+        process(t0 + 2, kb0, z, n);
+        if constexpr (FEAT) take(2, z, n);
+        load_tile(clamp_tile(tn), kb0);
+        process(t0 + 3, kb1, z, n);
+        if constexpr (FEAT) take(3, z, n);
+        load_tile(clamp_tile(tn + 1), kb1);
+        if constexpr (FEAT) {
+#pragma unroll
+          for (int s2 = 0; s2 < S_GMAX; ++s2) {
+            zr[s2] = s2 == k ? zz : zr[s2];
+            nr[s2] = s2 == k ? nn : nr[s2];
+          }
+        }
+      }
+    }
+  } else if (wave < ntiles) {
+    uint4 kb0[NT], kb1[NT];
+    load_tile(wave, kb0);
+    // the loop stores one retired pair per tile between the two buffers' loads;
+    // a store to the padding row here gives the loop's first wait the same
+    // sequence of outstanding operations as every later one
+    if constexpr (FEAT) *reinterpret_cast<float2*>(r_sink + 2 * (size_t)(a.lmax - 1 - sink0)) = make_float2(0.0f, 0.0f);
+    load_tile(clamp_tile(wave + SNW), kb1);
+    // every lane stores (a store under a branch would make the wait before the
+    // next tile's matrix ops cover it too); lanes without a retired row of their
+    // own write the padding row past the unit
+    auto sink = [&](int tt, float z, float n) {
+      if constexpr (FEAT) {
+        const int key = r0 + tt * 16 + i;
+        const int slot = (retire && g == 2 && key < r1) ? key - sink0 : a.lmax - 1 - sink0;
+        *reinterpret_cast<float2*>(r_sink + 2 * (size_t)slot) = make_float2(z, n);
+      }
+    };
+    for (int tile = wave; tile < ntiles; tile += 2 * SNW) {
+      float z, n;
+      process(tile, kb0, z, n);
+      sink(tile, z, n);
+      load_tile(clamp_tile(tile + 2 * SNW), kb0);
+      // unconditional: a tile past the end has no valid key, so it writes no
+      // logits and sends its retired pair to the padding row
+      process(tile + SNW, kb1, z, n);
+      sink(tile + SNW, z, n);
+      load_tile(clamp_tile(tile + 3 * SNW), kb1);
     }
   }
 }
@@ -263,7 +334,7 @@ template <int D, int G, int RS = G>
 __device__ __forceinline__ void pass_b(const DecodeArgs& a, int u, int r0, int r1,
                                        const float* pbuf, int p0, float (&o)[G][8]) {
   constexpr int LPR = MG<D>::LPR, NG = SNT / LPR;
-  constexpr int PF = 4;
+  constexpr int PF = 8;
   const int tid = threadIdx.x, grp = tid / LPR, lam = tid % LPR;
   const char* vc = (const char*)a.v + (size_t)u * a.cap * D * 2;
   const char* vn = a.append ? (const char*)a.v_new + (size_t)u * D * 2 : nullptr;
@@ -281,8 +352,17 @@ __device__ __forceinline__ void pass_b(const DecodeArgs& a, int u, int r0, int r
     const bool ok = row < r1;
     const int rc = ok ? row : r1 - 1;
     float pj[G];
+    if constexpr (RS == 4 && G == 4) {
+      const f32x4_t w = *reinterpret_cast<const f32x4_t*>(pbuf + (size_t)(rc - p0) * RS);
 #pragma unroll
-    for (int j = 0; j < G; ++j) pj[j] = ok ? pbuf[(size_t)(rc - p0) * RS + j] : 0.0f;
+      for (int j = 0; j < G; ++j) pj[j] = ok ? w[j] : 0.0f;
+    } else {
+#pragma unroll
+      for (int j = 0; j < G; ++j) {
+        const float w = pbuf[(size_t)(rc - p0) * RS + j];
+        pj[j] = ok ? w : 0.0f;
+      }
+    }
     float vf[8];
     unpack_slice<1>(vv, vf);
 #pragma unroll
@@ -292,19 +372,29 @@ __device__ __forceinline__ void pass_b(const DecodeArgs& a, int u, int r0, int r
   };
   const int nrows = r1 - r0;
   const int iters = (nrows + NG - 1) / NG;      // row slots per group (uniform)
+  // Two halves of PF/2 rows per group in flight.  The loads are unconditional
+  // (past the end they re-read the last row), and the scheduling barrier keeps
+  // each half's refill between the halves, so while one half is consumed the
+  // other half's loads are still outstanding; the last iters % PF rows are
+  // consumed after the loop without new loads.
+  constexpr int HF = PF / 2;
   uint4 vb[PF];
 #pragma unroll
-  for (int p = 0; p < PF; ++p)
-    if (p < iters) vb[p] = load_row(r0 + grp + p * NG);
-  for (int it = 0; it < iters; it += PF) {
+  for (int p = 0; p < PF; ++p) vb[p] = load_row(r0 + grp + p * NG);
+  const int full = iters / PF;
+  for (int f = 0; f < full; ++f) {
 #pragma unroll
-    for (int p = 0; p < PF; ++p) {
-      if (it + p < iters) {
-        accumulate(r0 + grp + (it + p) * NG, vb[p]);
-        if (it + p + PF < iters) vb[p] = load_row(r0 + grp + (it + p + PF) * NG);
-      }
+    for (int h = 0; h < 2; ++h) {
+#pragma unroll
+      for (int q = 0; q < HF; ++q) accumulate(r0 + grp + (f * PF + h * HF + q) * NG, vb[h * HF + q]);
+#pragma unroll
+      for (int q = 0; q < HF; ++q) vb[h * HF + q] = load_row(r0 + grp + ((f + 1) * PF + h * HF + q) * NG);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
+#pragma unroll
+  for (int p = 0; p < PF; ++p)
+    if (full * PF + p < iters) accumulate(r0 + grp + (full * PF + p) * NG, vb[p]);
 #pragma unroll
   for (int off = LPR; off < 64; off *= 2)
 #pragma unroll
@@ -417,7 +507,7 @@ struct RowStride {
 };
 
 template <int D, int G, bool FEAT, bool EVICT, int NH>
-__global__ void __launch_bounds__(SNT, 2) step_unit_kernel(DecodeArgs a, EvictArgs e) {
+__global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_kernel(DecodeArgs a, EvictArgs e) {
   constexpr int LPR = MG<D>::LPR;
   constexpr int RS = RowStride<G>::RS, KS = RowStride<G>::KS;
   extern __shared__ float lds[];
@@ -429,19 +519,19 @@ __global__ void __launch_bounds__(SNT, 2) step_unit_kernel(DecodeArgs a, EvictAr
   float* sbuf = lds;                                  // row stride RS
   float* obuf = lds + (size_t)L * RS;                 // (SNW / 2) * G * D
   int* mv = (int*)(obuf + (SNW / 2) * G * D);
-  float* rws = FEAT ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr;
   const size_t ub = (size_t)u * a.cap;
 
   if (a.append) append_rows<D>(a, u);
   const bool retire = FEAT && a.retire;
   float M[G], invl[G], H[G];
+  float zr[S_GMAX], nr[S_GMAX];     // retired pairs of the wave's 64-row groups (lane = row)
   {
     uint4 qa[MG<D>::NT];
     load_qfrag<D, G>(qa, a, u, retire);
     RetStats<G> rs;
     if (retire) load_ret<G>(rs, a, u);
     float mrun[4];
-    pass_a<D, G, FEAT, RS>(a, u, 0, L, sbuf, rws, 0, qa, retire, rs, mrun);
+    pass_a<D, G, FEAT, true, RS>(a, u, 0, L, sbuf, nullptr, 0, qa, retire, rs, mrun, zr, nr);
     block_max<G>(mrun, stat, M);
   }
   {
@@ -492,106 +582,101 @@ __global__ void __launch_bounds__(SNT, 2) step_unit_kernel(DecodeArgs a, EvictAr
     const float invT = 1.0f / (float)a.T;
     constexpr float invG = 1.0f / G;
     uint64_t* keys = reinterpret_cast<uint64_t*>(sbuf);   // row i's key replaces its weights
-    const int nslots = (L + SNT - 1) / SNT;
-    struct Batch {
-      float al[S_KB], vn[S_KB], rz[S_KB], rn[S_KB];
-      double nu[S_KB], de[S_KB];
-      int32_t p[S_KB];
+    // The rows of pass A's 64-row groups, one per lane: group b (wave b mod SNW)
+    // row 64 b + lane, whose retired pair this lane kept in registers.  The next
+    // group's state is requested before the current one is updated; in full
+    // groups every load and store is unconditional, only the unit's partial last
+    // group (one wave) guards its stores.
+    const int ngrp = (L + 63) / 64;
+    const int ngw = wave < ngrp ? (ngrp - 1 - wave) / SNW + 1 : 0;
+    const bool part = ngw > 0 && wave + SNW * (ngw - 1) == ngrp - 1 && (L & 63) != 0;
+    const int nfull = ngw - (part ? 1 : 0);
+    struct Row {
+      float al, vn;
+      double nu, de;
+      int32_t p;
     };
-    auto kact_of = [&](int kb) {
-      const int rem = L - kb * SNT - wave * 64;   // slots with a valid row in this wave
-      return rem > 0 ? min(S_KB, (rem + SNT - 1) / SNT) : 0;
+    auto load_row = [&](int k, Row& x) {
+      const int r = 64 * (wave + SNW * k) + lane;
+      const size_t gi = ub + (r < L ? r : L - 1);
+      x.al = a.alpha[gi];
+      x.nu = a.num[gi];
+      x.de = a.den[gi];
+      x.p = a.pos[gi];
+      x.vn = a.vnorm[gi];
     };
-    auto load_batch = [&](int kb, Batch& b) {
-      const int kact = kact_of(kb);
+    auto update = [&](int k, const Row& x, bool guard) {
+      const int r = 64 * (wave + SNW * k) + lane;
+      const bool valid = r < L;
+      const int ic = valid ? r : L - 1;
+      const size_t gi = ub + ic;
+      float w[G];
 #pragma unroll
-      for (int k = 0; k < S_KB; ++k) {
-        if (k < kact) {
-          const int i = (kb + k) * SNT + tid;
-          const int ic = i < L ? i : L - 1;
-          const size_t gi = ub + ic;
-          b.al[k] = a.alpha[gi];
-          b.nu[k] = a.num[gi];
-          b.de[k] = a.den[gi];
-          b.p[k] = a.pos[gi];
-          b.vn[k] = a.vnorm[gi];
-          if (retire) {
-            b.rz[k] = rws[2 * ic];
-            b.rn[k] = rws[2 * ic + 1];
-          }
-        }
+      for (int j = 0; j < G; ++j) w[j] = sbuf[ic * RS + j] * invl[j];
+      float cz, cn;
+      contrib_from_weights<G>(w, H, cz, cn);
+      float rz = zr[0], rn = nr[0];
+#pragma unroll
+      for (int s2 = 1; s2 < S_GMAX; ++s2) {
+        rz = s2 == k ? zr[s2] : rz;
+        rn = s2 == k ? nr[s2] : rn;
       }
-    };
-    Batch cur, nxt;
-    load_batch(0, cur);
-    for (int kb = 0; kb < nslots; kb += S_KB) {
-      if (kb + S_KB < nslots) load_batch(kb + S_KB, nxt);
-      const int kact = kact_of(kb);
-      float x[S_KB][4];
-      int32_t pk[S_KB];
-#pragma unroll
-      for (int k = 0; k < S_KB; ++k) {
-        if (k < kact) {
-          const int i = (kb + k) * SNT + tid;
-          const bool valid = i < L;
-          const int ic = valid ? i : L - 1;
-          const size_t gi = ub + ic;
-          float w[G];
-#pragma unroll
-          for (int j = 0; j < G; ++j) w[j] = sbuf[ic * RS + j] * invl[j];
-          float cz, cn;
-          contrib_from_weights<G>(w, H, cz, cn);
-          float al, vn;
-          double nu, de;
-          int32_t ps;
-          if (ic == newrow) {
-            al = cz * invG;
-            de = (double)cz;
-            nu = (double)cn;
-            ps = a.T - 1;
-            vn = newnorm;
-          } else {
-            al = cur.al[k] + cz * invG;
-            de = cur.de[k] + (double)cz;
-            nu = cur.nu[k] + (double)cn;
-            ps = cur.p[k];
-            vn = cur.vn[k];
-            if (retire && ps <= a.pmax_ret) {
-              de = de - (double)cur.rz[k];
-              nu = nu - (double)cur.rn[k];
-            }
-          }
-          if (valid) {
-            a.alpha[gi] = al;
-            a.den[gi] = de;
-            a.num[gi] = nu;
-            if (ic == newrow) {
-              a.pos[gi] = ps;
-              a.vnorm[gi] = vn;
-            }
-          }
-          make_features(al, vn, nu, de, ps, invT, x[k]);
-          pk[k] = ps;
-        }
+      float al = x.al + cz * invG;
+      double de = x.de + (double)cz;
+      double nu = x.nu + (double)cn;
+      int32_t ps = x.p;
+      float vn = x.vn;
+      if (retire && ps <= a.pmax_ret) {
+        de = de - (double)rz;
+        nu = nu - (double)rn;
+      }
+      if (ic == newrow) {
+        al = cz * invG;
+        de = (double)cz;
+        nu = (double)cn;
+        ps = a.T - 1;
+        vn = newnorm;
+      }
+      if (!guard || valid) {
+        a.alpha[gi] = al;
+        a.den[gi] = de;
+        a.num[gi] = nu;
       }
       if constexpr (EVICT) {
-        float sc[S_KB];
-        policy_scores<S_KB, NH>(e, x, sc, kact);
-#pragma unroll
-        for (int k = 0; k < S_KB; ++k) {
-          const int i = (kb + k) * SNT + tid;
-          if (k < kact && i < L) {
-            if (e.scores_out) e.scores_out[(size_t)u * L + i] = sc[k];
-            keys[(size_t)i * KS] = row_key(sc[k], pk[k]);
-          }
-        }
+        float f[1][4], sc[1];
+        make_features(al, vn, nu, de, ps, invT, f[0]);
+        policy_scores<1, NH>(e, f, sc, 1);
+        if (!guard || valid) keys[(size_t)r * KS] = row_key(sc[0], ps);
       }
-      cur = nxt;
+    };
+    if (ngw > 0) {
+      Row cur, nxt;
+      load_row(0, cur);
+      for (int k = 0; k < nfull; ++k) {
+        load_row(k + 1 < ngw ? k + 1 : k, nxt);
+        update(k, cur, false);
+        cur = nxt;
+      }
+      if (part) update(nfull, cur, true);
+    }
+    // the appended row's position and value norm (the other rows keep theirs)
+    if (a.append && tid == 0) {
+      a.pos[ub + newrow] = a.T - 1;
+      a.vnorm[ub + newrow] = newnorm;
     }
     if (a.window > 0) write_ring2<D, G>(a, u, M, invl, H);
     if constexpr (EVICT) {
       __syncthreads();
+      if (e.scores_out) {
+        // the scores, recovered from the ranking keys (-0 reads back as +0)
+        for (int r = tid; r < L; r += SNT) {
+          const uint32_t k = (uint32_t)(keys[(size_t)r * KS] >> 32);
+          const uint32_t bits = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+          e.scores_out[(size_t)u * L + r] = __uint_as_float(bits);
+        }
+      }
       if (e.evict) {
+        const int nslots = (L + SNT - 1) / SNT;
         LdsKeys<S_KMAX, SNT> lk{keys, KS};
         select_compact<LdsKeys<S_KMAX, SNT>, 1, D, SNT>(e, u, lk, nslots, sh, mv);
       } else if (e.kept_out) {
@@ -615,8 +700,10 @@ __global__ void __launch_bounds__(SNT) stepc_a_kernel(DecodeArgs a) {
   RetStats<G> rs;
   if (retire) load_ret<G>(rs, a, u);
   float mrun[4];
-  pass_a<D, G, FEAT>(a, u, r0, r1, a.ws_s + (size_t)u * a.lmax * G,
-                     FEAT ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr, 0, qa, retire, rs, mrun);
+  float zr[S_GMAX], nr[S_GMAX];   // unused on this path
+  pass_a<D, G, FEAT, false>(a, u, r0, r1, a.ws_s + (size_t)u * a.lmax * G,
+                            FEAT ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr, 0, qa, retire, rs,
+                            mrun, zr, nr);
   float M[G];
   block_max<G>(mrun, stat, M);
   if (threadIdx.x < G) {
