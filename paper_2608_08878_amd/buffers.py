@@ -56,6 +56,36 @@ class DecodeBuffers:
     def len(self) -> int:
         return self.kv.len
 
+    def shrink(self, capacity: int):
+        """Move the valid rows of every unit into buffers of a smaller capacity (device
+        copies; the old buffers are released).  After a compression step only
+        budget + 1 rows per unit are ever live, and the steady steps stream fewer
+        distinct pages when each unit's rows sit closer together."""
+        n = self.kv.len
+        if capacity < n + 1:
+            raise ValueError(f"capacity {capacity} cannot hold {n} rows plus an append")
+        td = self.k.dtype
+        dev = self.k.device
+
+        def moved(t):
+            out = torch.zeros((t.shape[0], capacity) + tuple(t.shape[2:]), dtype=t.dtype, device=dev)
+            out[:, :n] = t[:, :n]
+            return out
+
+        self.k = moved(self.k)
+        self.v = moved(self.v)
+        self.kv.k, self.kv.v = self.k.data_ptr(), self.v.data_ptr()
+        if self.feat is not None:
+            self.alpha, self.num, self.den = moved(self.alpha), moved(self.num), moved(self.den)
+            self.pos, self.vnorm = moved(self.pos), moved(self.vnorm)
+            self.feat.alpha, self.feat.ent_num = self.alpha.data_ptr(), self.num.data_ptr()
+            self.feat.ent_den, self.feat.pos = self.den.data_ptr(), self.pos.data_ptr()
+            self.feat.vnorm = self.vnorm.data_ptr()
+        self.cap = capacity
+        self.dims.capacity = capacity
+        assert self.k.dtype == td
+        torch.cuda.synchronize(dev)
+
     def reserve_workspace(self, max_len: int, kl_rows: int = 0, kl_vocab: int = 0):
         need = B.dc_workspace_bytes(self.dims, max_len, kl_rows, kl_vocab)
         if need > self.ws_bytes:

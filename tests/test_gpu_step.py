@@ -437,3 +437,38 @@ def test_fused_step_equals_decode_then_evict(n0, budget):
                 assert torch.equal(a0, a1), (t, name)
             else:
                 assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
+
+
+def test_shrink_after_compression_keeps_every_bit():
+    """Moving the live rows into budget-sized buffers after the compression step
+    changes no output, score, slot map or state bit of the following steps
+    (through the window retire)."""
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=2, n_q_heads=8, n0=3000, budget=700, steps=70)
+    U, budget = wl.units, wl.budget
+    bufs = [_buffers(wl), _buffers(wl)]
+    for b in bufs:
+        sg.init_cache(wl, b.k, b.v, U, b.cap)
+        b.feat_init(wl.n0, 0)
+    params, pol = _policy(wl)
+    q, kn, vn = _step_tensors(wl)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        L = bufs[0].kv.len + 1
+        sc = [torch.empty((U, L), dtype=torch.float32, device="cuda") for _ in range(2)]
+        kp = [torch.empty((U, min(L, budget)), dtype=torch.int32, device="cuda") for _ in range(2)]
+        outs = [b.decode_evict(pol, budget, q, kn, vn, scores_out=s, kept_out=k)
+                for b, s, k in zip(bufs, sc, kp)]
+        if t == 0:
+            bufs[1].shrink(budget + 1)
+            assert bufs[1].cap == budget + 1 and bufs[1].k.shape[1] == budget + 1
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0], outs[1]), t
+        assert torch.equal(sc[0], sc[1]) and torch.equal(kp[0], kp[1]), t
+        n = bufs[0].kv.len
+        for name in ("k", "v", "alpha", "num", "den", "pos", "vnorm", "qring", "qstat"):
+            a0, a1 = getattr(bufs[0], name), getattr(bufs[1], name)
+            if name in ("qring", "qstat"):
+                assert torch.equal(a0, a1), (t, name)
+            else:
+                assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
