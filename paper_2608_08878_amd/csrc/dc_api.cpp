@@ -319,7 +319,8 @@ dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   if (st != DC_OK) return st;
   const int G = group_of(dims), D = dims->head_dim;
   const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
-  const bool fused = dims->dtype == DC_BF16 && !split && dc::step_fits(a.L, G, D, true, nm);
+  const bool fused = dims->dtype == DC_BF16 && !split &&
+                     dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
   if (fused) {
     if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
   } else {

@@ -30,6 +30,12 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
   const float invT = 1.0f / (float)a.T;
   const int L = a.L;
   const int kact = L > wave * 64 ? (L - wave * 64 + ENT - 1) / ENT : 0;
+  // two hidden layers: the weights go to LDS after the move list
+  float* pl = NH == 2 ? reinterpret_cast<float*>(dyn) + a.mv_ints : nullptr;
+  if constexpr (NH == 2) {
+    stage_params(a, pl);
+    __syncthreads();
+  }
   float x[REG_KPT][4];
   int32_t pk[REG_KPT];
 #pragma unroll
@@ -40,7 +46,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
     }
   }
   float sc[REG_KPT];
-  policy_scores<REG_KPT, NH>(a, x, sc, kact);
+  policy_scores<REG_KPT, NH>(a, x, sc, kact, pl);
   RegKeys<REG_KPT> keys;
 #pragma unroll
   for (int k = 0; k < REG_KPT; ++k) {
@@ -62,6 +68,11 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
 // Long caches: scores to keys in the workspace (grid over rows) ...
 template <int NH>
 __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys, int kstride) {
+  extern __shared__ float spl[];
+  if constexpr (NH == 2) {
+    stage_params(a, spl);
+    __syncthreads();
+  }
   const int u = blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
@@ -71,7 +82,7 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
     int32_t p;
     load_features(a, ub + (r < a.L ? r : a.L - 1), invT, x[0], p);
     float sc[1];
-    policy_scores<1, NH>(a, x, sc, 1);
+    policy_scores<1, NH>(a, x, sc, 1, NH == 2 ? spl : nullptr);
     if (r < a.L) {
       if (a.scores_out) a.scores_out[(size_t)u * a.L + r] = sc[0];
       keys[(size_t)u * kstride + r] = row_key(sc[0], p);
@@ -102,20 +113,30 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
   if (!a.evict && !a.scores_out && !a.kept_out) return 0;
   const int E = a.L - a.budget;
   const int nmv = a.evict ? (E < a.budget ? E : a.budget) : 0;
-  const size_t dyn = (size_t)(2 * (nmv > 0 ? nmv : 1)) * sizeof(int);
+  EvictArgs b = a;
+  b.mv_ints = (2 * (nmv > 0 ? nmv : 1) + 3) / 4 * 4;   // keeps the weights after it 16-byte aligned
+  const size_t pbytes = a.nh == 2 ? (size_t)policy_floats(2, a.h1, a.h2) * sizeof(float) : 0;
+  const size_t dyn = (size_t)b.mv_ints * sizeof(int);
   if (a.L <= ENT * REG_KPT) {
     auto k = a.nh == 2 ? score_select_kernel<DTYPE, D, 2> : score_select_kernel<DTYPE, D, 1>;
-    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-    hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, a);
+    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)(dyn + pbytes));
+    hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn + pbytes, s, b);
   } else {
     const int kstride = (a.L + ENT - 1) / ENT * ENT;
+    // two hidden layers: each workgroup stages the weights once and scores
+    // several row blocks with them
     int gx = (a.L + 255) / 256;
-    if (a.nh == 2) hipLaunchKernelGGL(score_kernel<2>, dim3(gx, a.units), dim3(256), 0, s, a, ws_keys, kstride);
-    else hipLaunchKernelGGL(score_kernel<1>, dim3(gx, a.units), dim3(256), 0, s, a, ws_keys, kstride);
+    if (a.nh == 2) {
+      gx = gx < 16 ? gx : 16;
+      hipFuncSetAttribute((const void*)score_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pbytes);
+      hipLaunchKernelGGL(score_kernel<2>, dim3(gx, a.units), dim3(256), pbytes, s, b, ws_keys, kstride);
+    } else {
+      hipLaunchKernelGGL(score_kernel<1>, dim3(gx, a.units), dim3(256), 0, s, b, ws_keys, kstride);
+    }
     if (a.evict) {
       auto k = select_kernel<DTYPE, D>;
       hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-      hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, a, (const uint64_t*)ws_keys, kstride);
+      hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);
     } else if (a.kept_out) {
       hipLaunchKernelGGL(identity_kept_kernel, dim3(1024), dim3(256), 0, s, a.kept_out, a.units, a.L);
     }

@@ -62,6 +62,8 @@ struct EvictArgs {
   int h1, h2;
   int evict;            // 1 if rows are removed
   uint64_t* ws_keys;    // [units][kstride] row keys (long caches only)
+  int mv_ints;          // ints of the compaction move list at the start of the dynamic LDS
+                        // (the two-hidden-layer policy's weights follow it); set by the launchers
 };
 
 struct KLArgs {
@@ -87,7 +89,8 @@ int launch_kl(const KLArgs& a, void* stream);
 // bf16 matrix-core step (dc_step.hip); e != nullptr fuses scoring and eviction.
 int launch_step(const DecodeArgs& a, const EvictArgs* e, int D, int G, bool feat, bool chunked,
                 void* stream);
-bool step_fits(int L, int G, int D, bool feat, int nmoves);
+bool step_fits(int L, int G, int D, bool feat, int nmoves, size_t extra_lds = 0);
+size_t policy_lds_bytes(const EvictArgs& e);   // LDS of the two-hidden-layer policy's weights
 int step_chunk_rows();
 int kl_tile_cols();
 

@@ -74,19 +74,36 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   const char* arow = (const char*)(i < 8 ? a.h_full : a.h_comp) + (size_t)(avalid ? krow : 0) * a.hidden * 2;
   const char* brow = (const char*)a.w + (size_t)(n0 + i) * a.hidden * 2;
   f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  // lane's k range within an iteration: [32*kg, 32*kg + 32) = 4 MFMA slices of 8
-  for (int k0 = 0; k0 < a.hidden; k0 += KL_KSTEP) {
-    const int off = (k0 + 32 * kg) * 2;
-    uint4 av[4], bv[4];
+  // Hidden elements go in blocks of 128; MFMA t of a block takes 16-byte chunk
+  // 4t + kg (both operands use the same map, which the dot product does not
+  // see), so each load instruction reads 64 contiguous bytes of 16 rows.  Two
+  // blocks are in flight per wave; every load is unconditional (a block past
+  // the end re-reads the last one, and rows past `rows` are zeroed after the
+  // load), so a wait covers only the block it consumes.
+  const int nblk = a.hidden / KL_KSTEP;
+  auto load = [&](int blk, uint4 (&av)[4], uint4 (&bv)[4]) {
+    const int off = (blk < nblk ? blk : nblk - 1) * KL_KSTEP * 2;
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      av[t] = avalid ? ldg16(arow + off + 16 * t) : make_uint4(0, 0, 0, 0);
-      bv[t] = ldg16_nt(brow + off + 16 * t);
+      const uint4 x = ldg16(arow + off + 16 * (4 * t + kg));
+      av[t] = avalid ? x : make_uint4(0, 0, 0, 0);
+      bv[t] = ldg16(brow + off + 16 * (4 * t + kg));
     }
+  };
+  auto mma = [&](const uint4 (&av)[4], const uint4 (&bv)[4]) {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av[t]),
                                                     __builtin_bit_cast(bf16x8_t, bv[t]), acc, 0, 0, 0);
+  };
+  uint4 a0[4], b0[4], a1[4], b1[4];
+  load(0, a0, b0);
+  load(1, a1, b1);
+  for (int blk = 0; blk < nblk; blk += 2) {
+    mma(a0, b0);
+    load(blk + 2, a0, b0);
+    if (blk + 1 < nblk) mma(a1, b1);
+    load(blk + 3, a1, b1);
   }
   // lane holds C[4*kg + r][i] for r < 4: kg 0,1 full rows 0..7, kg 2,3 compressed rows 0..7
   float lf[4], lc[4];

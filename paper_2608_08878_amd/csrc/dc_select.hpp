@@ -48,31 +48,92 @@ __device__ __forceinline__ const cfloat* const_params(const float* p) {
   return (const cfloat*)p;
 }
 
+// Floats of the packed policy blob (W1, b1, [W2, b2,] w_out, b_out).
+__host__ __device__ inline int policy_floats(int nh, int h1, int h2) {
+  return nh == 1 ? 4 * h1 + h1 + h1 + 1 : 4 * h1 + h1 + h2 * h1 + h2 + h2 + 1;
+}
+
+// Copy the policy blob to LDS (block-cooperative; a barrier must follow before
+// any thread reads it).
+__device__ __forceinline__ void stage_params(const EvictArgs& a, float* dst) {
+  const int n = policy_floats(a.nh, a.h1, a.h2);
+  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = a.params[i];
+}
+
 // s = f_phi(x) for a 4 -> h1 -> h2 -> 1 ReLU MLP (two hidden layers), float32,
-// fixed evaluation order (bias first, then the inputs in order).
-__device__ __forceinline__ float mlp2(const cfloat* P, int h1, int h2, const float x[4]) {
-  const cfloat* W1 = P;
-  const cfloat* b1 = P + 4 * h1;
-  const cfloat* W2 = b1 + h1;
-  const cfloat* b2 = W2 + h2 * h1;
-  const cfloat* wo = b2 + h2;
+// fixed evaluation order (bias first, then the inputs in order; output units
+// in order), with the weights in LDS (every lane reads the same address:
+// broadcast reads).
+typedef __attribute__((address_space(3))) const float lfloat;
+typedef __attribute__((address_space(3))) const float4 lfloat4;
+
+// The 64 x 64 shape: no width tests.  The LDS pointer is made opaque on entry
+// so that the weight reads stay inside the caller's loops (hoisted out, the
+// first layer's 320 weights would occupy 320 registers).
+__device__ __forceinline__ float mlp2_lds_64(const float* params, const float x[4]) {
+  constexpr int H = MAX_H1_2L;
+  const lfloat* P = (const lfloat*)params;
+  asm volatile("" : "+v"(P));
+  const lfloat* W1 = P;
+  const lfloat* b1 = P + 4 * H;
+  const lfloat* W2 = b1 + H;
+  const lfloat* b2 = W2 + H * H;
+  const lfloat* wo = b2 + H;
+  float hv[H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    const float4 w = *reinterpret_cast<lfloat4*>(W1 + 4 * h);
+    float z = b1[h];
+    z = __builtin_fmaf(w.x, x[0], z);
+    z = __builtin_fmaf(w.y, x[1], z);
+    z = __builtin_fmaf(w.z, x[2], z);
+    z = __builtin_fmaf(w.w, x[3], z);
+    hv[h] = fmaxf(z, 0.0f);
+  }
+  float out = wo[H];
+#pragma unroll 1
+  for (int o = 0; o < H; ++o) {
+    const lfloat4* w = reinterpret_cast<lfloat4*>(W2 + o * H);
+    float z = b2[o];
+#pragma unroll
+    for (int q = 0; q < H / 4; ++q) {
+      const float4 w4 = w[q];
+      z = __builtin_fmaf(w4.x, hv[4 * q + 0], z);
+      z = __builtin_fmaf(w4.y, hv[4 * q + 1], z);
+      z = __builtin_fmaf(w4.z, hv[4 * q + 2], z);
+      z = __builtin_fmaf(w4.w, hv[4 * q + 3], z);
+    }
+    out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
+  }
+  return out;
+}
+
+// Any widths up to 64 (kept out of line: its per-width tests would otherwise
+// share registers with the fixed-shape code).
+__device__ __attribute__((noinline)) float mlp2_lds_any(const float* params, int h1, int h2,
+                                                         float x0, float x1, float x2, float x3) {
+  const lfloat* P = (const lfloat*)params;
+  const lfloat* W1 = P;
+  const lfloat* b1 = P + 4 * h1;
+  const lfloat* W2 = b1 + h1;
+  const lfloat* b2 = W2 + h2 * h1;
+  const lfloat* wo = b2 + h2;
   float hv[MAX_H1_2L];
 #pragma unroll
   for (int h = 0; h < MAX_H1_2L; ++h) {
+    float z = 0.0f;
     if (h < h1) {
-      float z = b1[h];
-      z = __builtin_fmaf(W1[4 * h + 0], x[0], z);
-      z = __builtin_fmaf(W1[4 * h + 1], x[1], z);
-      z = __builtin_fmaf(W1[4 * h + 2], x[2], z);
-      z = __builtin_fmaf(W1[4 * h + 3], x[3], z);
-      hv[h] = fmaxf(z, 0.0f);
-    } else {
-      hv[h] = 0.0f;
+      z = b1[h];
+      z = __builtin_fmaf(W1[4 * h + 0], x0, z);
+      z = __builtin_fmaf(W1[4 * h + 1], x1, z);
+      z = __builtin_fmaf(W1[4 * h + 2], x2, z);
+      z = __builtin_fmaf(W1[4 * h + 3], x3, z);
     }
+    hv[h] = fmaxf(z, 0.0f);
   }
   float out = wo[h2];
   for (int o = 0; o < h2; ++o) {
-    const cfloat* w = W2 + o * h1;
+    const lfloat* w = W2 + o * h1;
     float z = b2[o];
 #pragma unroll
     for (int h = 0; h < MAX_H1_2L; ++h)
@@ -80,6 +141,11 @@ __device__ __forceinline__ float mlp2(const cfloat* P, int h1, int h2, const flo
     out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
   }
   return out;
+}
+
+__device__ __forceinline__ float mlp2_lds(const float* params, int h1, int h2, const float x[4]) {
+  if (h1 == MAX_H1_2L && h2 == MAX_H1_2L) return mlp2_lds_64(params, x);
+  return mlp2_lds_any(params, h1, h2, x[0], x[1], x[2], x[3]);
 }
 
 // One hidden unit of the one-hidden-layer MLP for KP rows.
@@ -105,12 +171,13 @@ __device__ __forceinline__ void mlp1_unit(const cfloat* W1, const cfloat* b1, co
 // Scores of KP rows per thread, s = f_phi(x) in float32 with a fixed evaluation
 // order: out = b_out, then for every hidden unit h in order
 // out += w_out[h] relu(b1[h] + W1[h,0] x0 + W1[h,1] x1 + W1[h,2] x2 + W1[h,3] x3)
-// (for two hidden layers see mlp2).  Row slots k >= kact (uniform over the
+// (for two hidden layers see mlp2_lds).  Row slots k >= kact (uniform over the
 // wave) are skipped.  The loops over the hidden units are uniform, so every
 // weight is read once per wave and reused for all row slots.
 template <int KP, int NH>
 __device__ __forceinline__ void policy_scores(const EvictArgs& a, const float (&x)[KP][4],
-                                              float (&out)[KP], int kact) {
+                                              float (&out)[KP], int kact,
+                                              const float* lds_params = nullptr) {
   const cfloat* P = const_params(a.params);
   if constexpr (NH == 1) {
     const int h1 = a.h1;
@@ -127,9 +194,10 @@ __device__ __forceinline__ void policy_scores(const EvictArgs& a, const float (&
     }
     for (; h < h1; ++h) mlp1_unit<KP>(W1, b1, wo, h, x, out, kact);
   } else {
+    // two hidden layers: the caller staged the weights in LDS (stage_params)
 #pragma unroll
     for (int k = 0; k < KP; ++k)
-      if (k < kact) out[k] = mlp2(P, a.h1, a.h2, x[k]);
+      if (k < kact) out[k] = mlp2_lds(lds_params, a.h1, a.h2, x[k]);
   }
 }
 

@@ -519,6 +519,9 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
   float* sbuf = lds;                                  // row stride RS
   float* obuf = lds + (size_t)L * RS;                 // (SNW / 2) * G * D
   int* mv = (int*)(obuf + (SNW / 2) * G * D);
+  // two hidden layers: the policy weights sit in LDS after the move list
+  float* pl = (EVICT && NH == 2) ? reinterpret_cast<float*>(mv + e.mv_ints) : nullptr;
+  if constexpr (EVICT && NH == 2) stage_params(e, pl);     // read after the barriers below
   const size_t ub = (size_t)u * a.cap;
 
   if (a.append) append_rows<D>(a, u);
@@ -645,7 +648,7 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
       if constexpr (EVICT) {
         float f[1][4], sc[1];
         make_features(al, vn, nu, de, ps, invT, f[0]);
-        policy_scores<1, NH>(e, f, sc, 1);
+        policy_scores<1, NH>(e, f, sc, 1, pl);
         if (!guard || valid) keys[(size_t)r * KS] = row_key(sc[0], ps);
       }
     };
@@ -821,14 +824,23 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
 }
 
 // ---------------------------------------------------------------- dispatch
+// ints of the compaction move list (a multiple of four, so what follows it in
+// LDS stays 16-byte aligned)
+static int move_list_ints(int nmoves) { return (2 * (nmoves > 0 ? nmoves : 1) + 3) / 4 * 4; }
+
 size_t step_lds_bytes(int L, int G, int D, bool feat, int nmoves) {
   const size_t rs = G < 2 ? 2 : G;
   const size_t b = ((size_t)L * rs + (size_t)(SNW / 2) * G * D) * sizeof(float);
-  return b + (size_t)2 * (nmoves > 0 ? nmoves : 1) * sizeof(int);
+  return b + (size_t)move_list_ints(nmoves) * sizeof(int);
 }
 
-bool step_fits(int L, int G, int D, bool feat, int nmoves) {
-  return (!feat || L <= S_KMAX * SNT) && step_lds_bytes(L, G, D, feat, nmoves) <= (size_t)S_LDS;
+size_t policy_lds_bytes(const EvictArgs& e) {
+  return e.nh == 2 ? (size_t)policy_floats(2, e.h1, e.h2) * sizeof(float) : 0;
+}
+
+bool step_fits(int L, int G, int D, bool feat, int nmoves, size_t extra_lds) {
+  return (!feat || L <= S_KMAX * SNT) &&
+         step_lds_bytes(L, G, D, feat, nmoves) + extra_lds <= (size_t)S_LDS;
 }
 
 int step_chunk_rows() { return SCHUNK; }
@@ -838,10 +850,11 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
                          hipStream_t s) {
   if (!chunked) {
     const int nm = e && e->evict ? (a.L - e->budget < e->budget ? a.L - e->budget : e->budget) : 0;
-    const size_t lds = step_lds_bytes(a.L, G, D, feat, nm);
     EvictArgs ee;
     if (e) ee = *e;
     else __builtin_memset(&ee, 0, sizeof(ee));
+    ee.mv_ints = move_list_ints(nm);
+    const size_t lds = step_lds_bytes(a.L, G, D, feat, nm) + (e ? policy_lds_bytes(*e) : 0);
     auto pick = [&](auto kern) {
       hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       hipLaunchKernelGGL(kern, dim3(a.units), dim3(SNT), lds, s, a, ee);

@@ -472,3 +472,56 @@ def test_shrink_after_compression_keeps_every_bit():
                 assert torch.equal(a0, a1), (t, name)
             else:
                 assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
+
+
+def test_two_layer_policy_periodic_eviction():
+    """The 4->64->64->1 policy (weights staged in LDS) on the long-context recipe
+    with an eviction every 4th step: the fused decode+evict launch leaves every
+    buffer bit-identical to decode then score/evict (register-resident path), and
+    the scores match the oracle's MLP applied to the step's features."""
+    from oracle import features as ofeat
+    from oracle import policy as opol
+    wl = W.WORKLOADS[4].scaled(batch=1, n_layers=1, n_kv_heads=2, n_q_heads=8, n0=3000,
+                               budget=700, steps=70)
+    U, budget = wl.units, wl.budget
+    bufs = [_buffers(wl), _buffers(wl)]
+    for b in bufs:
+        sg.init_cache(wl, b.k, b.v, U, b.cap)
+        b.feat_init(wl.n0, 0)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    q, kn, vn = _step_tensors(wl)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        if t % 4 == 0:
+            L = bufs[0].kv.len + 1
+            sc = [torch.empty((U, L), dtype=torch.float32, device="cuda") for _ in range(2)]
+            kp = [torch.empty((U, min(L, budget)), dtype=torch.int32, device="cuda") for _ in range(2)]
+            o0 = bufs[0].decode_step(q, kn, vn)
+            torch.cuda.synchronize()
+            pre = [H.download_unit(bufs[0], u) for u in range(U)]
+            T = bufs[0].feat.next_pos
+            bufs[0].score_evict(pol, budget, sc[0], kp[0])
+            o1 = bufs[1].decode_evict(pol, budget, q, kn, vn, scores_out=sc[1], kept_out=kp[1])
+            torch.cuda.synchronize()
+            assert torch.equal(sc[0], sc[1]) and torch.equal(kp[0], kp[1]), t
+            scn = H.to_np(sc[0])
+            for u in range(U):
+                x = ofeat.feature_matrix(pre[u]["alpha"], pre[u]["v"], pre[u]["den"],
+                                         pre[u]["num"], pre[u]["pos"], T)
+                ok, worst = H.vec_ok(scn[u], opol.scores(pnp, x, wl.hidden))
+                assert ok, (t, u, worst)
+        else:
+            o0 = bufs[0].decode_step(q, kn, vn)
+            o1 = bufs[1].decode_step(q, kn, vn)
+            torch.cuda.synchronize()
+        assert torch.equal(o0, o1), t
+        assert bufs[0].kv.len == bufs[1].kv.len
+        n = bufs[0].kv.len
+        for name in ("k", "v", "alpha", "num", "den", "pos", "vnorm", "qring", "qstat"):
+            a0, a1 = getattr(bufs[0], name), getattr(bufs[1], name)
+            if name in ("qring", "qstat"):
+                assert torch.equal(a0, a1), (t, name)
+            else:
+                assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
