@@ -65,7 +65,8 @@ __device__ __forceinline__ void stage_params(const EvictArgs& a, float* dst) {
 // in order), with the weights in LDS (every lane reads the same address:
 // broadcast reads).
 typedef __attribute__((address_space(3))) const float lfloat;
-typedef __attribute__((address_space(3))) const float4 lfloat4;
+typedef float f32x4v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) const f32x4v lfloat4;
 
 // The 64 x 64 shape: no width tests.  The LDS pointer is made opaque on entry
 // so that the weight reads stay inside the caller's loops (hoisted out, the
@@ -82,7 +83,7 @@ __device__ __forceinline__ float mlp2_lds_64(const float* params, const float x[
   float hv[H];
 #pragma unroll
   for (int h = 0; h < H; ++h) {
-    const float4 w = *reinterpret_cast<lfloat4*>(W1 + 4 * h);
+    const f32x4v w = *reinterpret_cast<const lfloat4*>(W1 + 4 * h);
     float z = b1[h];
     z = __builtin_fmaf(w.x, x[0], z);
     z = __builtin_fmaf(w.y, x[1], z);
@@ -93,11 +94,11 @@ __device__ __forceinline__ float mlp2_lds_64(const float* params, const float x[
   float out = wo[H];
 #pragma unroll 1
   for (int o = 0; o < H; ++o) {
-    const lfloat4* w = reinterpret_cast<lfloat4*>(W2 + o * H);
+    const lfloat4* w = reinterpret_cast<const lfloat4*>(W2 + o * H);
     float z = b2[o];
 #pragma unroll
     for (int q = 0; q < H / 4; ++q) {
-      const float4 w4 = w[q];
+      const f32x4v w4 = w[q];
       z = __builtin_fmaf(w4.x, hv[4 * q + 0], z);
       z = __builtin_fmaf(w4.y, hv[4 * q + 1], z);
       z = __builtin_fmaf(w4.z, hv[4 * q + 2], z);
