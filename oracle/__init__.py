@@ -16,6 +16,8 @@ Every value is computed in binary64 from the exact stored input values
 * ``policy``     – the scoring MLP s_i = f_phi(x_i) (Sec. 3.1.2, App. D).
 * ``select``     – deterministic argtop_B (Sec. 3.3, Algorithm 1).
 * ``kl``         – the per-step reward R_t = -KL(P_t || P^_t) (Sec. 3.1.4).
+* ``sampling``   – training-mode selection: Gumbel-perturbed top-B, the exact
+  log-partition log Z(s, B, tau) and log pi(a | s) (Sec. 3.1.2, App. C).
 * ``unit``       – one unit's cache and feature state stepped through
   append -> attention -> features -> score -> select -> prune (Algorithm 1,
   Sec. 3.1.3 for the student/teacher caches).
