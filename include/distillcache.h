@@ -56,7 +56,8 @@ typedef enum {
   DC_ERR_CAPACITY = 4,     /* appending would exceed the capacity */
   DC_ERR_BUDGET = 5,       /* budget < 1 */
   DC_ERR_WORKSPACE = 6,    /* workspace missing or smaller than dc_workspace_bytes */
-  DC_ERR_HIP = 7           /* a HIP launch failed */
+  DC_ERR_HIP = 7,          /* a HIP launch failed */
+  DC_ERR_VALUE = 8         /* a scalar argument out of range (temperature not finite and > 0) */
 } dc_status;
 
 typedef enum { DC_F32 = 0, DC_BF16 = 1 } dc_dtype;
@@ -190,6 +191,63 @@ dc_status dc_decode_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const d
                           int32_t budget, const void *q, const void *k_new, const void *v_new,
                           void *out, float *scores_out, int32_t *kept_out, void *ws,
                           size_t ws_bytes, void *hip_stream);
+
+/* Gumbel noise of the training-mode selection (Sec. 3.1.2: during training the
+ * ranking is sampled by perturbing every score with an independent standard
+ * Gumbel draw; App. C adds the temperature tau).  The draw of the token at
+ * position p in unit u is a pure function of (seed, draw, u, p):
+ *   x = first output word of Philox4x32-10 (Salmon et al., SC'11) with
+ *       counter (p, u, draw, 0) and key (seed[0], seed[1]),
+ *   U = (2 (x >> 9) + 1) 2^-24   (exact in float32, 0 < U < 1),
+ *   g = -ln(-ln U). */
+typedef struct {
+  float tau;           /* temperature, finite and > 0 */
+  uint32_t seed[2];    /* Philox key: low and high word of a 64-bit seed */
+  uint32_t draw;       /* draw number: use a new value for every sampling call on a cache */
+} dc_gumbel;
+
+/* Training-mode scoring and selection (Sec. 3.1.2 stochastic ranking, App. C).
+ * As dc_score_evict, except that rows are ranked by the perturbed score
+ *   s~_i = s_i / tau + g_i           (float32; same tie rule and compaction)
+ * with g_i from `gumbel`; scores_out still receives the unperturbed s_i.  If
+ * logp_out is not NULL it receives, per unit, the log-probability of the kept
+ * set a under App. C's subset law,
+ *   logp_out[u] = sum_{i in a} s_i / tau - log Z(s, budget, tau)
+ * (see dc_subset_log_prob; 0 when budget >= len), which needs scores_out and
+ * kept_out.  Workspace: as dc_score_evict (it also covers the log-partition).
+ * Errors: those of dc_score_evict; DC_ERR_NULL (gumbel NULL, or logp_out
+ * without scores_out and kept_out); DC_ERR_VALUE (tau). */
+dc_status dc_sample_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const dc_policy *policy,
+                          int32_t budget, const dc_gumbel *gumbel, float *scores_out,
+                          int32_t *kept_out, double *logp_out, void *ws, size_t ws_bytes,
+                          void *hip_stream);
+
+/* Exact log-partition function of the size-B subset law and the
+ * log-probability of kept sets (App. C), for `units` independent score rows:
+ *   logz_out[u] = log Z = log sum over size-budget subsets a of exp(sum_{i in a} s[u][i] / tau)
+ *   logp_out[u] = sum_{i in kept[u]} s[u][i] / tau - logz_out[u]
+ * When budget >= len the only subset is the whole row: log Z = sum_i s_i / tau
+ * and logp = 0.
+ *   scores    [units][len] float32
+ *   kept      [units][min(budget, len)] int32 indices into the row (the
+ *             kept_out layout of dc_score_evict); needed for logp_out only
+ *   logz_out, logp_out  [units] float64; either may be NULL
+ * Computed by an O(len K) recursion, K = min(budget, len - budget), exact up
+ * to rounding: the relative error of Z stays below about (K + len) 2^-24.
+ * Scores whose spread divided by tau exceeds about 11000 fall outside exact
+ * coverage (the smallest weights are clamped); a non-finite score or a kept
+ * index outside [0, len) gives NaN for that unit.
+ * Workspace: dc_subset_log_prob_workspace_bytes(units, len, budget) bytes
+ * (zero unless K > 4096).
+ * Errors: DC_ERR_NULL (scores, or kept with logp_out), DC_ERR_SHAPE (units or
+ * len < 1), DC_ERR_BUDGET, DC_ERR_VALUE (tau), DC_ERR_UNSUPPORTED (len > 40960,
+ * units > 2^24), DC_ERR_WORKSPACE. */
+dc_status dc_subset_log_prob(int32_t units, int32_t len, int32_t budget, float tau,
+                             const float *scores, const int32_t *kept, double *logz_out,
+                             double *logp_out, void *ws, size_t ws_bytes, void *hip_stream);
+
+/* Workspace bytes of dc_subset_log_prob (0 for invalid sizes). */
+size_t dc_subset_log_prob_workspace_bytes(int32_t units, int32_t len, int32_t budget);
 
 /* Per-step KL reward (Sec. 3.1.4): for each row r,
  *   kl_out[r] = KL(P || Q) = sum_v P_v (ln P_v - ln Q_v)   (nats),

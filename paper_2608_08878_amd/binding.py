@@ -12,7 +12,8 @@ LIB_PATH = os.path.join(HERE, "libdistillcache.so")
 MAX_WINDOW = 64
 DC_F32, DC_BF16 = 0, 1
 STATUS = {0: "DC_OK", 1: "DC_ERR_NULL", 2: "DC_ERR_SHAPE", 3: "DC_ERR_UNSUPPORTED",
-          4: "DC_ERR_CAPACITY", 5: "DC_ERR_BUDGET", 6: "DC_ERR_WORKSPACE", 7: "DC_ERR_HIP"}
+          4: "DC_ERR_CAPACITY", 5: "DC_ERR_BUDGET", 6: "DC_ERR_WORKSPACE", 7: "DC_ERR_HIP",
+          8: "DC_ERR_VALUE"}
 
 
 class dc_dims(ctypes.Structure):
@@ -40,8 +41,18 @@ class dc_policy(ctypes.Structure):
                 ("hidden", ctypes.c_int32 * 2), ("params", ctypes.c_void_p)]
 
 
+class dc_gumbel(ctypes.Structure):
+    _fields_ = [("tau", ctypes.c_float), ("seed", ctypes.c_uint32 * 2), ("draw", ctypes.c_uint32)]
+
+
+def make_gumbel(tau: float, seed: int, draw: int) -> dc_gumbel:
+    s = (ctypes.c_uint32 * 2)(seed & 0xFFFFFFFF, (seed >> 32) & 0xFFFFFFFF)
+    return dc_gumbel(tau, s, draw & 0xFFFFFFFF)
+
+
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
-           "dc_decode_evict", "dc_kl_reward", "dc_status_str")
+           "dc_decode_evict", "dc_sample_evict", "dc_subset_log_prob",
+           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_status_str")
 
 _lib = None
 
@@ -71,6 +82,14 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
                                       vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.dc_decode_evict.restype = ctypes.c_int
+        L.dc_sample_evict.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                      ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
+                                      ctypes.POINTER(dc_gumbel), vp, vp, vp, vp, sz, vp]
+        L.dc_sample_evict.restype = ctypes.c_int
+        L.dc_subset_log_prob.argtypes = [i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
+        L.dc_subset_log_prob.restype = ctypes.c_int
+        L.dc_subset_log_prob_workspace_bytes.argtypes = [i32, i32, i32]
+        L.dc_subset_log_prob_workspace_bytes.restype = sz
         L.dc_kl_reward.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
         L.dc_kl_reward.restype = ctypes.c_int
         L.dc_status_str.argtypes = [ctypes.c_int]
@@ -139,3 +158,21 @@ def dc_kl_reward(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_ou
                  ws_bytes: int = 0, stream=None) -> None:
     _check(lib().dc_kl_reward(rows, hidden, vocab, _ptr(h_full), _ptr(h_comp), _ptr(w_lm),
                               _ptr(kl_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_sample_evict(dims, kv, feat, policy, budget: int, gumbel, scores_out=None, kept_out=None,
+                    logp_out=None, ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_sample_evict(ctypes.byref(dims), ctypes.byref(kv), _ref(feat), _ref(policy),
+                                 budget, _ref(gumbel), _ptr(scores_out), _ptr(kept_out),
+                                 _ptr(logp_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_subset_log_prob(units: int, length: int, budget: int, tau: float, scores, kept=None,
+                       logz_out=None, logp_out=None, ws=None, ws_bytes: int = 0,
+                       stream=None) -> None:
+    _check(lib().dc_subset_log_prob(units, length, budget, tau, _ptr(scores), _ptr(kept),
+                                    _ptr(logz_out), _ptr(logp_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_subset_log_prob_workspace_bytes(units: int, length: int, budget: int) -> int:
+    return int(lib().dc_subset_log_prob_workspace_bytes(units, length, budget))

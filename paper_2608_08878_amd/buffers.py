@@ -117,6 +117,27 @@ class DecodeBuffers:
                          self.ws, self.ws_bytes, stream_handle(stream))
 
 
+    def sample_evict(self, policy, budget, gumbel, scores_out=None, kept_out=None, logp_out=None,
+                     stream=None):
+        B.dc_sample_evict(self.dims, self.kv, self.feat, policy, budget, gumbel, scores_out,
+                          kept_out, logp_out, self.ws, self.ws_bytes, stream_handle(stream))
+
+
+def subset_log_prob(scores: torch.Tensor, budget: int, tau: float = 1.0, kept=None, logz=True,
+                    stream=None):
+    """log Z and (with `kept`) log pi for every row of `scores` ([units][len] float32
+    on the device).  Returns (logz, logp) float64 tensors (logp None without kept)."""
+    units, length = scores.shape
+    dev = scores.device
+    lz = torch.empty(units, dtype=torch.float64, device=dev) if logz else None
+    lp = torch.empty(units, dtype=torch.float64, device=dev) if kept is not None else None
+    need = B.dc_subset_log_prob_workspace_bytes(units, length, budget)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev) if need else None
+    B.dc_subset_log_prob(units, length, budget, tau, scores, kept, lz, lp, ws, need,
+                         stream_handle(stream))
+    return lz, lp
+
+
 def make_policy(params: torch.Tensor, hidden) -> B.dc_policy:
     hidden = tuple(hidden)
     h = (ctypes.c_int32 * 2)(hidden[0], hidden[1] if len(hidden) > 1 else 0)

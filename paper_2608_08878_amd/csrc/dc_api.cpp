@@ -77,6 +77,7 @@ const char* dc_status_str(dc_status s) {
     case DC_ERR_BUDGET: return "DC_ERR_BUDGET: budget must be >= 1";
     case DC_ERR_WORKSPACE: return "DC_ERR_WORKSPACE: workspace missing or too small";
     case DC_ERR_HIP: return "DC_ERR_HIP: a HIP launch failed";
+    case DC_ERR_VALUE: return "DC_ERR_VALUE: scalar argument out of range";
   }
   return "unknown dc_status";
 }
@@ -271,6 +272,36 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   return DC_OK;
 }
 
+// Validate a log-partition call and fill its arguments.
+dc_status prep_logz(int32_t units, int32_t L, int32_t B, float tau, const float* scores,
+                    const int32_t* kept, double* logz, double* logp, void* ws, size_t ws_bytes,
+                    dc::LogzArgs& z) {
+  if (!scores || (logp && !kept)) return DC_ERR_NULL;
+  if (units < 1 || L < 1) return DC_ERR_SHAPE;
+  if (B < 1) return DC_ERR_BUDGET;
+  if (!(tau > 0.0f) || isinf(tau)) return DC_ERR_VALUE;
+  if (L > dc::evict_max_len() || units > (1 << 24)) return DC_ERR_UNSUPPORTED;
+  const size_t need = dc::logz_ws_bytes(units, L, B);
+  if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
+  memset(&z, 0, sizeof(z));
+  z.scores = scores;
+  z.kept = logp ? kept : nullptr;
+  z.nk = B < L ? B : L;
+  z.logz = logz;
+  z.logp = logp;
+  if (need) {
+    z.col_m = (float*)ws;
+    z.col_k = (int*)((char*)ws + (size_t)units * L * sizeof(float));
+  }
+  z.units = units;
+  z.L = L;
+  z.B = B;
+  z.K = B >= L ? 0 : (B <= L - B ? B : L - B);
+  z.neg = B < L && L - B < B;
+  z.tau = tau;
+  return DC_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -301,6 +332,54 @@ dc_status dc_score_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc
   if (dc::launch_evict(e, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
   kv->len = e.budget;
   return DC_OK;
+}
+
+dc_status dc_sample_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,
+                          int32_t budget, const dc_gumbel* gumbel, float* scores_out,
+                          int32_t* kept_out, double* logp_out, void* ws, size_t ws_bytes,
+                          void* hip_stream) {
+  if (!kv || !feat || !gumbel) return DC_ERR_NULL;
+  if (logp_out && (!scores_out || !kept_out)) return DC_ERR_NULL;
+  dc::EvictArgs e;
+  size_t need = 0;
+  dc_status st = prep_evict(dims, kv, feat, policy, budget, scores_out, kept_out, ws, ws_bytes,
+                            kv->len, feat->next_pos, e, need);
+  if (st != DC_OK) return st;
+  if (!(gumbel->tau > 0.0f) || isinf(gumbel->tau)) return DC_ERR_VALUE;
+  e.sample = 1;
+  e.tau = gumbel->tau;
+  e.seed0 = gumbel->seed[0];
+  e.seed1 = gumbel->seed[1];
+  e.draw = gumbel->draw;
+  dc::LogzArgs z;
+  if (logp_out) {
+    // the log-partition runs after the selection on the same stream and may
+    // reuse the selection's workspace
+    st = prep_logz(e.units, e.L, budget, gumbel->tau, scores_out, kept_out, nullptr, logp_out, ws,
+                   ws_bytes, z);
+    if (st != DC_OK) return st;
+  }
+  if (dc::launch_evict(e, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
+  if (logp_out && dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  kv->len = e.budget;
+  return DC_OK;
+}
+
+dc_status dc_subset_log_prob(int32_t units, int32_t len, int32_t budget, float tau,
+                             const float* scores, const int32_t* kept, double* logz_out,
+                             double* logp_out, void* ws, size_t ws_bytes, void* hip_stream) {
+  dc::LogzArgs z;
+  const dc_status st =
+      prep_logz(units, len, budget, tau, scores, kept, logz_out, logp_out, ws, ws_bytes, z);
+  if (st != DC_OK) return st;
+  if (!logz_out && !logp_out) return DC_OK;
+  if (dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  return DC_OK;
+}
+
+size_t dc_subset_log_prob_workspace_bytes(int32_t units, int32_t len, int32_t budget) {
+  if (units < 1 || len < 1 || budget < 1 || len > dc::evict_max_len() || units > (1 << 24)) return 0;
+  return dc::logz_ws_bytes(units, len, budget);
 }
 
 dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,

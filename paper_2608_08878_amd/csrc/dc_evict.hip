@@ -1,9 +1,11 @@
-// Policy scoring, deterministic top-B selection and in-place compaction (gfx950).
+// Policy scoring, top-B selection and in-place compaction (gfx950).
 //
 // Per unit (Algorithm 1: scores, argtop_B, prune):
 //   x_i = [alpha_i, ||v_i||_2, H_i = num_i / den_i (0 if den_i = 0), pos_i / T]
 //   s_i = f_phi(x_i)                                   (ReLU MLP, float32)
 //   keep the `budget` rows that rank highest under (s desc, pos asc)
+// In training mode (Sec. 3.1.2, App. C) the ranking score is the
+// Gumbel-perturbed s_i / tau + g_i instead; scores_out still receives s_i.
 // Ranking uses one unsigned 64-bit key per row: the order-preserving image of
 // the float32 score in the high word (-0 -> +0, NaN lowest) and ~pos in the low
 // word, so keys are unique and "keep the top B" is "drop the E = L - B smallest
@@ -54,7 +56,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
     keys.key[k] = ~0ull;
     if (k < kact && r < L) {
       if (a.scores_out) a.scores_out[(size_t)u * L + r] = sc[k];
-      keys.key[k] = row_key(sc[k], pk[k]);
+      keys.key[k] = row_key(a.sample ? sampled_score(a, sc[k], pk[k], u) : sc[k], pk[k]);
     }
   }
   if (!a.evict) {
@@ -85,7 +87,7 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
     policy_scores<1, NH>(a, x, sc, 1, NH == 2 ? spl : nullptr);
     if (r < a.L) {
       if (a.scores_out) a.scores_out[(size_t)u * a.L + r] = sc[0];
-      keys[(size_t)u * kstride + r] = row_key(sc[0], p);
+      keys[(size_t)u * kstride + r] = row_key(a.sample ? sampled_score(a, sc[0], p, u) : sc[0], p);
     }
   }
 }

@@ -64,6 +64,24 @@ struct EvictArgs {
   uint64_t* ws_keys;    // [units][kstride] row keys (long caches only)
   int mv_ints;          // ints of the compaction move list at the start of the dynamic LDS
                         // (the two-hidden-layer policy's weights follow it); set by the launchers
+  int sample;           // 1: rank by the Gumbel-perturbed score s / tau + g (training mode)
+  float tau;            // sampling temperature
+  uint32_t seed0, seed1, draw;  // Philox key and draw number of the Gumbel noise
+};
+
+// Log-partition / log-probability of size-B subsets (one call covers every unit).
+struct LogzArgs {
+  const float* scores;      // [units][L] policy scores s_i
+  const int32_t* kept;      // [units][nk] kept rows (indices into the scores) or null
+  int nk;                   // min(B, L)
+  double* logz;             // [units] or null
+  double* logp;             // [units] or null (needs kept)
+  float* col_m;             // [units][L] band column (K > logz_band_entries()) or null
+  int* col_k;
+  int units, L, B;
+  int K;                    // min(B, L - B); 0 when B >= L
+  int neg;                  // 1: the programme runs over exp(-r) (K = L - B < B)
+  float tau;
 };
 
 struct KLArgs {
@@ -83,6 +101,9 @@ size_t decode_lds_bytes(int L, int G, int D, bool feat);
 bool decode_fits_lds(int L, int G, int D);
 int decode_chunk_rows();
 int launch_evict(const EvictArgs& a, int dtype, int D, void* stream);
+int launch_logz(const LogzArgs& a, void* stream);
+size_t logz_ws_bytes(int units, int L, int B);
+int logz_band_entries();
 int evict_max_len();
 size_t evict_ws_bytes(int units, int L);
 int launch_kl(const KLArgs& a, void* stream);

@@ -23,6 +23,36 @@ __device__ __forceinline__ uint64_t row_key(float s, int32_t pos) {
   return ((uint64_t)score_key(s) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)pos);
 }
 
+// Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32
+// multiplies with the key advanced by the Weyl constants; only the first output
+// word is used.
+__device__ __forceinline__ uint32_t philox4x32_10_w0(uint32_t c0, uint32_t c1, uint32_t c2,
+                                                     uint32_t c3, uint32_t k0, uint32_t k1) {
+#pragma unroll
+  for (int r = 0; r < 10; ++r) {
+    const uint32_t h0 = __umulhi(0xD2511F53u, c0), l0 = 0xD2511F53u * c0;
+    const uint32_t h1 = __umulhi(0xCD9E8D57u, c2), l1 = 0xCD9E8D57u * c2;
+    c0 = h1 ^ c1 ^ k0;
+    c1 = l1;
+    c2 = h0 ^ c3 ^ k1;
+    c3 = l0;
+    k0 += 0x9E3779B9u;
+    k1 += 0xBB67AE85u;
+  }
+  return c0;
+}
+
+// Training-mode ranking score (Sec. 3.1.2 Gumbel perturbation, App. C
+// temperature): s / tau + g with g = -ln(-ln U) a standard Gumbel draw, U
+// taken from Philox with counter (position, unit, draw, 0) so that a token
+// keeps its draw wherever its row sits.  U = (2 (x >> 9) + 1) 2^-24 is exact in
+// float32 and strictly inside (0, 1).
+__device__ __forceinline__ float sampled_score(const EvictArgs& a, float s, int32_t pos, int unit) {
+  const uint32_t x = philox4x32_10_w0((uint32_t)pos, (uint32_t)unit, a.draw, 0u, a.seed0, a.seed1);
+  const float U = (float)(2u * (x >> 9) + 1u) * 0x1p-24f;
+  return s / a.tau - logf(-logf(U));
+}
+
 // Feature vector x = [alpha, ||v||, H = num/den (0 if den = 0), pos / T].
 __device__ __forceinline__ void make_features(float alpha, float vnorm, double num, double den,
                                               int32_t p, float invT, float x[4]) {

@@ -136,3 +136,52 @@ def test_workspace_sizes():
     assert B.dc_workspace_bytes(d, 4097, 0, 0) < big
     assert B.dc_workspace_bytes(d, 0, 8, 32768) >= 8 * 512 * 16
     assert B.dc_workspace_bytes(_dims(head_dim=96), 100, 0, 0) == 0
+
+
+def _logprob(units=4, length=100, budget=10, tau=1.0, scores=FAKE, kept=FAKE, logz=FAKE,
+             logp=FAKE, ws=None, wsb=0):
+    return B.lib().dc_subset_log_prob(units, length, budget, tau, scores, kept, logz, logp, ws,
+                                      wsb, None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(scores=None), 1), (dict(kept=None), 1), (dict(units=0), 2), (dict(length=0), 2),
+    (dict(budget=0), 5), (dict(tau=0.0), 8), (dict(tau=-1.0), 8), (dict(tau=float("nan")), 8),
+    (dict(tau=float("inf")), 8), (dict(length=40961), 3), (dict(units=(1 << 24) + 1), 3),
+    # K = min(B, L - B) = 5000 > 4096 needs the band workspace
+    (dict(length=10000, budget=5000), 6), (dict(length=10000, budget=5000, ws=FAKE, wsb=16), 6)])
+def test_subset_log_prob_rejects_bad_arguments(kw, status):
+    assert _logprob(**kw) == status
+
+
+def test_subset_log_prob_workspace_sizes():
+    W = B.dc_subset_log_prob_workspace_bytes
+    assert W(4, 8192, 4096) == 0                 # K = 4096 fits one band
+    assert W(4, 10000, 5000) == 4 * 10000 * 8    # K = 5000: one float and one int per row
+    assert W(4, 10000, 9000) == 0                # K = 1000 through the complement
+    assert W(0, 100, 10) == 0 and W(4, 0, 10) == 0 and W(4, 100, 0) == 0
+    assert W(1, 40961, 20000) == 0
+
+
+def test_sample_evict_rejects_bad_arguments():
+    L = B.lib()
+    pol = B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)
+    for tau, want in [(0.0, 8), (float("nan"), 8), (-2.0, 8), (float("inf"), 8)]:
+        kv = B.dc_kv(FAKE, FAKE, 10)
+        feat = _feat()
+        g = B.make_gumbel(tau, 1, 0)
+        st = L.dc_sample_evict(ctypes.byref(_dims()), ctypes.byref(kv), ctypes.byref(feat),
+                               ctypes.byref(pol), 5, ctypes.byref(g), FAKE, FAKE, FAKE, None, 0, None)
+        assert st == want and kv.len == 10
+    kv = B.dc_kv(FAKE, FAKE, 10)
+    g = B.make_gumbel(1.0, 1, 0)
+    # no gumbel struct; logp_out without scores_out / kept_out
+    assert L.dc_sample_evict(ctypes.byref(_dims()), ctypes.byref(kv), ctypes.byref(_feat()),
+                             ctypes.byref(pol), 5, None, FAKE, FAKE, FAKE, None, 0, None) == 1
+    assert L.dc_sample_evict(ctypes.byref(_dims()), ctypes.byref(kv), ctypes.byref(_feat()),
+                             ctypes.byref(pol), 5, ctypes.byref(g), None, FAKE, FAKE, None, 0, None) == 1
+    assert L.dc_sample_evict(ctypes.byref(_dims()), ctypes.byref(kv), ctypes.byref(_feat()),
+                             ctypes.byref(pol), 5, ctypes.byref(g), FAKE, None, FAKE, None, 0, None) == 1
+    assert L.dc_sample_evict(ctypes.byref(_dims()), ctypes.byref(kv), ctypes.byref(_feat()),
+                             ctypes.byref(pol), 0, ctypes.byref(g), FAKE, FAKE, FAKE, None, 0, None) == 5
+    assert kv.len == 10
