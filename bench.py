@@ -275,14 +275,28 @@ def bench_teacher_student_kl(args, wl, dev, log):
     sh = stream_handle()
     parts = {"teacher": [], "student": [], "kl": [], "step": []}
     first_ms = None
+    train = args.train_select
+    if train:
+        # training-mode student: Gumbel-perturbed top-B and log pi of the kept set
+        sc_flat = torch.empty(U * (wl.n0 + 1), dtype=torch.float32, device=dev)
+        kept = torch.empty((U, wl.budget), dtype=torch.int32, device=dev)
+        logp = torch.empty(U, dtype=torch.float64, device=dev)
+        parts["sample"] = []
     for t in range(nsteps):
         sg.queries(wl, t, q)
         sg.new_rows(wl, t, kn, vn, U)
-        ev = _events(4)
+        ev = _events(5)
         ev[0].record()
         tea.decode_step(q, kn, vn, o_t, features=False)
         ev[1].record()
-        stu.decode_evict(pol, wl.budget, q, kn, vn, o_s)
+        if train:
+            stu.decode_step(q, kn, vn, o_s)
+            ev[4].record()
+            L = stu.kv.len
+            stu.sample_evict(pol, wl.budget, B.make_gumbel(1.0, wl.seed, t),
+                             sc_flat[:U * L].view(U, L), kept, logp)
+        else:
+            stu.decode_evict(pol, wl.budget, q, kn, vn, o_s)
         ev[2].record()
         B.dc_kl_reward(rows, hid, voc, hf[t], hc[t], w, kl, ws, ws.numel(), sh)
         ev[3].record()
@@ -296,7 +310,14 @@ def bench_teacher_student_kl(args, wl, dev, log):
             parts["student"].append(ev[1].elapsed_time(ev[2]))
             parts["kl"].append(ev[2].elapsed_time(ev[3]))
             parts["step"].append(ev[0].elapsed_time(ev[3]))
+            if train:
+                parts["sample"].append(ev[4].elapsed_time(ev[2]))
     m = {k: float(np.mean(v)) for k, v in parts.items()}
+    extra = {}
+    if train:
+        extra = {"student_select": "gumbel top-B + log pi (training mode)",
+                 "sample_evict_ms": round(m["sample"], 4)}
+        extra.update(time_log_partition(wl, U, dev, log))
     Lt = wl.n0 + 1 + args.warmup + args.steps / 2.0
     kvb = U * (Lt + wl.budget + 1) * 2 * D * 2 + voc * hid * 2
     return {"value": round(1e3 / m["step"], 3), "unit": "decode steps/s",
@@ -307,7 +328,48 @@ def bench_teacher_student_kl(args, wl, dev, log):
             "kl_ms": round(m["kl"], 4), "first_step_ms": round(first_ms, 3),
             "kl_gbps": round(voc * hid * 2 / (m["kl"] * 1e-3) / 1e9, 1),
             "note": "teacher K/V read + student K/V read + lm head per step; steps timed "
-                    "one by one (events per part)"}
+                    "one by one (events per part)", **extra}
+
+
+LOGZ_OPS_PER_UPDATE = 7     # VALU instructions of one recursion update (see the design notes)
+VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # lane-instructions/s without packed math
+
+
+def time_log_partition(wl, U, dev, log, reps=5):
+    """dc_subset_log_prob alone at the compression step (L = n0 + 1 -> budget) and
+    at the one-eviction step (budget + 1 -> budget), inputs resident."""
+    import torch
+    from paper_2608_08878_amd import binding as B
+    from paper_2608_08878_amd.buffers import stream_handle
+    out = {}
+    for tag, L in (("compress", wl.n0 + 1), ("evict1", wl.budget + 1)):
+        Bk = wl.budget
+        K = min(Bk, L - Bk)
+        g = torch.Generator(device=dev).manual_seed(5)
+        s = torch.randn((U, L), generator=g, device=dev) * 3.0
+        kept = torch.arange(Bk, dtype=torch.int32, device=dev).repeat(U, 1)
+        lz = torch.empty(U, dtype=torch.float64, device=dev)
+        lp = torch.empty(U, dtype=torch.float64, device=dev)
+        need = B.dc_subset_log_prob_workspace_bytes(U, L, Bk)
+        ws = torch.empty(max(need, 1), dtype=torch.uint8, device=dev)
+        sh = stream_handle()
+        B.dc_subset_log_prob(U, L, Bk, 1.0, s, kept, lz, lp, ws, need, sh)
+        torch.cuda.synchronize()
+        ev = _events(2)
+        ev[0].record()
+        for _ in range(reps):
+            B.dc_subset_log_prob(U, L, Bk, 1.0, s, kept, lz, lp, ws, need, sh)
+        ev[1].record()
+        torch.cuda.synchronize()
+        ms = ev[0].elapsed_time(ev[1]) / reps
+        upd = U * L * max(K, 1)
+        out[f"logz_{tag}_ms"] = round(ms, 4)
+        out[f"logz_{tag}_shape"] = f"units={U} L={L} B={Bk} K={K}"
+        if K > 8:
+            tops = upd * LOGZ_OPS_PER_UPDATE / (ms * 1e-3) / 1e12
+            out[f"logz_{tag}_alu_frac"] = round(tops / VALU_PEAK_TOPS, 4)
+        log(f"log-partition {tag}: {ms:.4f} ms ({U} units, L={L}, K={K})")
+    return out
 
 
 def main():
@@ -319,6 +381,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-shrink", action="store_true",
                     help="keep the steady steps in the capacity-16385 buffers of step 0")
+    ap.add_argument("--train-select", action="store_true",
+                    help="workload 5: the student keeps a Gumbel-sampled top-B and computes "
+                         "log pi (training mode) instead of the deterministic selection")
     ap.add_argument("--cpu-units", type=int, default=64)
     ap.add_argument("--cpu-steps", type=int, default=96)
     ap.add_argument("--calib-copy-mib", type=int, default=1024,

@@ -18,6 +18,8 @@ Every value is computed in binary64 from the exact stored input values
 * ``kl``         – the per-step reward R_t = -KL(P_t || P^_t) (Sec. 3.1.4).
 * ``sampling``   – training-mode selection: Gumbel-perturbed top-B, the exact
   log-partition log Z(s, B, tau) and log pi(a | s) (Sec. 3.1.2, App. C).
+* ``reinforce``  – rollout reward math of the REINFORCE update: discounted
+  returns, RLOO and EMA baselines, entropy surrogate, loss (Sec. 3.2).
 * ``unit``       – one unit's cache and feature state stepped through
   append -> attention -> features -> score -> select -> prune (Algorithm 1,
   Sec. 3.1.3 for the student/teacher caches).

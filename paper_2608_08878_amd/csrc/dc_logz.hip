@@ -14,12 +14,12 @@
 //   E_i[j] = E_{i-1}[j] + x_i E_{i-1}[j - 1],   E[0] = 1,
 // adds positive terms only, so it runs in linear space: each entry is a
 // float32 mantissa in [0.5, 1) with its own int32 exponent (the entries span
-// far more than any floating-point exponent range), renormalised after every
-// update with frexp.  One update is one fused multiply-add plus exponent
-// bookkeeping (no transcendental), and it is more accurate than log-space
-// float32: every term is positive, so the relative error of E_L[K] stays
-// below about (K + L) 2^-24 (rounding of the weights plus one rounding per
-// update).
+// far more than any floating-point exponent range), renormalised with frexp
+// once per 64 updates.  One update is one fused multiply-add plus exponent
+// alignment (seven VALU instructions, no transcendental), and it is more
+// accurate than log-space float32: every term is positive, so the relative
+// error of E_L[K] stays below about (K + L) 2^-24 (rounding of the weights plus
+// one rounding per update).
 //
 // Two layouts, one wave (64 lanes) per unit:
 //  - K <= 8 (row split): every lane folds the rows i = lane (mod 64) into its
@@ -67,14 +67,25 @@ __device__ __forceinline__ void norm(float v, int kn, float& m, int& k) {
   k = kn + __builtin_amdgcn_frexp_expf(v);
 }
 
-// E[j] <- E[j] + x E[j-1]  (x = xm 2^xk; (pm, pk) the previous E[j-1]).
+// E[j] <- E[j] + x E[j-1]  (x = xm 2^xk, xm in [0.5, 1); (pm, pk) the previous
+// E[j-1]).  Both terms are aligned to the larger exponent and the sum keeps
+// that exponent without renormalising: the mantissa of the aligned-to term is
+// at most halved (x's mantissa) and the sum at most doubled per update, so
+// after at most RENORM updates from [0.5, 1) every mantissa lies in
+// [2^-65, 2^64], far inside float32's normal range, and a term shifted below
+// float32's range is under 2^-61 of the sum it joins.
 __device__ __forceinline__ void upd(float& m, int& k, float pm, int pk, float xm, int xk) {
   const int kb = pk + xk;
   const int kn = k > kb ? k : kb;
   const float a = __builtin_amdgcn_ldexpf(m, k - kn);
   const float b = __builtin_amdgcn_ldexpf(pm, kb - kn);
-  norm(__builtin_fmaf(xm, b, a), kn, m, k);
+  m = __builtin_fmaf(xm, b, a);
+  k = kn;
 }
+
+constexpr int RENORM = 64;   // updates between renormalisations (one row batch)
+
+__device__ __forceinline__ void renorm(float& m, int& k) { norm(m, k, m, k); }
 
 // Weight exp(z), z <= 0, as (m, k): z = n ln2 + f with f in [0, ln2) (Cody-Waite).
 __device__ __forceinline__ void weight(double z, float& m, int& k) {
@@ -195,13 +206,18 @@ __global__ void __launch_bounds__(64) logz_rows_kernel(LogzArgs a) {
     m[j] = 0.0f;
     k[j] = KZERO;
   }
-  for (int i = lane; i < a.L; i += 64) {
-    float xm;
-    int xk;
-    row_weight(a, s[i], st.shift, xm, xk);
+  for (int i0 = 0; i0 < a.L; i0 += 64 * RENORM) {
+    const int iend = a.L < i0 + 64 * RENORM ? a.L : i0 + 64 * RENORM;
+    for (int i = i0 + lane; i < iend; i += 64) {
+      float xm;
+      int xk;
+      row_weight(a, s[i], st.shift, xm, xk);
 #pragma unroll
-    for (int j = KS - 1; j >= 1; --j) upd(m[j], k[j], m[j - 1], k[j - 1], xm, xk);
-    upd(m[0], k[0], 0.5f, 1, xm, xk);
+      for (int j = KS - 1; j >= 1; --j) upd(m[j], k[j], m[j - 1], k[j - 1], xm, xk);
+      upd(m[0], k[0], 0.5f, 1, xm, xk);
+    }
+#pragma unroll
+    for (int j = 0; j < KS; ++j) renorm(m[j], k[j]);
   }
 #pragma unroll
   for (int d = 1; d < 64; d <<= 1) {
@@ -261,7 +277,9 @@ __global__ void __launch_bounds__(64) logz_col_kernel(LogzArgs a) {
             ink = ck[i0 + lane];
           }
         }
-        for (int r = 0; r < n; ++r) {
+        // one row: entry l C + 1 takes lane l - 1's top entry (lane 0: the band
+        // column, or E[0] = 1); the band's top entry is recorded before the update
+        auto row = [&](int r) {
           const float sxm = rdl(xm, r);
           const int sxk = rdl(xk, r);
           float nm = __shfl_up(m[C - 1], 1);
@@ -281,7 +299,19 @@ __global__ void __launch_bounds__(64) logz_col_kernel(LogzArgs a) {
 #pragma unroll
           for (int t = C - 1; t >= 1; --t) upd(m[t], k[t], m[t - 1], k[t - 1], sxm, sxk);
           upd(m[0], k[0], nm, nk, sxm, sxk);
+        };
+        // two rows per trip (written out: the loop holds cross-lane operations,
+        // which the compiler does not unroll), so that the exponents alternate
+        // between two register sets instead of being copied back every row
+        int r = 0;
+        for (; r + 1 < n; r += 2) {
+          row(r);
+          row(r + 1);
         }
+        if (r < n) row(r);
+        static_assert(RENORM >= 64, "one renormalisation per row batch");
+#pragma unroll
+        for (int t = 0; t < C; ++t) renorm(m[t], k[t]);
         if (wr && lane < n) {
           cm[i0 + lane] = outm;
           ck[i0 + lane] = outk;
