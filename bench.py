@@ -314,6 +314,27 @@ def bench_teacher_student_kl(args, wl, dev, log):
                 parts["sample"].append(ev[4].elapsed_time(ev[2]))
     m = {k: float(np.mean(v)) for k, v in parts.items()}
     extra = {}
+    # the same rewards deferred to the end of the rollout: one call over all
+    # steps x batch rows reads the lm head once
+    Td = nsteps
+    wsd = torch.empty(B.dc_workspace_bytes(stu.dims, 0, Td * rows, voc), dtype=torch.uint8, device=dev)
+    kld = torch.empty(Td * rows, dtype=torch.float32, device=dev)
+    hfv, hcv = hf.view(Td * rows, hid), hc.view(Td * rows, hid)
+    B.dc_kl_reward(Td * rows, hid, voc, hfv, hcv, w, kld, wsd, wsd.numel(), sh)
+    torch.cuda.synchronize()
+    ev = _events(2)
+    ev[0].record()
+    for _ in range(3):
+        B.dc_kl_reward(Td * rows, hid, voc, hfv, hcv, w, kld, wsd, wsd.numel(), sh)
+    ev[1].record()
+    torch.cuda.synchronize()
+    kd_ms = ev[0].elapsed_time(ev[1]) / 3
+    flops = 2.0 * 2 * Td * rows * hid * voc
+    extra.update({"kl_deferred_rows": Td * rows, "kl_deferred_ms": round(kd_ms, 4),
+                  "kl_deferred_ms_per_step": round(kd_ms / Td, 4),
+                  "kl_deferred_tflops": round(flops / (kd_ms * 1e-3) / 1e12, 1)})
+    log(f"deferred KL over {Td} steps x {rows} rows: {kd_ms:.3f} ms "
+        f"({kd_ms / Td:.4f} ms per step vs {m['kl']:.4f} per-step calls)")
     if train:
         extra = {"student_select": "gumbel top-B + log pi (training mode)",
                  "sample_evict_ms": round(m["sample"], 4)}

@@ -249,17 +249,55 @@ dc_status dc_subset_log_prob(int32_t units, int32_t len, int32_t budget, float t
 /* Workspace bytes of dc_subset_log_prob (0 for invalid sizes). */
 size_t dc_subset_log_prob_workspace_bytes(int32_t units, int32_t len, int32_t budget);
 
+/* Largest row count of one dc_kl_reward call. */
+#define DC_KL_MAX_ROWS 16384
+
 /* Per-step KL reward (Sec. 3.1.4): for each row r,
  *   kl_out[r] = KL(P || Q) = sum_v P_v (ln P_v - ln Q_v)   (nats),
  * P = softmax(h_full[r] W^T), Q = softmax(h_comp[r] W^T) over the whole vocab.
  *   h_full, h_comp  [rows][hidden] bfloat16
  *   w_lm            [vocab][hidden] bfloat16 (the lm-head weight)
  *   kl_out          [rows] float32; the reward is R = -kl_out.
- * Supported: hidden % 128 == 0, vocab % 64 == 0, 1 <= rows <= 64.
+ * Rows are independent, so a training loop may defer the rewards of a whole
+ * rollout (steps x batch rows, the hidden states kept per step) to one call:
+ * the lm head is then read once for all of them.
+ * Supported: hidden % 128 == 0, vocab % 64 == 0, 1 <= rows <= DC_KL_MAX_ROWS.
  * Errors: DC_ERR_NULL, DC_ERR_SHAPE, DC_ERR_UNSUPPORTED, DC_ERR_WORKSPACE. */
 dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void *h_full,
                        const void *h_comp, const void *w_lm, float *kl_out, void *ws,
                        size_t ws_bytes, void *hip_stream);
+
+/* Hyper-parameters of the REINFORCE update (Sec. 3.2; App. D gives gamma =
+ * 0.99 and beta = 0.01). */
+typedef struct {
+  double gamma;       /* discount factor, 0 <= gamma <= 1 */
+  double beta;        /* entropy regularisation coefficient, finite */
+  double ema_decay;   /* decay d of the exponential-moving-average baseline, 0 <= d < 1 */
+} dc_reinforce_cfg;
+
+/* Rollout reward math of the REINFORCE update with entropy regularisation and
+ * variance-reduction baselines (Sec. 3.2), for `steps` decode steps of
+ * `rollouts` sampled rollouts.  All arrays are row-major [steps][rollouts]:
+ *   rewards       float32 R[t][k] = -KL_t (dc_kl_reward)
+ *   logp          float64 log pi(a_t | s_t) of the sampled kept sets
+ *                 (dc_sample_evict, dc_subset_log_prob)
+ *   returns_out   float64 G[t][k] = sum_{tau >= t} gamma^(tau - t) R[tau][k]   (required)
+ *   baseline_out  float64 b[t][k]: the mean return of the other rollouts at step t
+ *                 (leave-one-out, rollouts >= 2), else the EMA baseline      (or NULL)
+ *   adv_out       float64 A = G - b                                          (or NULL)
+ *   weight_out    float64 d loss / d log pi = -(A - beta) / (steps rollouts) (or NULL)
+ *   stats_out     float64 [3]: loss = -mean(log pi A - beta log pi) (the
+ *                 entropy term uses the single-sample surrogate -log pi), the
+ *                 mean surrogate entropy, the mean return               (or NULL)
+ *   ema           float64 [1], in/out: the EMA baseline e; after the call
+ *                 e = d e + (1 - d) mean(G)
+ * One small float64 kernel, deterministic.  Errors: DC_ERR_NULL, DC_ERR_SHAPE
+ * (steps or rollouts < 1), DC_ERR_UNSUPPORTED (steps * rollouts > 2^26),
+ * DC_ERR_VALUE (gamma, beta, ema_decay out of range). */
+dc_status dc_reinforce_terms(int32_t steps, int32_t rollouts, const dc_reinforce_cfg *cfg,
+                             const float *rewards, const double *logp, double *ema,
+                             double *returns_out, double *baseline_out, double *adv_out,
+                             double *weight_out, double *stats_out, void *hip_stream);
 
 /* Static string naming a status. */
 const char *dc_status_str(dc_status s);

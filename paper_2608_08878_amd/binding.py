@@ -50,9 +50,16 @@ def make_gumbel(tau: float, seed: int, draw: int) -> dc_gumbel:
     return dc_gumbel(tau, s, draw & 0xFFFFFFFF)
 
 
+class dc_reinforce_cfg(ctypes.Structure):
+    _fields_ = [("gamma", ctypes.c_double), ("beta", ctypes.c_double), ("ema_decay", ctypes.c_double)]
+
+
+KL_MAX_ROWS = 16384
+
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
            "dc_decode_evict", "dc_sample_evict", "dc_subset_log_prob",
-           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_status_str")
+           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_reinforce_terms",
+           "dc_status_str")
 
 _lib = None
 
@@ -92,6 +99,9 @@ def lib() -> ctypes.CDLL:
         L.dc_subset_log_prob_workspace_bytes.restype = sz
         L.dc_kl_reward.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
         L.dc_kl_reward.restype = ctypes.c_int
+        L.dc_reinforce_terms.argtypes = [i32, i32, ctypes.POINTER(dc_reinforce_cfg), vp, vp, vp,
+                                         vp, vp, vp, vp, vp, vp]
+        L.dc_reinforce_terms.restype = ctypes.c_int
         L.dc_status_str.argtypes = [ctypes.c_int]
         L.dc_status_str.restype = ctypes.c_char_p
         _lib = L
@@ -176,3 +186,11 @@ def dc_subset_log_prob(units: int, length: int, budget: int, tau: float, scores,
 
 def dc_subset_log_prob_workspace_bytes(units: int, length: int, budget: int) -> int:
     return int(lib().dc_subset_log_prob_workspace_bytes(units, length, budget))
+
+
+def dc_reinforce_terms(steps: int, rollouts: int, cfg, rewards, logp, ema, returns_out,
+                       baseline_out=None, adv_out=None, weight_out=None, stats_out=None,
+                       stream=None) -> None:
+    _check(lib().dc_reinforce_terms(steps, rollouts, ctypes.byref(cfg), _ptr(rewards), _ptr(logp),
+                                    _ptr(ema), _ptr(returns_out), _ptr(baseline_out),
+                                    _ptr(adv_out), _ptr(weight_out), _ptr(stats_out), stream))

@@ -125,6 +125,34 @@ dc_status dc_feat_init(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, int3
   return DC_OK;
 }
 
+dc_status dc_reinforce_terms(int32_t steps, int32_t rollouts, const dc_reinforce_cfg* cfg,
+                             const float* rewards, const double* logp, double* ema,
+                             double* returns_out, double* baseline_out, double* adv_out,
+                             double* weight_out, double* stats_out, void* hip_stream) {
+  if (!cfg || !rewards || !logp || !ema || !returns_out) return DC_ERR_NULL;
+  if (steps < 1 || rollouts < 1) return DC_ERR_SHAPE;
+  if ((int64_t)steps * rollouts > (1 << 26)) return DC_ERR_UNSUPPORTED;
+  if (!(cfg->gamma >= 0.0 && cfg->gamma <= 1.0) || !isfinite(cfg->beta) ||
+      !(cfg->ema_decay >= 0.0 && cfg->ema_decay < 1.0))
+    return DC_ERR_VALUE;
+  dc::ReinforceArgs a;
+  a.rewards = rewards;
+  a.logp = logp;
+  a.ema = ema;
+  a.returns = returns_out;
+  a.baseline = baseline_out;
+  a.adv = adv_out;
+  a.weight = weight_out;
+  a.stats = stats_out;
+  a.steps = steps;
+  a.rollouts = rollouts;
+  a.gamma = cfg->gamma;
+  a.beta = cfg->beta;
+  a.ema_decay = cfg->ema_decay;
+  if (dc::launch_reinforce(a, hip_stream) != 0) return DC_ERR_HIP;
+  return DC_OK;
+}
+
 }  // extern "C"
 
 namespace {
@@ -417,7 +445,7 @@ dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void* 
                        size_t ws_bytes, void* hip_stream) {
   if (!h_full || !h_comp || !w_lm || !kl_out) return DC_ERR_NULL;
   if (rows < 1 || hidden < 1 || vocab < 1) return DC_ERR_SHAPE;
-  if (rows > 64 || hidden % 128 || vocab % dc::kl_tile_cols()) return DC_ERR_UNSUPPORTED;
+  if (rows > DC_KL_MAX_ROWS || hidden % 128 || vocab % dc::kl_tile_cols()) return DC_ERR_UNSUPPORTED;
   const size_t need = kl_bytes(rows, vocab);
   if (!ws || ws_bytes < need) return DC_ERR_WORKSPACE;
   dc::KLArgs a;

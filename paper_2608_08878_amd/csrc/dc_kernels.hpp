@@ -84,6 +84,20 @@ struct LogzArgs {
   float tau;
 };
 
+// REINFORCE rollout terms over [steps][rollouts] arrays.
+struct ReinforceArgs {
+  const float* rewards;
+  const double* logp;
+  double* ema;              // [1] in/out
+  double* returns;          // required (also read back by the baseline pass)
+  double* baseline;         // optional outputs
+  double* adv;
+  double* weight;
+  double* stats;            // [3] loss, mean entropy surrogate, mean return (optional)
+  int steps, rollouts;
+  double gamma, beta, ema_decay;
+};
+
 struct KLArgs {
   const void* h_full;
   const void* h_comp;
@@ -102,6 +116,7 @@ bool decode_fits_lds(int L, int G, int D);
 int decode_chunk_rows();
 int launch_evict(const EvictArgs& a, int dtype, int D, void* stream);
 int launch_logz(const LogzArgs& a, void* stream);
+int launch_reinforce(const ReinforceArgs& a, void* stream);
 size_t logz_ws_bytes(int units, int L, int B);
 int logz_band_entries();
 int evict_max_len();

@@ -61,11 +61,19 @@ __device__ __forceinline__ float max16(float x) {
   return x;
 }
 
-// grid: (vocab / 64, ceil(rows / 8)); block: 256 threads (4 waves).
+// grid: 8 ceil(tiles / 8) ceil(rows / 8) workgroups of 256 threads (4 waves).
+// Workgroups are dealt to the 8 XCDs round-robin by index, so index g runs on
+// XCD g mod 8; every 8-row block of one 64-column vocabulary tile is given to
+// the same XCD back to back, and the tile's lm-head slab (64 x hidden bf16) is
+// fetched from HBM once and then served from that XCD's L2 to the other row
+// blocks (many rows: the deferred reward of a whole rollout in one call).
 __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   __shared__ float red[KL_WAVES][8][4];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int tile = blockIdx.x, rb = blockIdx.y;
+  const int nrb = (a.rows + 7) / 8;
+  const int slot = blockIdx.x >> 3;
+  const int tile = (blockIdx.x & 7) + 8 * (slot / nrb), rb = slot % nrb;
+  if (tile >= a.ntiles) return;      // whole workgroup: no barrier is skipped
   const int n0 = tile * KL_TILE + wave * 16;      // this wave's 16 columns
   const int i = lane & 15, kg = lane >> 4;        // MFMA row/col index, k group
   // A row i: rows 0..7 full, 8..15 compressed, of kl rows rb*8 + (i & 7)
@@ -237,8 +245,9 @@ int kl_tile_cols() { return KL_TILE; }
 
 int launch_kl(const KLArgs& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  dim3 g1(a.vocab / KL_TILE, (a.rows + 7) / 8);
-  hipLaunchKernelGGL(kl_tile_kernel, g1, dim3(64 * KL_WAVES), 0, s, a);
+  const int nrb = (a.rows + 7) / 8;
+  const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
+  hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), 0, s, a);
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();
 }

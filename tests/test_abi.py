@@ -122,7 +122,7 @@ def test_kl_reward_rejects_bad_arguments():
     L = B.lib()
     assert L.dc_kl_reward(8, 4096, 32768, None, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 1
     assert L.dc_kl_reward(0, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 2
-    assert L.dc_kl_reward(65, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
+    assert L.dc_kl_reward(B.KL_MAX_ROWS + 1, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40, None) == 3
     assert L.dc_kl_reward(8, 4000, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
     assert L.dc_kl_reward(8, 4096, 32700, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
     assert L.dc_kl_reward(8, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == 6
@@ -185,3 +185,21 @@ def test_sample_evict_rejects_bad_arguments():
     assert L.dc_sample_evict(ctypes.byref(_dims()), ctypes.byref(kv), ctypes.byref(_feat()),
                              ctypes.byref(pol), 0, ctypes.byref(g), FAKE, FAKE, FAKE, None, 0, None) == 5
     assert kv.len == 10
+
+
+def test_reinforce_terms_rejects_bad_arguments():
+    L = B.lib()
+    ok = B.dc_reinforce_cfg(0.99, 0.01, 0.9)
+
+    def call(steps=64, rollouts=8, cfg=ok, r=FAKE, lp=FAKE, ema=FAKE, ret=FAKE):
+        return L.dc_reinforce_terms(steps, rollouts, None if cfg is None else ctypes.byref(cfg), r,
+                                    lp, ema, ret, None, None, None, None, None)
+
+    assert call(cfg=None) == 1 and call(r=None) == 1 and call(lp=None) == 1
+    assert call(ema=None) == 1 and call(ret=None) == 1
+    assert call(steps=0) == 2 and call(rollouts=0) == 2
+    assert call(steps=1 << 14, rollouts=1 << 13) == 3
+    for cfg in (B.dc_reinforce_cfg(1.5, 0.01, 0.9), B.dc_reinforce_cfg(-0.1, 0.01, 0.9),
+                B.dc_reinforce_cfg(float("nan"), 0.01, 0.9), B.dc_reinforce_cfg(0.99, float("inf"), 0.9),
+                B.dc_reinforce_cfg(0.99, 0.01, 1.0), B.dc_reinforce_cfg(0.99, 0.01, -0.5)):
+        assert call(cfg=cfg) == 8
