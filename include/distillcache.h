@@ -267,6 +267,15 @@ dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void *
                        const void *h_comp, const void *w_lm, float *kl_out, void *ws,
                        size_t ws_bytes, void *hip_stream);
 
+/* Dynamic budget (App. D, experimental protocol): the budget of a decode step
+ * scales with the sequence, B_t = max(floor(ratio * seq_len), b_min).  The
+ * paper writes the length as the cache size |C_t|, which would shrink the
+ * budget geometrically once eviction starts; here seq_len is the number of
+ * tokens seen (dc_feat.next_pos after the step's append).  The product is
+ * formed in binary64 from the float32 ratio.  Host function: no device work.
+ * Returns -1 unless 0 < ratio <= 1, seq_len >= 0 and b_min >= 1. */
+int32_t dc_dynamic_budget(float ratio, int32_t seq_len, int32_t b_min);
+
 /* Hyper-parameters of the REINFORCE update (Sec. 3.2; App. D gives gamma =
  * 0.99 and beta = 0.01). */
 typedef struct {

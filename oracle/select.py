@@ -8,6 +8,10 @@ s_i > s_k, or s_i == s_k and i is the earlier token (smaller absolute
 position).  -0.0 equals +0.0.  A NaN score ranks below every number (and NaNs
 rank among themselves by position).  If B >= L every token is kept.
 
+Dynamic budget (App. D): B_t = max(floor(r T_t), B_min), with T_t read as the
+number of tokens seen (the paper's |C_t| would collapse the budget
+geometrically once eviction starts; reading recorded with the design notes).
+
 Parity pinned by: exhaustive enumeration of all size-B subsets on small L
 (the kept set maximises the score sum, ties resolved toward earlier tokens),
 |kept| = min(B, L), min kept score >= max evicted score, and all-equal scores.
@@ -36,3 +40,11 @@ def top_budget(scores, positions, budget: int) -> np.ndarray:
         raise ValueError("budget must be >= 1")
     order = ranking(scores, positions)
     return np.sort(order[:budget])
+
+
+def dynamic_budget(ratio: float, seq_len: int, b_min: int = 32) -> int:
+    """max(floor(ratio * seq_len), b_min); the ratio is taken as its float32 value."""
+    r = float(np.float32(ratio))
+    if not (0.0 < r <= 1.0) or seq_len < 0 or b_min < 1:
+        raise ValueError("ratio in (0, 1], seq_len >= 0, b_min >= 1")
+    return max(int(np.floor(r * seq_len)), b_min)

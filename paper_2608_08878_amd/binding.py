@@ -59,7 +59,7 @@ KL_MAX_ROWS = 16384
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
            "dc_decode_evict", "dc_sample_evict", "dc_subset_log_prob",
            "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_reinforce_terms",
-           "dc_status_str")
+           "dc_dynamic_budget", "dc_status_str")
 
 _lib = None
 
@@ -102,6 +102,8 @@ def lib() -> ctypes.CDLL:
         L.dc_reinforce_terms.argtypes = [i32, i32, ctypes.POINTER(dc_reinforce_cfg), vp, vp, vp,
                                          vp, vp, vp, vp, vp, vp]
         L.dc_reinforce_terms.restype = ctypes.c_int
+        L.dc_dynamic_budget.argtypes = [ctypes.c_float, i32, i32]
+        L.dc_dynamic_budget.restype = i32
         L.dc_status_str.argtypes = [ctypes.c_int]
         L.dc_status_str.restype = ctypes.c_char_p
         _lib = L
@@ -194,3 +196,7 @@ def dc_reinforce_terms(steps: int, rollouts: int, cfg, rewards, logp, ema, retur
     _check(lib().dc_reinforce_terms(steps, rollouts, ctypes.byref(cfg), _ptr(rewards), _ptr(logp),
                                     _ptr(ema), _ptr(returns_out), _ptr(baseline_out),
                                     _ptr(adv_out), _ptr(weight_out), _ptr(stats_out), stream))
+
+
+def dc_dynamic_budget(ratio: float, seq_len: int, b_min: int = 32) -> int:
+    return int(lib().dc_dynamic_budget(ratio, seq_len, b_min))

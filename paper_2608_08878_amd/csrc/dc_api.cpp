@@ -125,6 +125,12 @@ dc_status dc_feat_init(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, int3
   return DC_OK;
 }
 
+int32_t dc_dynamic_budget(float ratio, int32_t seq_len, int32_t b_min) {
+  if (!(ratio > 0.0f && ratio <= 1.0f) || seq_len < 0 || b_min < 1) return -1;
+  const double b = floor((double)ratio * (double)seq_len);
+  return b > (double)b_min ? (int32_t)b : b_min;
+}
+
 dc_status dc_reinforce_terms(int32_t steps, int32_t rollouts, const dc_reinforce_cfg* cfg,
                              const float* rewards, const double* logp, double* ema,
                              double* returns_out, double* baseline_out, double* adv_out,

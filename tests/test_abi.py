@@ -203,3 +203,15 @@ def test_reinforce_terms_rejects_bad_arguments():
                 B.dc_reinforce_cfg(float("nan"), 0.01, 0.9), B.dc_reinforce_cfg(0.99, float("inf"), 0.9),
                 B.dc_reinforce_cfg(0.99, 0.01, 1.0), B.dc_reinforce_cfg(0.99, 0.01, -0.5)):
         assert call(cfg=cfg) == 8
+
+
+def test_dynamic_budget_matches_the_oracle():
+    from oracle import select as osel
+    for r in (0.25, 0.125, 0.5, 0.1, 1.0, 0.3333):
+        for T in (0, 1, 31, 127, 128, 129, 1025, 4097, 8193, 16385, 40960, 123457):
+            assert B.dc_dynamic_budget(r, T, 32) == osel.dynamic_budget(r, T, 32), (r, T)
+    assert B.dc_dynamic_budget(0.0, 100, 32) == -1
+    assert B.dc_dynamic_budget(1.5, 100, 32) == -1
+    assert B.dc_dynamic_budget(float("nan"), 100, 32) == -1
+    assert B.dc_dynamic_budget(0.25, -1, 32) == -1
+    assert B.dc_dynamic_budget(0.25, 100, 0) == -1

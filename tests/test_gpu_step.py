@@ -525,3 +525,42 @@ def test_two_layer_policy_periodic_eviction():
                 assert torch.equal(a0, a1), (t, name)
             else:
                 assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
+
+
+def test_dynamic_budget_trajectory():
+    """The budget of every step follows max(floor(0.25 T), 32) (App. D protocol):
+    step 0 compresses 301 -> 75 rows, then the budget grows by one every four
+    tokens.  Fused steps on the device against the oracle until a near-tie."""
+    from paper_2608_08878_amd import binding as B
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=2, n_q_heads=8, n0=300, budget=75, steps=80)
+    U = wl.units
+    buf = _buffers(wl)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(wl.n0, 0)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    sts = [H.oracle_student(wl, u) for u in range(U)]
+    q, kn, vn = _step_tensors(wl)
+    lens = []
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        budget = B.dc_dynamic_budget(0.25, buf.feat.next_pos + 1, 32)
+        assert budget == osel.dynamic_budget(0.25, wl.n0 + t + 1, 32)
+        buf.decode_evict(pol, budget, q, kn, vn)
+        torch.cuda.synchronize()
+        lens.append(buf.kv.len)
+        diverged = False
+        for u in range(U):
+            ounit.decode_step(sts[u], *H.step_inputs_np(wl, t, u))
+            s_or = ounit.scores(sts[u], pnp, wl.hidden)
+            post = H.download_unit(buf, u)
+            ok, amb, flips = H.selection_check(s_or, sts[u].pos, post["pos"], budget)
+            assert ok, (t, u, amb, flips)
+            ounit.evict(sts[u], s_or, budget)
+            assert buf.kv.len == sts[u].L
+            diverged |= flips > 0
+        if diverged:
+            print("trajectories parted at a near-tie at step", t)
+            break
+    assert lens[0] == 75 and max(lens) <= 95

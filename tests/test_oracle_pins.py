@@ -331,3 +331,25 @@ def test_eviction_carries_rows_and_state():
     assert st.L == 20 and np.all(np.diff(st.pos) > 0)
     for arr, old in zip((st.K, st.V, st.pos, st.alpha, st.hist.z), before):
         assert np.array_equal(arr, old[kept])
+
+
+def test_dynamic_budget_schedule():
+    from oracle import select as osel
+    # the paper's protocol: ratio 0.25, minimum 32
+    assert osel.dynamic_budget(0.25, 8193) == 2048
+    assert osel.dynamic_budget(0.25, 100) == 32 and osel.dynamic_budget(0.25, 128) == 32
+    assert osel.dynamic_budget(0.25, 132) == 33
+    assert osel.dynamic_budget(0.125, 16384, 32) == 2048
+    # non-decreasing in the sequence length, and a cache that follows it loses at
+    # most one row per step once it is at the budget
+    L, prev = 300, 0
+    for T in range(301, 2000):
+        B = osel.dynamic_budget(0.25, T)
+        assert B >= prev
+        prev = B
+        newL = min(B, L + 1)
+        if T > 301:
+            assert L + 1 - newL <= 1
+        L = newL
+    with pytest.raises(ValueError):
+        osel.dynamic_budget(0.0, 10)
