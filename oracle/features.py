@@ -91,7 +91,24 @@ def entropy_feature(Z, N) -> np.ndarray:
 
 
 def feature_matrix(alpha, V, Z, N, pos, T: int) -> np.ndarray:
-    """x = [alpha, ||v||_2, H, pos/T] as an (L, 4) matrix."""
+    """x = [alpha, ||v||_2, H, pos/T] as an (L, 4) matrix (sigma left out)."""
     vnorm = np.sqrt((np.asarray(V, np.float64) ** 2).sum(axis=1))
     return np.stack([np.asarray(alpha, np.float64), vnorm, entropy_feature(Z, N),
                      np.asarray(pos, np.float64) / float(T)], axis=1)
+
+
+def head_variance(a) -> np.ndarray:
+    """sigma_i (Sec. 3.1.1): the variance over the G query heads of the unit of
+    the attention mass token i receives at the step, (1/G) sum_j (a_j(i) - abar(i))^2
+    with abar the head mean (population variance; 0 for G = 1).  Reading: taken at
+    the current step, like the attention the step's other features come from."""
+    a = np.asarray(a, np.float64)
+    G = a.shape[0]
+    mean = a.sum(axis=0) / G
+    return ((a - mean[None, :]) ** 2).sum(axis=0) / G
+
+
+def feature_matrix5(alpha, V, sigma, Z, N, pos, T: int) -> np.ndarray:
+    """x = [alpha, ||v||_2, sigma, H, pos/T] (the paper's five features, in its order)."""
+    x4 = feature_matrix(alpha, V, Z, N, pos, T)
+    return np.stack([x4[:, 0], x4[:, 1], np.asarray(sigma, np.float64), x4[:, 2], x4[:, 3]], axis=1)

@@ -53,6 +53,7 @@ class StudentState:
     G: int
     scale: float
     records: dict = field(default_factory=dict)
+    sigma: np.ndarray | None = None    # per-row head variance of the last step's attention
 
     @property
     def L(self) -> int:
@@ -78,7 +79,7 @@ def new_student(K, V, positions, *, G: int, scale: float, window: int = 64,
     return StudentState(K=K.copy(), V=V.copy(), pos=pos.copy(), alpha=np.zeros(L),
                         hist=features.WindowHistory(L, window), N=np.zeros(L), Z=np.zeros(L),
                         step=0, next_pos=int(pos.max()) + 1 if next_pos is None else next_pos,
-                        window=window, G=G, scale=scale)
+                        window=window, G=G, scale=scale, sigma=np.zeros(L))
 
 
 def new_teacher(K, V, positions, *, scale: float, next_pos: int | None = None) -> TeacherState:
@@ -112,6 +113,7 @@ def decode_step(st: StudentState, q, k_new=None, v_new=None) -> attention.Attent
         st.Z = np.append(st.Z, 0.0)
     att = attention.attend(q, st.K, st.V, st.scale)
     cz, cn = features.step_contributions(att.a, att.H)
+    st.sigma = features.head_variance(att.a)
     t = st.step
     st.alpha = st.alpha + cz / st.G
     st.hist.record(t, cz, cn)
@@ -131,13 +133,15 @@ def decode_step(st: StudentState, q, k_new=None, v_new=None) -> attention.Attent
     return att
 
 
-def feature_matrix(st: StudentState) -> np.ndarray:
+def feature_matrix(st: StudentState, n_in: int = 4) -> np.ndarray:
     Z, N = st.hist.sums()
+    if n_in == 5:
+        return features.feature_matrix5(st.alpha, st.V, st.sigma, Z, N, st.pos, st.next_pos)
     return features.feature_matrix(st.alpha, st.V, Z, N, st.pos, st.next_pos)
 
 
-def scores(st: StudentState, params, hidden) -> np.ndarray:
-    return policy.scores(params, feature_matrix(st), hidden)
+def scores(st: StudentState, params, hidden, n_in: int = 4, layer_norm: bool = False) -> np.ndarray:
+    return policy.scores(params, feature_matrix(st, n_in), hidden, layer_norm=layer_norm)
 
 
 def evict(st: StudentState, scores_, budget: int) -> np.ndarray:
@@ -146,6 +150,7 @@ def evict(st: StudentState, scores_, budget: int) -> np.ndarray:
     kept = select.top_budget(scores_, st.pos, budget)
     st.K, st.V, st.pos = st.K[kept], st.V[kept], st.pos[kept]
     st.alpha, st.N, st.Z = st.alpha[kept], st.N[kept], st.Z[kept]
+    st.sigma = st.sigma[kept]
     st.hist.keep_rows(kept)
     return kept
 
