@@ -83,14 +83,18 @@ typedef struct {
 } dc_kv;
 
 /* Per-token feature state of the student cache (Sec. 3.1.1, state space).
- * The feature vector is x_i = [alpha_i, ||v_i||_2, H_i, pos_i]:
+ * The feature vector is x_i = [alpha_i, ||v_i||_2, H_i, pos_i], or with a
+ * five-input policy the paper's full [alpha_i, ||v_i||_2, sigma_i, H_i, pos_i]:
  *   alpha_i  attention mass token i received, averaged over the G query heads
  *            of its unit and accumulated over decode steps;
  *   H_i      = ent_num_i / ent_den_i (0 when ent_den_i = 0), where over the
  *            queries q of the last w steps (each (step, query head) pair)
  *            ent_den_i = sum_q a_q(i) and ent_num_i = sum_q a_q(i) H(a_q),
  *            H(a) = -sum a ln a the entropy of the query's attention;
- *   pos_i    = pos[i] / T.
+ *   pos_i    = pos[i] / T;
+ *   sigma_i  variance over the G query heads of the attention weight token i
+ *            received at the last decode step, (1/G) sum_j (a_j(i) - mean_j a_j(i))^2
+ *            (population variance; 0 when G = 1).
  * Row arrays are [units][capacity] and follow the K/V slots.  The query ring
  * keeps, for each of the last w steps (slot = step mod w), the G queries and
  * their softmax statistics so that the contribution of step t - w can be
@@ -108,25 +112,35 @@ typedef struct {
   int32_t step;        /* host: decode steps done since the state was initialised */
   int32_t next_pos;    /* host: T, the position the next appended token receives */
   int32_t ring_pmax[DC_MAX_WINDOW]; /* host: per ring slot, largest position present (T - 1) */
+  float   *sigma;      /* [units][capacity] sigma_i of the last step, or NULL; written by
+                          every decode step and dc_feat_init (0) when present, moved by
+                          eviction; required by five-input policies */
 } dc_feat;
 
 /* Policy MLP f_phi (Sec. 3.1.2; a small ReLU MLP per App. D).  params is a
- * packed float32 blob, row-major:
- *   W1[hidden[0]][n_in], b1[hidden[0]],
- *   (W2[hidden[1]][hidden[0]], b2[hidden[1]]),   -- only if n_hidden_layers == 2
- *   w_out[hidden[last]], b_out
- * h = relu(W1 x + b1) [, h = relu(W2 h + b2)], s = w_out . h + b_out.
- * Supported: n_in = 4, n_hidden_layers in {1, 2}, hidden widths 1..128 (the
- * first width at most 64 when there are two hidden layers). */
+ * packed float32 blob, row-major, per hidden layer l (width h_l, input width
+ * h_{l-1}, h_0 = n_in):
+ *   W_l[h_l][h_{l-1}], b_l[h_l], (gain_l[h_l], bias_l[h_l] if layer_norm)
+ * followed by w_out[h_last], b_out.  Each hidden layer computes z = W h + b,
+ * then, with layer_norm, z = gain (z - mean z) / sqrt(var z + 1e-5) + bias over
+ * the layer's units (population variance), then h = relu(z); s = w_out . h + b_out.
+ * Inputs: n_in = 4 takes [alpha, ||v||, H, pos/T]; n_in = 5 takes the paper's
+ * [alpha, ||v||, sigma, H, pos/T] and needs dc_feat.sigma.
+ * Supported: n_in in {4, 5}, n_hidden_layers in {1, 2}, hidden widths 1..128
+ * (the first width at most 64 for a two-layer policy with n_in = 4 and no
+ * layer_norm, whose weights are staged on chip).  Four-input policies without
+ * layer_norm run inside the fused decode step; the others run in a separate
+ * scoring pass. */
 typedef struct {
   int32_t n_in;
   int32_t n_hidden_layers;
   int32_t hidden[2];
   const float *params;  /* device */
+  int32_t layer_norm;   /* 0 or 1 */
 } dc_policy;
 
 /* Bytes of caller workspace the entry points need for caches of up to max_len
- * rows per unit (dc_decode_step, dc_score_evict) and for a KL reward over
+ * rows per unit (dc_decode_step, dc_score_evict with any policy) and for a KL reward over
  * kl_rows rows of a kl_vocab-entry vocabulary (dc_kl_reward).  Pass 0 for the
  * parts not used.  Returns 0 for invalid dims. */
 size_t dc_workspace_bytes(const dc_dims *dims, int32_t max_len, int32_t kl_rows, int32_t kl_vocab);

@@ -33,12 +33,14 @@ class dc_feat(ctypes.Structure):
                 ("ent_den", ctypes.c_void_p), ("pos", ctypes.c_void_p),
                 ("vnorm", ctypes.c_void_p), ("qring", ctypes.c_void_p),
                 ("qstat", ctypes.c_void_p), ("step", ctypes.c_int32),
-                ("next_pos", ctypes.c_int32), ("ring_pmax", ctypes.c_int32 * MAX_WINDOW)]
+                ("next_pos", ctypes.c_int32), ("ring_pmax", ctypes.c_int32 * MAX_WINDOW),
+                ("sigma", ctypes.c_void_p)]
 
 
 class dc_policy(ctypes.Structure):
     _fields_ = [("n_in", ctypes.c_int32), ("n_hidden_layers", ctypes.c_int32),
-                ("hidden", ctypes.c_int32 * 2), ("params", ctypes.c_void_p)]
+                ("hidden", ctypes.c_int32 * 2), ("params", ctypes.c_void_p),
+                ("layer_norm", ctypes.c_int32)]
 
 
 class dc_gumbel(ctypes.Structure):

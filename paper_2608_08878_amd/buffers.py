@@ -21,7 +21,7 @@ class DecodeBuffers:
     """K/V cache and (optionally) feature state for `units` caches of `capacity` rows."""
 
     def __init__(self, batch, n_layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype="bf16",
-                 ent_window=64, scale=0.0, features=True, device="cuda"):
+                 ent_window=64, scale=0.0, features=True, device="cuda", sigma=False):
         self.G = n_q_heads // n_kv_heads
         self.U = batch * n_layers * n_kv_heads
         self.D = head_dim
@@ -47,6 +47,11 @@ class DecodeBuffers:
             self.feat = B.dc_feat(self.alpha.data_ptr(), self.num.data_ptr(), self.den.data_ptr(),
                                   self.pos.data_ptr(), self.vnorm.data_ptr(),
                                   self.qring.data_ptr(), self.qstat.data_ptr(), 0, 0)
+            self.sigma = None
+            if sigma:
+                # the fifth feature (needed by five-input policies)
+                self.sigma = torch.zeros((self.U, capacity), dtype=torch.float32, device=device)
+                self.feat.sigma = self.sigma.data_ptr()
         self.ws = None
         self.ws_bytes = 0
         if features:
@@ -78,6 +83,9 @@ class DecodeBuffers:
         if self.feat is not None:
             self.alpha, self.num, self.den = moved(self.alpha), moved(self.num), moved(self.den)
             self.pos, self.vnorm = moved(self.pos), moved(self.vnorm)
+            if self.sigma is not None:
+                self.sigma = moved(self.sigma)
+                self.feat.sigma = self.sigma.data_ptr()
             self.feat.alpha, self.feat.ent_num = self.alpha.data_ptr(), self.num.data_ptr()
             self.feat.ent_den, self.feat.pos = self.den.data_ptr(), self.pos.data_ptr()
             self.feat.vnorm = self.vnorm.data_ptr()
@@ -138,7 +146,7 @@ def subset_log_prob(scores: torch.Tensor, budget: int, tau: float = 1.0, kept=No
     return lz, lp
 
 
-def make_policy(params: torch.Tensor, hidden) -> B.dc_policy:
+def make_policy(params: torch.Tensor, hidden, n_in: int = 4, layer_norm: bool = False) -> B.dc_policy:
     hidden = tuple(hidden)
     h = (ctypes.c_int32 * 2)(hidden[0], hidden[1] if len(hidden) > 1 else 0)
-    return B.dc_policy(4, len(hidden), h, params.data_ptr())
+    return B.dc_policy(n_in, len(hidden), h, params.data_ptr(), int(layer_norm))

@@ -87,7 +87,9 @@ size_t dc_workspace_bytes(const dc_dims* dims, int32_t max_len, int32_t kl_rows,
   if (max_len > 0) {
     if (check_dims(dims) != DC_OK) return 0;
     const size_t a = split_bytes(dims, max_len), b = evict_bytes(dims, max_len);
+    const size_t x = align256(dc::evict_ext_ws_bytes((int)units_of(dims), max_len));
     need = a > b ? a : b;
+    need = x > need ? x : need;
   }
   if (kl_rows > 0 && kl_vocab > 0) {
     const size_t c = kl_bytes(kl_rows, kl_vocab);
@@ -113,6 +115,7 @@ dc_status dc_feat_init(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, int3
     a.den = feat->ent_den;
     a.pos = feat->pos;
     a.vnorm = feat->vnorm;
+    a.sigma = feat->sigma;
     a.cap = dims->capacity;
     a.units = (int)units_of(dims);
     a.L = kv->len;
@@ -215,6 +218,7 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
     a.den = feat->ent_den;
     a.pos = feat->pos;
     a.vnorm = feat->vnorm;
+    a.sigma = feat->sigma;
     a.qring = feat->qring;
     a.qstat = feat->qstat;
     a.T = feat->next_pos + append;
@@ -269,18 +273,25 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   if (!kv || !kv->k || !kv->v || !feat || !policy || !policy->params) return DC_ERR_NULL;
   if (!feat->alpha || !feat->ent_num || !feat->ent_den || !feat->pos || !feat->vnorm)
     return DC_ERR_NULL;
-  if (policy->n_in != 4 || (policy->n_hidden_layers != 1 && policy->n_hidden_layers != 2))
+  if ((policy->n_in != 4 && policy->n_in != 5) ||
+      (policy->n_hidden_layers != 1 && policy->n_hidden_layers != 2) ||
+      (policy->layer_norm != 0 && policy->layer_norm != 1))
     return DC_ERR_UNSUPPORTED;
   if (policy->hidden[0] < 1 || policy->hidden[0] > 128) return DC_ERR_UNSUPPORTED;
-  if (policy->n_hidden_layers == 2 &&
-      (policy->hidden[0] > 64 || policy->hidden[1] < 1 || policy->hidden[1] > 128))
+  if (policy->n_hidden_layers == 2 && (policy->hidden[1] < 1 || policy->hidden[1] > 128))
     return DC_ERR_UNSUPPORTED;
+  // outside the fixed fast paths: a fifth input, LayerNorm, or a wide first layer
+  // of a two-layer policy run through the out-of-line MLP
+  const int ext = policy->n_in == 5 || policy->layer_norm ||
+                  (policy->n_hidden_layers == 2 && policy->hidden[0] > 64);
+  if (policy->n_in == 5 && !feat->sigma) return DC_ERR_NULL;
   if (budget < 1) return DC_ERR_BUDGET;
   if (L < 1 || L > dims->capacity) return DC_ERR_SHAPE;
   if (L > dc::evict_max_len()) return DC_ERR_UNSUPPORTED;
   if (T < 1) return DC_ERR_SHAPE;
   const int evict = budget < L;
-  need = L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0;
+  need = ext ? align256(dc::evict_ext_ws_bytes((int)units_of(dims), L))
+             : (L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0);
   if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
   memset(&e, 0, sizeof(e));
   e.k = kv->k;
@@ -290,6 +301,7 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   e.den = feat->ent_den;
   e.pos = feat->pos;
   e.vnorm = feat->vnorm;
+  e.sigma = feat->sigma;
   e.params = policy->params;
   e.scores_out = scores_out;
   e.kept_out = kept_out;
@@ -301,6 +313,9 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   e.nh = policy->n_hidden_layers;
   e.h1 = policy->hidden[0];
   e.h2 = policy->n_hidden_layers == 2 ? policy->hidden[1] : 0;
+  e.n_in = policy->n_in;
+  e.ln = policy->layer_norm;
+  e.ext = ext;
   e.evict = evict;
   e.ws_keys = (uint64_t*)ws;
   return DC_OK;
@@ -432,7 +447,9 @@ dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   if (st != DC_OK) return st;
   const int G = group_of(dims), D = dims->head_dim;
   const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
-  const bool fused = dims->dtype == DC_BF16 && !split &&
+  // the single-launch step serves four-input policies without LayerNorm and
+  // does not produce sigma
+  const bool fused = dims->dtype == DC_BF16 && !split && !e.ext && !feat->sigma &&
                      dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
   if (fused) {
     if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;

@@ -256,12 +256,13 @@ __device__ __forceinline__ void phase_d(const DecodeArgs& a, int u, int r0, int 
   constexpr float invG = 1.0f / G;
   for (int i = r0 + threadIdx.x; i < r1; i += NTH) {
     const int si = i - sink0;
-    float s[G];
+    float w[G];
 #pragma unroll
-    for (int j = 0; j < G; ++j) s[j] = s_src[si * G + j];
+    for (int j = 0; j < G; ++j) w[j] = attn_weight(s_src[si * G + j], M[j], invl[j]);
     float cz, cn;
-    row_contrib<G>(s, M, invl, H, cz, cn);
+    contrib_from_weights<G>(w, H, cz, cn);
     const size_t gi = ub + i;
+    if (a.sigma) a.sigma[gi] = head_variance<G>(w);
     if (i == newrow) {
       a.alpha[gi] = cz * invG;
       a.den[gi] = (double)cz;
@@ -485,6 +486,7 @@ __global__ void __launch_bounds__(256) feat_init_kernel(DecodeArgs a, int first_
     if (lam == 0) {
       a.vnorm[gi] = __builtin_sqrtf(v2);
       a.alpha[gi] = 0.0f;
+      if (a.sigma) a.sigma[gi] = 0.0f;
       a.num[gi] = 0.0;
       a.den[gi] = 0.0;
       a.pos[gi] = first_pos + i;

@@ -122,6 +122,23 @@ __device__ __forceinline__ void row_contrib(const float* s, const float* m, cons
   contrib_from_weights<G>(a, H, cz, cn);
 }
 
+// sigma_i: variance over the G heads of the weights a row received this step,
+// (1/G) sum_j (a_j - mean)^2 (two passes: no cancellation; 0 for G = 1).
+template <int G>
+__device__ __forceinline__ float head_variance(const float* a) {
+  float m = a[0];
+#pragma unroll
+  for (int j = 1; j < G; ++j) m = m + a[j];
+  m = m * (1.0f / G);
+  float v = 0.0f;
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    const float d = a[j] - m;
+    v = __builtin_fmaf(d, d, v);
+  }
+  return v * (1.0f / G);
+}
+
 __device__ __forceinline__ uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ uint4 ldg16_nt(const void* p) {

@@ -92,6 +92,22 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
   }
 }
 
+// Extended policies: the same grid over rows, the out-of-line MLP per row.
+__global__ void __launch_bounds__(256) score_ext_kernel(EvictArgs a, uint64_t* keys, int kstride) {
+  const int u = blockIdx.y;
+  const size_t ub = (size_t)u * a.cap;
+  const float invT = 1.0f / (float)a.T;
+  for (int base = blockIdx.x * 256; base < a.L; base += gridDim.x * 256) {
+    const int r = base + threadIdx.x;
+    if (r < a.L) {
+      int32_t p;
+      const float sc = ext_score(a, ub + r, invT, p);
+      if (a.scores_out) a.scores_out[(size_t)u * a.L + r] = sc;
+      keys[(size_t)u * kstride + r] = row_key(a.sample ? sampled_score(a, sc, p, u) : sc, p);
+    }
+  }
+}
+
 // ... then one workgroup per unit selects and compacts.
 template <int DTYPE, int D>
 __global__ void __launch_bounds__(ENT) select_kernel(EvictArgs a, const uint64_t* keys, int kstride) {
@@ -119,12 +135,22 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
   b.mv_ints = (2 * (nmv > 0 ? nmv : 1) + 3) / 4 * 4;   // keeps the weights after it 16-byte aligned
   const size_t pbytes = a.nh == 2 ? (size_t)policy_floats(2, a.h1, a.h2) * sizeof(float) : 0;
   const size_t dyn = (size_t)b.mv_ints * sizeof(int);
-  if (a.L <= ENT * REG_KPT) {
+  const int kstride = (a.L + ENT - 1) / ENT * ENT;
+  if (a.ext) {
+    hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
+                       ws_keys, kstride);
+    if (a.evict) {
+      auto k = select_kernel<DTYPE, D>;
+      hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+      hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);
+    } else if (a.kept_out) {
+      hipLaunchKernelGGL(identity_kept_kernel, dim3(1024), dim3(256), 0, s, a.kept_out, a.units, a.L);
+    }
+  } else if (a.L <= ENT * REG_KPT) {
     auto k = a.nh == 2 ? score_select_kernel<DTYPE, D, 2> : score_select_kernel<DTYPE, D, 1>;
     hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)(dyn + pbytes));
     hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn + pbytes, s, b);
   } else {
-    const int kstride = (a.L + ENT - 1) / ENT * ENT;
     // two hidden layers: each workgroup stages the weights once and scores
     // several row blocks with them
     int gx = (a.L + 255) / 256;
@@ -153,6 +179,11 @@ int launch_evict(const EvictArgs& a, int dtype, int D, void* stream) {
   if (dtype == 0 && D == 128) return launch_evict_t<0, 128>(a, a.ws_keys, s);
   if (dtype == 0 && D == 64) return launch_evict_t<0, 64>(a, a.ws_keys, s);
   return (int)hipErrorInvalidValue;
+}
+
+size_t evict_ext_ws_bytes(int units, int L) {
+  const size_t kstride = (size_t)(L + ENT - 1) / ENT * ENT;
+  return (size_t)units * kstride * sizeof(uint64_t);
 }
 
 size_t evict_ws_bytes(int units, int L) {

@@ -20,6 +20,7 @@ struct DecodeArgs {
   float* vnorm;
   void* qring;          // [units][w][G][D]
   float* qstat;         // [units][w][G][3]
+  float* sigma;         // [units][cap] head variance of this step's weights, or null
   int64_t cap;
   int units;
   int len_old;          // valid rows before the append
@@ -50,6 +51,7 @@ struct EvictArgs {
   double* den;
   int32_t* pos;
   float* vnorm;
+  float* sigma;         // [units][cap] or null (moved with the rows; read by 5-input policies)
   const float* params;
   float* scores_out;
   int32_t* kept_out;
@@ -60,6 +62,9 @@ struct EvictArgs {
   int T;
   int nh;               // hidden layers (1 or 2)
   int h1, h2;
+  int n_in;             // 4 or 5 policy inputs
+  int ln;               // 1: LayerNorm in every hidden layer
+  int ext;              // 1: policy outside the fixed fast paths (n_in 5 or LayerNorm)
   int evict;            // 1 if rows are removed
   uint64_t* ws_keys;    // [units][kstride] row keys (long caches only)
   int mv_ints;          // ints of the compaction move list at the start of the dynamic LDS
@@ -121,6 +126,7 @@ size_t logz_ws_bytes(int units, int L, int B);
 int logz_band_entries();
 int evict_max_len();
 size_t evict_ws_bytes(int units, int L);
+size_t evict_ext_ws_bytes(int units, int L);
 int launch_kl(const KLArgs& a, void* stream);
 // bf16 matrix-core step (dc_step.hip); e != nullptr fuses scoring and eviction.
 int launch_step(const DecodeArgs& a, const EvictArgs* e, int D, int G, bool feat, bool chunked,

@@ -78,6 +78,113 @@ __device__ __forceinline__ const cfloat* const_params(const float* p) {
   return (const cfloat*)p;
 }
 
+// Extended policy (any of: a fifth input sigma_i, LayerNorm, widths up to 128
+// for two layers): x has n_in inputs in the paper's order, each hidden layer is
+// z = W h + b, [z = gain (z - mean) / sqrt(var + 1e-5) + bias over the layer],
+// h = relu(z); s = w_out . h + b_out.  Float32 with fixed evaluation order
+// (bias first, inputs / units in order); LayerNorm moments accumulated in
+// binary64.  The first hidden layer lives in registers (128 slots); the second
+// is evaluated one unit at a time, twice with LayerNorm (moments, then values).
+// Out of line: its 128-register hidden vector must not share the caller's
+// register budget.
+constexpr int EXT_HMAX = 128;
+constexpr float LN_EPS = 1e-5f;
+
+__device__ __attribute__((noinline)) float mlp_ext(const float* params, int n_in, int nh, int h1,
+                                                   int h2, int ln, float x0, float x1, float x2,
+                                                   float x3, float x4) {
+  const cfloat* W = const_params(params);
+  const cfloat* b = W + h1 * n_in;
+  const float xin[5] = {x0, x1, x2, x3, x4};
+  float h[EXT_HMAX];
+  double s1 = 0.0, s2 = 0.0;
+#pragma unroll
+  for (int i = 0; i < EXT_HMAX; ++i) {
+    float z = 0.0f;
+    if (i < h1) {
+      z = b[i];
+#pragma unroll
+      for (int k = 0; k < 5; ++k)
+        if (k < n_in) z = __builtin_fmaf(W[i * n_in + k], xin[k], z);
+      s1 += (double)z;
+      s2 += (double)z * (double)z;
+    }
+    h[i] = z;
+  }
+  const cfloat* next = b + h1;
+  if (ln) {
+    const cfloat* g = next;
+    const cfloat* be = next + h1;
+    next += 2 * h1;
+    const double mean = s1 / h1;
+    const double var = s2 / h1 - mean * mean;
+    const float m = (float)mean;
+    const float rs = (float)(1.0 / sqrt((var > 0.0 ? var : 0.0) + (double)LN_EPS));
+#pragma unroll
+    for (int i = 0; i < EXT_HMAX; ++i)
+      if (i < h1) h[i] = __builtin_fmaf((h[i] - m) * rs, g[i], be[i]);
+  }
+#pragma unroll
+  for (int i = 0; i < EXT_HMAX; ++i) h[i] = fmaxf(h[i], 0.0f);
+  if (nh == 1) {
+    const cfloat* wo = next;
+    float out = wo[h1];
+#pragma unroll
+    for (int i = 0; i < EXT_HMAX; ++i)
+      if (i < h1) out = __builtin_fmaf(wo[i], h[i], out);
+    return out;
+  }
+  const cfloat* W2 = next;
+  const cfloat* b2 = W2 + h2 * h1;
+  next = b2 + h2;
+  const cfloat* g2 = next;
+  const cfloat* be2 = next + h2;
+  if (ln) next += 2 * h2;
+  const cfloat* wo = next;
+  auto unit = [&](int o) {
+    const cfloat* w = W2 + o * h1;
+    float z = b2[o];
+#pragma unroll
+    for (int i = 0; i < EXT_HMAX; ++i)
+      if (i < h1) z = __builtin_fmaf(w[i], h[i], z);
+    return z;
+  };
+  float m2 = 0.0f, rs2 = 1.0f;
+  if (ln) {
+    double t1 = 0.0, t2 = 0.0;
+#pragma unroll 1
+    for (int o = 0; o < h2; ++o) {
+      const float z = unit(o);
+      t1 += (double)z;
+      t2 += (double)z * (double)z;
+    }
+    const double mean = t1 / h2;
+    const double var = t2 / h2 - mean * mean;
+    m2 = (float)mean;
+    rs2 = (float)(1.0 / sqrt((var > 0.0 ? var : 0.0) + (double)LN_EPS));
+  }
+  float out = wo[h2];
+#pragma unroll 1
+  for (int o = 0; o < h2; ++o) {
+    float z = unit(o);
+    if (ln) z = __builtin_fmaf((z - m2) * rs2, g2[o], be2[o]);
+    out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
+  }
+  return out;
+}
+
+// Score of row gi under the extended policy (features in the paper's order;
+// sigma only with five inputs).
+__device__ __forceinline__ float ext_score(const EvictArgs& a, size_t gi, float invT, int32_t& p) {
+  p = a.pos[gi];
+  const double num = a.num[gi], den = a.den[gi];
+  const float H = den > 0.0 ? (float)(num / den) : 0.0f;
+  const float al = a.alpha[gi], vn = a.vnorm[gi], ps = (float)p * invT;
+  if (a.n_in == 5)
+    return mlp_ext(a.params, 5, a.nh, a.h1, a.h2, a.ln, al, vn, a.sigma[gi], H, ps);
+  return mlp_ext(a.params, 4, a.nh, a.h1, a.h2, a.ln, al, vn, H, ps, 0.0f);
+}
+
 // Floats of the packed policy blob (W1, b1, [W2, b2,] w_out, b_out).
 __host__ __device__ inline int policy_floats(int nh, int h1, int h2) {
   return nh == 1 ? 4 * h1 + h1 + h1 + 1 : 4 * h1 + h1 + h2 * h1 + h2 + h2 + 1;
@@ -369,6 +476,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
         a.den[gd] = a.den[gs];
         a.pos[gd] = a.pos[gs];
         a.vnorm[gd] = a.vnorm[gs];
+        if (a.sigma) a.sigma[gd] = a.sigma[gs];
       }
     }
     return;
@@ -455,6 +563,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
       a.den[gd] = a.den[gs];
       a.pos[gd] = a.pos[gs];
       a.vnorm[gd] = a.vnorm[gs];
+      if (a.sigma) a.sigma[gd] = a.sigma[gs];
       if (a.kept_out) a.kept_out[(size_t)u * B + dst] = src;
     }
   }

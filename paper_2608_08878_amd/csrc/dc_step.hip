@@ -457,6 +457,7 @@ __device__ __forceinline__ void update_row(const DecodeArgs& a, size_t gi, bool 
   a.alpha[gi] = alpha;
   a.den[gi] = den;
   a.num[gi] = num;
+  if (a.sigma) a.sigma[gi] = head_variance<G>(w);
 }
 
 template <int D, int G>
@@ -506,8 +507,9 @@ struct RowStride {
   static constexpr int KS = RS / 2;            // u64 per row
 };
 
-template <int D, int G, bool FEAT, bool EVICT, int NH>
+template <int D, int G, bool FEAT, bool EVICT, int NH, bool SIG = false>
 __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_kernel(DecodeArgs a, EvictArgs e) {
+  static_assert(!SIG || (FEAT && !EVICT), "sigma is stored by the decode-only variant");
   constexpr int LPR = MG<D>::LPR;
   constexpr int RS = RowStride<G>::RS, KS = RowStride<G>::KS;
   extern __shared__ float lds[];
@@ -644,6 +646,7 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
         a.alpha[gi] = al;
         a.den[gi] = de;
         a.num[gi] = nu;
+        if constexpr (SIG) a.sigma[gi] = head_variance<G>(w);
       }
       if constexpr (EVICT) {
         float f[1][4], sc[1];
@@ -862,6 +865,7 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
     if (!feat) pick(step_unit_kernel<D, G, false, false, 1>);
     else if (e && e->nh == 2) pick(step_unit_kernel<D, G, true, true, 2>);
     else if (e) pick(step_unit_kernel<D, G, true, true, 1>);
+    else if (a.sigma) pick(step_unit_kernel<D, G, true, false, 1, true>);
     else pick(step_unit_kernel<D, G, true, false, 1>);
   } else {
     dim3 grid(a.nchunks, a.units);

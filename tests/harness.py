@@ -109,11 +109,11 @@ def rel_err_rows(got, ref) -> float:
     return float((np.abs(got - ref).max(axis=1) / den).max())
 
 
-def vec_ok(got, ref, tol=FP_TOL) -> tuple[bool, float]:
-    """|g - o| <= tol * max(|o|, 1e-3 max|o|) elementwise; returns (ok, worst ratio)."""
+def vec_ok(got, ref, tol=FP_TOL, floor_frac=1e-3) -> tuple[bool, float]:
+    """|g - o| <= tol * max(|o|, floor_frac max|o|) elementwise; returns (ok, worst ratio)."""
     got = np.asarray(got, np.float64)
     ref = np.asarray(ref, np.float64)
-    floor = 1e-3 * max(np.abs(ref).max(), 1e-30)
+    floor = floor_frac * max(np.abs(ref).max(), 1e-30)
     lim = tol * np.maximum(np.abs(ref), floor)
     ratio = np.abs(got - ref) / lim
     return bool(np.all(ratio <= 1.0)), float(ratio.max() if ratio.size else 0.0)

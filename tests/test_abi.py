@@ -99,10 +99,21 @@ def test_score_evict_rejects_bad_arguments():
 
     assert call(budget=0) == 5
     assert call(budget=-3) == 5
-    assert call(pol=B.dc_policy(5, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)) == 3
+    assert call(pol=B.dc_policy(6, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)) == 3
+    assert call(pol=B.dc_policy(3, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)) == 3
+    # five inputs need the sigma state
+    assert call(pol=B.dc_policy(5, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)) == 1
     assert call(pol=B.dc_policy(4, 3, (ctypes.c_int32 * 2)(32, 32), FAKE)) == 3
-    assert call(pol=B.dc_policy(4, 2, (ctypes.c_int32 * 2)(65, 32), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 2, (ctypes.c_int32 * 2)(129, 32), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 2, (ctypes.c_int32 * 2)(32, 129), FAKE)) == 3
+    assert call(pol=B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE, 2)) == 3
     assert call(pol=B.dc_policy(4, 1, (ctypes.c_int32 * 2)(0, 0), FAKE)) == 3
+    # extended policies (LayerNorm, five inputs, a 65..128-wide first of two layers)
+    # score through row keys in the workspace at every length
+    assert call(pol=B.dc_policy(4, 2, (ctypes.c_int32 * 2)(65, 32), FAKE)) == 6
+    assert call(pol=B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE, 1)) == 6
+    assert call(pol=B.dc_policy(5, 2, (ctypes.c_int32 * 2)(128, 128), FAKE, 1),
+                feat=_feat(sigma=FAKE)) == 6
     assert call(pol=B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), None)) == 1
     assert call(kv=B.dc_kv(FAKE, FAKE, 0)) == 2
     assert call(feat=_feat(vnorm=None)) == 1
