@@ -412,12 +412,13 @@ def bench_paper_policy(args, wl, dev, log):
             parts["step"].append(ev[0].elapsed_time(ev[2]))
     m = {k: float(np.mean(v)) for k, v in parts.items()}
     L = wl.budget + 1
-    flop_row = 2 * (n_in * hidden[0] + 2 * hidden[0] * hidden[1] + hidden[1])  # layer 2 twice (LayerNorm)
+    flop_row = 2 * (n_in * hidden[0] + hidden[0] * hidden[1] + hidden[1])
     return {"value": round(1e3 / m["step"], 3), "unit": "decode steps/s",
             "ms_per_step": round(m["step"], 4), "decode_ms": round(m["decode"], 4),
             "score_select_ms": round(m["score_select"], 4), "first_step_ms": round(first_ms, 3),
             "policy": "5->128->128->1 ReLU MLP with LayerNorm, features [alpha, |v|, sigma, H, pos]",
             "mlp_tflops": round(U * L * flop_row / (m["score_select"] * 1e-3) / 1e12, 2),
+            "mlp_frac_of_f32_mfma": round(U * L * flop_row / (m["score_select"] * 1e-3) / 157.3e12, 4),
             "note": "paper-faithful state and policy; decode + separate scoring pass, timed apart"}
 
 

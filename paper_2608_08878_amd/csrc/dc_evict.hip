@@ -16,6 +16,7 @@
 // below `budget` (holes, ascending) receive the kept rows from slots >= budget
 // (ascending).  Sources and destinations are disjoint, so the copies need no
 // ordering.
+#include "dc_mlp.hpp"
 #include "dc_select.hpp"
 
 #pragma clang fp contract(off)
@@ -137,8 +138,13 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
   const size_t dyn = (size_t)b.mv_ints * sizeof(int);
   const int kstride = (a.L + ENT - 1) / ENT * ENT;
   if (a.ext) {
-    hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
-                       ws_keys, kstride);
+    if (a.nh == 2) {
+      const int rc = launch_score_mlp2(b, ws_keys, kstride, s);
+      if (rc) return rc;
+    } else {
+      hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
+                         ws_keys, kstride);
+    }
     if (a.evict) {
       auto k = select_kernel<DTYPE, D>;
       hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);

@@ -1,0 +1,230 @@
+// Two-hidden-layer policy on matrix cores (Sec. 3.1.2 scoring with the App. D
+// network: n_in -> h1 -> h2 -> 1, optional LayerNorm, widths up to 128), gfx950.
+//
+// Scoring every cached row with a 128 x 128 hidden layer is a dense
+// contraction, [rows x h1] x [h1 x h2], so it runs on v_mfma_f32_16x16x4_f32
+// (float32 operands and accumulation: the same precision as the scalar path).
+// One wave takes 16 rows at a time:
+//   layer 1 (VALU): lane l computes, for row l % 16, the units k = 4 s + l / 16
+//     (s < 32) -- exactly the A operand MFMA step s needs from that lane --
+//     with LayerNorm moments reduced over the four lanes that share the row;
+//   layer 2 (MFMA): 8 column blocks x 32 k-steps; B comes from W2 staged in
+//     LDS as [k][n] with a row stride of 144 floats (the four k rows one
+//     instruction reads fall in different bank halves);
+//   the accumulators hold row 4 (l / 16) + i, column 16 cb + l % 16: LayerNorm
+//     moments, ReLU and the output dot product reduce over the 16 lanes of a
+//     DPP row.
+// Padded units (k >= h1, n >= h2) are exact zeros and are left out of the
+// LayerNorm moments.
+#include <hip/hip_runtime.h>
+
+#include "dc_mlp.hpp"
+#include "dc_select.hpp"
+
+#pragma clang fp contract(off)
+
+namespace dc {
+
+namespace {
+
+constexpr int MT = 256;              // 4 waves
+constexpr int HP = 128;              // padded hidden width
+constexpr int W2S = HP + 16;         // LDS row stride of W2 (floats)
+constexpr int NX = 5;                // padded input width
+typedef float f32x4_v __attribute__((ext_vector_type(4)));
+
+// LDS layout (floats)
+constexpr int O_W2 = 0;                        // [HP][W2S]  W2 as [k][n]
+constexpr int O_B2 = O_W2 + HP * W2S;          // b2, g2, be2, wo   [HP] each
+constexpr int O_W1 = O_B2 + 4 * HP;            // [HP][NX]
+constexpr int O_B1 = O_W1 + HP * NX;           // b1, g1, be1       [HP] each
+constexpr int LDS_FLOATS = O_B1 + 3 * HP;
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float sum16(float x) {    // over the 16 lanes of a DPP row
+  x += dpp_f<0xB1>(x);    // quad_perm [1,0,3,2]
+  x += dpp_f<0x4E>(x);    // quad_perm [2,3,0,1]
+  x += dpp_f<0x141>(x);   // row_half_mirror
+  x += dpp_f<0x140>(x);   // row_mirror
+  return x;
+}
+__device__ __forceinline__ float sum4rows(float x) {  // over lanes l, l^16, l^32, l^48
+  x += __shfl_xor(x, 16);
+  x += __shfl_xor(x, 32);
+  return x;
+}
+
+__device__ void stage(const EvictArgs& a, float* sm) {
+  const cfloat* P = const_params(a.params);
+  const int h1 = a.h1, h2 = a.h2, nin = a.n_in, ln = a.ln;
+  const cfloat* W1 = P;
+  const cfloat* b1 = W1 + h1 * nin;
+  const cfloat* g1 = b1 + h1;
+  const cfloat* be1 = g1 + h1;
+  const cfloat* W2 = b1 + h1 + (ln ? 2 * h1 : 0);
+  const cfloat* b2 = W2 + h2 * h1;
+  const cfloat* g2 = b2 + h2;
+  const cfloat* be2 = g2 + h2;
+  const cfloat* wo = b2 + h2 + (ln ? 2 * h2 : 0);
+  for (int i = threadIdx.x; i < HP * W2S; i += MT) {
+    const int k = i / W2S, n = i % W2S;
+    sm[O_W2 + i] = (k < h1 && n < h2) ? W2[n * h1 + k] : 0.0f;
+  }
+  for (int i = threadIdx.x; i < HP; i += MT) {
+    const bool v2 = i < h2, v1 = i < h1;
+    sm[O_B2 + i] = v2 ? b2[i] : 0.0f;
+    sm[O_B2 + HP + i] = v2 ? (ln ? g2[i] : 1.0f) : 0.0f;
+    sm[O_B2 + 2 * HP + i] = v2 && ln ? be2[i] : 0.0f;
+    sm[O_B2 + 3 * HP + i] = v2 ? wo[i] : 0.0f;
+    sm[O_B1 + i] = v1 ? b1[i] : 0.0f;
+    sm[O_B1 + HP + i] = v1 ? (ln ? g1[i] : 1.0f) : 0.0f;
+    sm[O_B1 + 2 * HP + i] = v1 && ln ? be1[i] : 0.0f;
+#pragma unroll
+    for (int x = 0; x < NX; ++x) sm[O_W1 + i * NX + x] = (v1 && x < nin) ? W1[i * nin + x] : 0.0f;
+  }
+}
+
+__global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
+  extern __shared__ float sm[];
+  stage(a, sm);
+  __syncthreads();
+  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ri = lane & 15, kg = lane >> 4;
+  const int h1 = a.h1, h2 = a.h2, ln = a.ln, L = a.L;
+  const float fh1 = (float)h1, fh2 = (float)h2;
+  const size_t ub = (size_t)u * a.cap;
+  const float invT = 1.0f / (float)a.T;
+  const float bout = const_params(a.params)[h1 * a.n_in + h1 + (ln ? 2 * h1 : 0) + h2 * h1 + h2 +
+                                            (ln ? 2 * h2 : 0) + h2];
+  for (int rb = (blockIdx.x * 4 + wave) * 16; rb < L; rb += gridDim.x * 64) {
+    // features of this lane's A row (the four lanes of a row load the same row)
+    const int r = rb + ri;
+    const size_t gi = ub + (r < L ? r : L - 1);
+    float x[NX];
+    {
+      const double num = a.num[gi], den = a.den[gi];
+      const float H = den > 0.0 ? (float)(num / den) : 0.0f;
+      const float ps = (float)a.pos[gi] * invT;
+      x[0] = a.alpha[gi];
+      x[1] = a.vnorm[gi];
+      if (a.n_in == 5) {
+        x[2] = a.sigma[gi];
+        x[3] = H;
+        x[4] = ps;
+      } else {
+        x[2] = H;
+        x[3] = ps;
+        x[4] = 0.0f;
+      }
+    }
+    // layer 1: units k = 4 s + kg (the weights are re-read from LDS per row
+    // block: held across blocks they would take 256 registers)
+    const float* p1 = sm;
+    asm volatile("" : "+v"(p1));
+    float h[32];
+    float s1 = 0.0f;
+#pragma unroll
+    for (int s = 0; s < 32; ++s) {
+      const int k = 4 * s + kg;
+      float z = p1[O_B1 + k];
+#pragma unroll
+      for (int i = 0; i < NX; ++i) z = __builtin_fmaf(p1[O_W1 + k * NX + i], x[i], z);
+      h[s] = z;
+      s1 += k < h1 ? z : 0.0f;
+    }
+    if (ln) {
+      const float mean = sum4rows(s1) / fh1;
+      float s2 = 0.0f;
+#pragma unroll
+      for (int s = 0; s < 32; ++s) {
+        const float d = h[s] - mean;
+        s2 += (4 * s + kg) < h1 ? d * d : 0.0f;
+      }
+      const float rs = 1.0f / __builtin_sqrtf(sum4rows(s2) / fh1 + LN_EPS);
+#pragma unroll
+      for (int s = 0; s < 32; ++s) {
+        const int k = 4 * s + kg;
+        h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + k], p1[O_B1 + 2 * HP + k]);
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 32; ++s) h[s] = (4 * s + kg) < h1 ? fmaxf(h[s], 0.0f) : 0.0f;
+    // layer 2 on MFMA
+    f32x4_v acc[8];
+#pragma unroll
+    for (int cb = 0; cb < 8; ++cb) acc[cb] = (f32x4_v){0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int s = 0; s < 32; ++s) {
+      const float* brow = sm + O_W2 + (4 * s + kg) * W2S + ri;
+      asm volatile("" : "+v"(brow));   // keeps each step's B reads in the step (no 256-value prefetch)
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb)
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[s], brow[16 * cb], acc[cb], 0, 0, 0);
+    }
+    // rows 4 kg + i of the block, columns 16 cb + ri
+    float score[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float z[8];
+      float t1 = 0.0f;
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) {
+        const int n = 16 * cb + ri;
+        z[cb] = acc[cb][i] + sm[O_B2 + n];
+        t1 += n < h2 ? z[cb] : 0.0f;
+      }
+      float mean = 0.0f, rs = 1.0f;
+      if (ln) {
+        mean = sum16(t1) / fh2;
+        float t2 = 0.0f;
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) {
+          const float d = z[cb] - mean;
+          t2 += (16 * cb + ri) < h2 ? d * d : 0.0f;
+        }
+        rs = 1.0f / __builtin_sqrtf(sum16(t2) / fh2 + LN_EPS);
+      }
+      float o = 0.0f;
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) {
+        const int n = 16 * cb + ri;
+        float y = ln ? __builtin_fmaf((z[cb] - mean) * rs, sm[O_B2 + HP + n], sm[O_B2 + 2 * HP + n])
+                     : z[cb];
+        o = __builtin_fmaf(sm[O_B2 + 3 * HP + n], fmaxf(y, 0.0f), o);   // padded units: wo = 0
+      }
+      score[i] = sum16(o) + bout;
+    }
+    // lanes ri < 4 of each row group write rows 4 kg + ri
+    if (ri < 4) {
+      const int row = rb + 4 * kg + ri;
+      float sc = score[0];
+#pragma unroll
+      for (int i = 1; i < 4; ++i) sc = ri == i ? score[i] : sc;
+      if (row < L) {
+        const int32_t p = a.pos[ub + row];
+        if (a.scores_out) a.scores_out[(size_t)u * L + row] = sc;
+        keys[(size_t)u * kstride + row] = row_key(a.sample ? sampled_score(a, sc, p, u) : sc, p);
+      }
+    }
+  }
+}
+
+}  // namespace
+
+size_t mlp2_lds_bytes() { return (size_t)LDS_FLOATS * sizeof(float); }
+
+int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* stream) {
+  const int nblk = (a.L + 63) / 64;
+  const int gx = nblk < 8 ? nblk : 8;
+  const size_t lds = mlp2_lds_bytes();
+  hipFuncSetAttribute((const void*)score_mlp2_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
+                      (int)lds);
+  hipLaunchKernelGGL(score_mlp2_kernel, dim3(gx, a.units), dim3(MT), lds, (hipStream_t)stream, a,
+                     keys, kstride);
+  return (int)hipGetLastError();
+}
+
+}  // namespace dc
