@@ -281,20 +281,17 @@ def bench_teacher_student_kl(args, wl, dev, log):
         sc_flat = torch.empty(U * (wl.n0 + 1), dtype=torch.float32, device=dev)
         kept = torch.empty((U, wl.budget), dtype=torch.int32, device=dev)
         logp = torch.empty(U, dtype=torch.float64, device=dev)
-        parts["sample"] = []
     for t in range(nsteps):
         sg.queries(wl, t, q)
         sg.new_rows(wl, t, kn, vn, U)
-        ev = _events(5)
+        ev = _events(4)
         ev[0].record()
         tea.decode_step(q, kn, vn, o_t, features=False)
         ev[1].record()
         if train:
-            stu.decode_step(q, kn, vn, o_s)
-            ev[4].record()
-            L = stu.kv.len
-            stu.sample_evict(pol, wl.budget, B.make_gumbel(1.0, wl.seed, t),
-                             sc_flat[:U * L].view(U, L), kept, logp)
+            L = stu.kv.len + 1
+            stu.decode_sample_evict(pol, wl.budget, B.make_gumbel(1.0, wl.seed, t), q, kn, vn,
+                                    o_s, sc_flat[:U * L].view(U, L), kept, logp)
         else:
             stu.decode_evict(pol, wl.budget, q, kn, vn, o_s)
         ev[2].record()
@@ -310,8 +307,6 @@ def bench_teacher_student_kl(args, wl, dev, log):
             parts["student"].append(ev[1].elapsed_time(ev[2]))
             parts["kl"].append(ev[2].elapsed_time(ev[3]))
             parts["step"].append(ev[0].elapsed_time(ev[3]))
-            if train:
-                parts["sample"].append(ev[4].elapsed_time(ev[2]))
     m = {k: float(np.mean(v)) for k, v in parts.items()}
     extra = {}
     # the same rewards deferred to the end of the rollout: one call over all
@@ -336,8 +331,8 @@ def bench_teacher_student_kl(args, wl, dev, log):
     log(f"deferred KL over {Td} steps x {rows} rows: {kd_ms:.3f} ms "
         f"({kd_ms / Td:.4f} ms per step vs {m['kl']:.4f} per-step calls)")
     if train:
-        extra = {"student_select": "gumbel top-B + log pi (training mode)",
-                 "sample_evict_ms": round(m["sample"], 4)}
+        extra.update({"student_select": "gumbel top-B + log pi (training mode, one fused "
+                                        "launch + the log-partition)"})
         extra.update(time_log_partition(wl, U, dev, log))
     Lt = wl.n0 + 1 + args.warmup + args.steps / 2.0
     kvb = U * (Lt + wl.budget + 1) * 2 * D * 2 + voc * hid * 2

@@ -236,6 +236,20 @@ dc_status dc_sample_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const d
                           int32_t *kept_out, double *logp_out, void *ws, size_t ws_bytes,
                           void *hip_stream);
 
+/* One whole training-mode decode step: dc_decode_step followed by
+ * dc_sample_evict with the same policy, budget, noise and outputs, with results
+ * and host bookkeeping bit-identical to the two calls in sequence.  Where the
+ * cache fits on chip (bf16, G >= 4, a four-input policy without LayerNorm) it
+ * runs as one launch that streams K/V once, draws the noise, selects and
+ * compacts, followed by the log-partition when logp_out is requested.
+ * Errors: those of dc_decode_step and dc_sample_evict; nothing is enqueued
+ * unless both validate. */
+dc_status dc_decode_sample_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat,
+                                 const dc_policy *policy, int32_t budget, const dc_gumbel *gumbel,
+                                 const void *q, const void *k_new, const void *v_new, void *out,
+                                 float *scores_out, int32_t *kept_out, double *logp_out, void *ws,
+                                 size_t ws_bytes, void *hip_stream);
+
 /* Exact log-partition function of the size-B subset law and the
  * log-probability of kept sets (App. C), for `units` independent score rows:
  *   logz_out[u] = log Z = log sum over size-budget subsets a of exp(sum_{i in a} s[u][i] / tau)

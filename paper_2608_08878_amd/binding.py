@@ -59,7 +59,7 @@ class dc_reinforce_cfg(ctypes.Structure):
 KL_MAX_ROWS = 16384
 
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
-           "dc_decode_evict", "dc_sample_evict", "dc_subset_log_prob",
+           "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_subset_log_prob",
            "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_reinforce_terms",
            "dc_dynamic_budget", "dc_status_str")
 
@@ -95,6 +95,11 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
                                       ctypes.POINTER(dc_gumbel), vp, vp, vp, vp, sz, vp]
         L.dc_sample_evict.restype = ctypes.c_int
+        L.dc_decode_sample_evict.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                             ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), i32,
+                                             ctypes.POINTER(dc_gumbel), vp, vp, vp, vp, vp, vp, vp,
+                                             vp, sz, vp]
+        L.dc_decode_sample_evict.restype = ctypes.c_int
         L.dc_subset_log_prob.argtypes = [i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
         L.dc_subset_log_prob.restype = ctypes.c_int
         L.dc_subset_log_prob_workspace_bytes.argtypes = [i32, i32, i32]
@@ -202,3 +207,12 @@ def dc_reinforce_terms(steps: int, rollouts: int, cfg, rewards, logp, ema, retur
 
 def dc_dynamic_budget(ratio: float, seq_len: int, b_min: int = 32) -> int:
     return int(lib().dc_dynamic_budget(ratio, seq_len, b_min))
+
+
+def dc_decode_sample_evict(dims, kv, feat, policy, budget: int, gumbel, q, k_new, v_new, out,
+                           scores_out=None, kept_out=None, logp_out=None, ws=None,
+                           ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_decode_sample_evict(ctypes.byref(dims), ctypes.byref(kv), _ref(feat),
+                                        _ref(policy), budget, _ref(gumbel), _ptr(q), _ptr(k_new),
+                                        _ptr(v_new), _ptr(out), _ptr(scores_out), _ptr(kept_out),
+                                        _ptr(logp_out), _ptr(ws), ws_bytes, stream))

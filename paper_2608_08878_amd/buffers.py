@@ -125,6 +125,15 @@ class DecodeBuffers:
                          self.ws, self.ws_bytes, stream_handle(stream))
 
 
+    def decode_sample_evict(self, policy, budget, gumbel, q, k_new=None, v_new=None, out=None,
+                            scores_out=None, kept_out=None, logp_out=None, stream=None):
+        if out is None:
+            out = torch.empty_like(q)
+        B.dc_decode_sample_evict(self.dims, self.kv, self.feat, policy, budget, gumbel, q, k_new,
+                                 v_new, out, scores_out, kept_out, logp_out, self.ws, self.ws_bytes,
+                                 stream_handle(stream))
+        return out
+
     def sample_evict(self, policy, budget, gumbel, scores_out=None, kept_out=None, logp_out=None,
                      stream=None):
         B.dc_sample_evict(self.dims, self.kv, self.feat, policy, budget, gumbel, scores_out,

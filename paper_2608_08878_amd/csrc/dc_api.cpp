@@ -414,6 +414,51 @@ dc_status dc_sample_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   return DC_OK;
 }
 
+dc_status dc_decode_sample_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat,
+                                 const dc_policy* policy, int32_t budget, const dc_gumbel* gumbel,
+                                 const void* q, const void* k_new, const void* v_new, void* out,
+                                 float* scores_out, int32_t* kept_out, double* logp_out, void* ws,
+                                 size_t ws_bytes, void* hip_stream) {
+  if (!feat || !gumbel) return DC_ERR_NULL;
+  if (logp_out && (!scores_out || !kept_out)) return DC_ERR_NULL;
+  dc::DecodeArgs a;
+  bool split = false;
+  size_t need_d = 0, need_e = 0;
+  dc_status st = prep_decode(dims, kv, feat, q, k_new, v_new, out, ws, ws_bytes, a, split, need_d);
+  if (st != DC_OK) return st;
+  dc::EvictArgs e;
+  st = prep_evict(dims, kv, feat, policy, budget, scores_out, kept_out, ws, ws_bytes, a.L, a.T, e,
+                  need_e);
+  if (st != DC_OK) return st;
+  if (!(gumbel->tau > 0.0f) || isinf(gumbel->tau)) return DC_ERR_VALUE;
+  e.sample = 1;
+  e.tau = gumbel->tau;
+  e.seed0 = gumbel->seed[0];
+  e.seed1 = gumbel->seed[1];
+  e.draw = gumbel->draw;
+  dc::LogzArgs z;
+  if (logp_out) {
+    st = prep_logz(e.units, a.L, budget, gumbel->tau, scores_out, kept_out, nullptr, logp_out, ws,
+                   ws_bytes, z);
+    if (st != DC_OK) return st;
+  }
+  const int G = group_of(dims), D = dims->head_dim;
+  const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
+  const bool fused = dims->dtype == DC_BF16 && !split && !e.ext && !feat->sigma && G >= 4 &&
+                     dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
+  if (fused) {
+    if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
+  } else {
+    st = launch_decode_any(dims, a, true, split, hip_stream);
+    if (st != DC_OK) return st;
+    if (dc::launch_evict(e, dims->dtype, D, hip_stream) != 0) return DC_ERR_HIP;
+  }
+  if (logp_out && dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  commit_decode(kv, feat, a, dims->ent_window);
+  kv->len = e.budget;
+  return DC_OK;
+}
+
 dc_status dc_subset_log_prob(int32_t units, int32_t len, int32_t budget, float tau,
                              const float* scores, const int32_t* kept, double* logz_out,
                              double* logp_out, void* ws, size_t ws_bytes, void* hip_stream) {

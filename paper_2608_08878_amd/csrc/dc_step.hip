@@ -507,9 +507,12 @@ struct RowStride {
   static constexpr int KS = RS / 2;            // u64 per row
 };
 
-template <int D, int G, bool FEAT, bool EVICT, int NH, bool SIG = false>
+// SMP: training-mode ranking by the Gumbel-perturbed score; the unperturbed
+// score is kept in the row's LDS slot beside its key (needs RS >= 4, G >= 4).
+template <int D, int G, bool FEAT, bool EVICT, int NH, bool SIG = false, bool SMP = false>
 __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_kernel(DecodeArgs a, EvictArgs e) {
   static_assert(!SIG || (FEAT && !EVICT), "sigma is stored by the decode-only variant");
+  static_assert(!SMP || (EVICT && RowStride<G>::RS >= 4), "sampling keeps the score beside the key");
   constexpr int LPR = MG<D>::LPR;
   constexpr int RS = RowStride<G>::RS, KS = RowStride<G>::KS;
   extern __shared__ float lds[];
@@ -652,7 +655,15 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
         float f[1][4], sc[1];
         make_features(al, vn, nu, de, ps, invT, f[0]);
         policy_scores<1, NH>(e, f, sc, 1, pl);
-        if (!guard || valid) keys[(size_t)r * KS] = row_key(sc[0], ps);
+        if constexpr (SMP) {
+          const float ks = sampled_score(e, sc[0], ps, u);
+          if (!guard || valid) {
+            keys[(size_t)r * KS] = row_key(ks, ps);
+            sbuf[(size_t)r * RS + 2] = sc[0];
+          }
+        } else {
+          if (!guard || valid) keys[(size_t)r * KS] = row_key(sc[0], ps);
+        }
       }
     };
     if (ngw > 0) {
@@ -674,11 +685,16 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
     if constexpr (EVICT) {
       __syncthreads();
       if (e.scores_out) {
-        // the scores, recovered from the ranking keys (-0 reads back as +0)
+        // the scores: beside the keys when sampling, else recovered from the
+        // ranking keys (-0 reads back as +0)
         for (int r = tid; r < L; r += SNT) {
-          const uint32_t k = (uint32_t)(keys[(size_t)r * KS] >> 32);
-          const uint32_t bits = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
-          e.scores_out[(size_t)u * L + r] = __uint_as_float(bits);
+          if constexpr (SMP) {
+            e.scores_out[(size_t)u * L + r] = sbuf[(size_t)r * RS + 2];
+          } else {
+            const uint32_t k = (uint32_t)(keys[(size_t)r * KS] >> 32);
+            const uint32_t bits = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
+            e.scores_out[(size_t)u * L + r] = __uint_as_float(bits);
+          }
         }
       }
       if (e.evict) {
@@ -863,6 +879,14 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
       hipLaunchKernelGGL(kern, dim3(a.units), dim3(SNT), lds, s, a, ee);
     };
     if (!feat) pick(step_unit_kernel<D, G, false, false, 1>);
+    else if (e && e->sample) {
+      if constexpr (RowStride<G>::RS >= 4) {
+        if (e->nh == 2) pick(step_unit_kernel<D, G, true, true, 2, false, true>);
+        else pick(step_unit_kernel<D, G, true, true, 1, false, true>);
+      } else {
+        return (int)hipErrorInvalidValue;     // the caller takes the separate path
+      }
+    }
     else if (e && e->nh == 2) pick(step_unit_kernel<D, G, true, true, 2>);
     else if (e) pick(step_unit_kernel<D, G, true, true, 1>);
     else if (a.sigma) pick(step_unit_kernel<D, G, true, false, 1, true>);

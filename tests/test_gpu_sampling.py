@@ -281,3 +281,62 @@ def test_vanishing_temperature_reproduces_deterministic_selection():
         torch.cuda.synchronize()
         out.append(H.to_np(kept).copy())
     assert np.array_equal(out[0], out[1])
+
+
+def _sampled_run(wl, n0, budget, tau, seed, draws, fused):
+    U = wl.units
+    buf = _buffers(wl)
+    buf.reserve_workspace(wl.capacity)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(n0, 0)
+    _, pol = _policy(wl)
+    q, kn, vn = _step_tensors(wl)
+    snaps = []
+    for t, draw in enumerate(draws):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        L = buf.kv.len + 1
+        scores = torch.empty((U, L), dtype=torch.float32, device="cuda")
+        kept = torch.empty((U, min(budget, L)), dtype=torch.int32, device="cuda")
+        logp = torch.empty(U, dtype=torch.float64, device="cuda")
+        g = B.make_gumbel(tau, seed, draw)
+        if fused:
+            out = buf.decode_sample_evict(pol, budget, g, q, kn, vn, None, scores, kept, logp)
+        else:
+            out = buf.decode_step(q, kn, vn)
+            buf.sample_evict(pol, budget, g, scores, kept, logp)
+        torch.cuda.synchronize()
+        snaps.append({"out": H.to_np(out).copy(), "scores": H.to_np(scores).copy(),
+                      "kept": H.to_np(kept).copy(), "logp": logp.cpu().numpy().copy(),
+                      "state": [H.download_unit(buf, u) for u in range(U)]})
+    return snaps
+
+
+@pytest.mark.parametrize("cid,n0,budget", [(5, 2048, 2048), (5, 3000, 900), (4, 3340, 3277)])
+def test_fused_sampled_step_equals_decode_then_sample(cid, n0, budget):
+    """dc_decode_sample_evict (one launch where the cache fits) against
+    dc_decode_step + dc_sample_evict: every output bit and the post-step state,
+    over three steps with a new draw each; the fused kept set against the
+    oracle's sampled selection at the first step."""
+    wl = W.WORKLOADS[cid].scaled(batch=1, n_layers=1, n_kv_heads=2, n_q_heads=8, n0=n0,
+                                 budget=budget, steps=3)
+    print(f"fused sampled workload {cid} n0={n0} B={budget}", flush=True)
+    a = _sampled_run(wl, n0, budget, 0.9, 4242, (7, 8, 9), True)
+    b = _sampled_run(wl, n0, budget, 0.9, 4242, (7, 8, 9), False)
+    for t, (x, y) in enumerate(zip(a, b)):
+        for name in ("out", "scores", "kept", "logp"):
+            assert np.array_equal(x[name], y[name]), (t, name)
+        for u, (su, tu) in enumerate(zip(x["state"], y["state"])):
+            for name in su:
+                assert np.array_equal(su[name], tu[name]), (t, u, name)
+    params, _ = _policy(wl)
+    pnp = H.to_np(params)
+    for u in range(wl.units):
+        st = H.oracle_student(wl, u, n0=n0)
+        ounit.decode_step(st, *H.step_inputs_np(wl, 0, u))
+        s_or = ounit.scores(st, pnp, wl.hidden)
+        ok, worst = H.vec_ok(a[0]["scores"][u], s_or)
+        assert ok, (u, worst)
+        ok, _, amb, flips = _sampled_check(s_or, st.pos, a[0]["state"][u]["pos"], budget, 0.9, 4242,
+                                           u, 7)
+        assert ok, (u, amb, flips)
