@@ -28,6 +28,9 @@ namespace dc {
 constexpr int KL_WAVES = 4;
 constexpr int KL_TILE = 16 * KL_WAVES;   // vocabulary columns per workgroup
 constexpr int KL_KSTEP = 128;            // hidden elements per main-loop iteration
+constexpr int KL_PH = 2048;              // hidden elements of the 16 A rows staged in LDS at a time
+constexpr int KL_AROW = KL_PH * 2 + 16;  // LDS bytes per staged row (16-byte pad: the 16 rows of one
+                                         // 16-lane read group fall in different banks)
 
 // g(y) = e^y - 1 - y without cancellation.
 __device__ __forceinline__ float gfun(float y) {
@@ -77,41 +80,56 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   const int n0 = tile * KL_TILE + wave * 16;      // this wave's 16 columns
   const int i = lane & 15, kg = lane >> 4;        // MFMA row/col index, k group
   // A row i: rows 0..7 full, 8..15 compressed, of kl rows rb*8 + (i & 7)
-  const int krow = rb * 8 + (i & 7);
-  const bool avalid = krow < a.rows;
-  const char* arow = (const char*)(i < 8 ? a.h_full : a.h_comp) + (size_t)(avalid ? krow : 0) * a.hidden * 2;
   const char* brow = (const char*)a.w + (size_t)(n0 + i) * a.hidden * 2;
   f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
   // Hidden elements go in blocks of 128; MFMA t of a block takes 16-byte chunk
   // 4t + kg (both operands use the same map, which the dot product does not
-  // see), so each load instruction reads 64 contiguous bytes of 16 rows.  Two
-  // blocks are in flight per wave; every load is unconditional (a block past
-  // the end re-reads the last one, and rows past `rows` are zeroed after the
-  // load), so a wait covers only the block it consumes.
-  const int nblk = a.hidden / KL_KSTEP;
-  auto load = [&](int blk, uint4 (&av)[4], uint4 (&bv)[4]) {
-    const int off = (blk < nblk ? blk : nblk - 1) * KL_KSTEP * 2;
+  // see), so each lm-head load instruction reads 64 contiguous bytes of 16
+  // rows.  The 16 A rows (8 full, 8 compressed hidden states of this row block)
+  // are shared by the 4 waves: they are staged in LDS 2048 elements at a time
+  // (one read from L2 per workgroup instead of one per wave) and each wave
+  // reads its fragments there.  Two lm-head blocks are in flight per wave;
+  // every load is unconditional (a block past the phase re-reads its last one),
+  // so a wait covers only the block it consumes.
+  extern __shared__ __attribute__((aligned(16))) char alds[];
+  const char* arow_lds = alds + i * KL_AROW;
+  auto mma = [&](int lblk, const uint4 (&bv)[4]) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const uint4 x = ldg16(arow + off + 16 * (4 * t + kg));
-      av[t] = avalid ? x : make_uint4(0, 0, 0, 0);
-      bv[t] = ldg16(brow + off + 16 * (4 * t + kg));
+      const uint4 av = *reinterpret_cast<const uint4*>(arow_lds + (lblk * 16 + 4 * t + kg) * 16);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
+                                                    __builtin_bit_cast(bf16x8_t, bv[t]), acc, 0, 0, 0);
     }
   };
-  auto mma = [&](const uint4 (&av)[4], const uint4 (&bv)[4]) {
+  for (int k0 = 0; k0 < a.hidden; k0 += KL_PH) {
+    const int kn = a.hidden - k0 < KL_PH ? a.hidden - k0 : KL_PH;
+    const int nb = kn / KL_KSTEP;
+    auto load = [&](int lb, uint4 (&bv)[4]) {
+      const int off = (k0 + (lb < nb ? lb : nb - 1) * KL_KSTEP) * 2;
 #pragma unroll
-    for (int t = 0; t < 4; ++t)
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av[t]),
-                                                    __builtin_bit_cast(bf16x8_t, bv[t]), acc, 0, 0, 0);
-  };
-  uint4 a0[4], b0[4], a1[4], b1[4];
-  load(0, a0, b0);
-  load(1, a1, b1);
-  for (int blk = 0; blk < nblk; blk += 2) {
-    mma(a0, b0);
-    load(blk + 2, a0, b0);
-    if (blk + 1 < nblk) mma(a1, b1);
-    load(blk + 3, a1, b1);
+      for (int t = 0; t < 4; ++t) bv[t] = ldg16(brow + off + 16 * (4 * t + kg));
+    };
+    uint4 b0[4], b1[4];
+    load(0, b0);
+    load(1, b1);
+    // stage A[16][k0 .. k0 + kn) (rows past `rows` as zeros)
+    __syncthreads();                      // the previous phase's readers are done
+    const int cpr = kn / 8;               // 16-byte chunks per row
+    for (int c = threadIdx.x; c < 16 * cpr; c += 64 * KL_WAVES) {
+      const int r = c / cpr, ch = c - r * cpr;
+      const int kr = rb * 8 + (r & 7);
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (kr < a.rows)
+        x = ldg16((const char*)(r < 8 ? a.h_full : a.h_comp) + ((size_t)kr * a.hidden + k0 + ch * 8) * 2);
+      *reinterpret_cast<uint4*>(alds + r * KL_AROW + ch * 16) = x;
+    }
+    __syncthreads();
+    for (int lb = 0; lb < nb; lb += 2) {
+      mma(lb, b0);
+      load(lb + 2, b0);
+      if (lb + 1 < nb) mma(lb + 1, b1);
+      load(lb + 3, b1);
+    }
   }
   // lane holds C[4*kg + r][i] for r < 4: kg 0,1 full rows 0..7, kg 2,3 compressed rows 0..7
   float lf[4], lc[4];
@@ -247,7 +265,9 @@ int launch_kl(const KLArgs& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   const int nrb = (a.rows + 7) / 8;
   const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
-  hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), 0, s, a);
+  const int lds = 16 * KL_AROW;
+  hipFuncSetAttribute((const void*)kl_tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), lds, s, a);
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();
 }
