@@ -79,7 +79,15 @@ typedef struct {
  * order: eviction fills holes (see dc_score_evict). */
 typedef struct {
   void *k, *v;         /* [units][capacity][head_dim], dtype */
-  int32_t len;         /* host: valid rows per unit (identical for all units) */
+  int32_t len;         /* host: valid rows per unit (identical for all units); with unit_len,
+                          an upper bound of every unit's rows */
+  int32_t *unit_len;   /* device [units] or NULL.  When present the cache is ragged: unit u
+                          holds unit_len[u] rows (1 <= unit_len[u] <= len; kernels clamp
+                          to that range).  Every entry point keeps it current (+1 per
+                          append, min(rows, budget) per eviction) on the stream, and len
+                          as the bound.  Ragged caches need bf16 and run the chunked
+                          decode kernels and the row-key selection (no single-launch
+                          step), with dc_workspace_bytes scratch. */
 } dc_kv;
 
 /* Per-token feature state of the student cache (Sec. 3.1.1, state space).
@@ -235,6 +243,28 @@ dc_status dc_sample_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const d
                           int32_t budget, const dc_gumbel *gumbel, float *scores_out,
                           int32_t *kept_out, double *logp_out, void *ws, size_t ws_bytes,
                           void *hip_stream);
+
+/* Per-unit budgets (the appendix's head-level hybrid gives a subset of heads
+ * their full cache and the policy's budget to the rest; Table "head-level
+ * hybrid").  As dc_score_evict / dc_sample_evict with unit u
+ * keeping the top budgets[u] of its rows:
+ *   budgets     device [units]; each clamped to [1, max_budget]
+ *   max_budget  host: the largest budget (>= 1)
+ *   gumbel      NULL for the deterministic selection, else the training-mode
+ *               ranking (and logp_out may be requested)
+ *   scores_out  [units][kv->len] (rows past a unit's length untouched)
+ *   kept_out    [units][min(max_budget, kv->len)]: pre-eviction slots of the
+ *               rows that end in each slot, -1 past the unit's kept count
+ *   logp_out    [units] log pi of each unit's kept set under its own budget
+ * kv->unit_len is required (the units' lengths diverge); afterwards unit_len[u]
+ * = min(rows, budget) and kv->len = min(kv->len, max_budget).  A unit whose
+ * budget covers its rows keeps them all in place.
+ * Errors: those of dc_score_evict; DC_ERR_NULL (budgets, kv->unit_len, logp_out
+ * without gumbel, scores_out or kept_out), DC_ERR_BUDGET (max_budget < 1). */
+dc_status dc_score_evict_units(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const dc_policy *policy,
+                               const int32_t *budgets, int32_t max_budget, const dc_gumbel *gumbel,
+                               float *scores_out, int32_t *kept_out, double *logp_out, void *ws,
+                               size_t ws_bytes, void *hip_stream);
 
 /* One whole training-mode decode step: dc_decode_step followed by
  * dc_sample_evict with the same policy, budget, noise and outputs, with results

@@ -25,7 +25,8 @@ class dc_dims(ctypes.Structure):
 
 
 class dc_kv(ctypes.Structure):
-    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("len", ctypes.c_int32)]
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p), ("len", ctypes.c_int32),
+                ("unit_len", ctypes.c_void_p)]
 
 
 class dc_feat(ctypes.Structure):
@@ -59,7 +60,8 @@ class dc_reinforce_cfg(ctypes.Structure):
 KL_MAX_ROWS = 16384
 
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
-           "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_subset_log_prob",
+           "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_score_evict_units",
+           "dc_subset_log_prob",
            "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_reinforce_terms",
            "dc_dynamic_budget", "dc_status_str")
 
@@ -100,6 +102,10 @@ def lib() -> ctypes.CDLL:
                                              ctypes.POINTER(dc_gumbel), vp, vp, vp, vp, vp, vp, vp,
                                              vp, sz, vp]
         L.dc_decode_sample_evict.restype = ctypes.c_int
+        L.dc_score_evict_units.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                           ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), vp,
+                                           i32, ctypes.POINTER(dc_gumbel), vp, vp, vp, vp, sz, vp]
+        L.dc_score_evict_units.restype = ctypes.c_int
         L.dc_subset_log_prob.argtypes = [i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
         L.dc_subset_log_prob.restype = ctypes.c_int
         L.dc_subset_log_prob_workspace_bytes.argtypes = [i32, i32, i32]
@@ -216,3 +222,11 @@ def dc_decode_sample_evict(dims, kv, feat, policy, budget: int, gumbel, q, k_new
                                         _ref(policy), budget, _ref(gumbel), _ptr(q), _ptr(k_new),
                                         _ptr(v_new), _ptr(out), _ptr(scores_out), _ptr(kept_out),
                                         _ptr(logp_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_score_evict_units(dims, kv, feat, policy, budgets, max_budget: int, gumbel=None,
+                         scores_out=None, kept_out=None, logp_out=None, ws=None, ws_bytes: int = 0,
+                         stream=None) -> None:
+    _check(lib().dc_score_evict_units(ctypes.byref(dims), ctypes.byref(kv), _ref(feat), _ref(policy),
+                                      _ptr(budgets), max_budget, _ref(gumbel), _ptr(scores_out),
+                                      _ptr(kept_out), _ptr(logp_out), _ptr(ws), ws_bytes, stream))

@@ -21,7 +21,8 @@ class DecodeBuffers:
     """K/V cache and (optionally) feature state for `units` caches of `capacity` rows."""
 
     def __init__(self, batch, n_layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype="bf16",
-                 ent_window=64, scale=0.0, features=True, device="cuda", sigma=False):
+                 ent_window=64, scale=0.0, features=True, device="cuda", sigma=False,
+                 ragged=False):
         self.G = n_q_heads // n_kv_heads
         self.U = batch * n_layers * n_kv_heads
         self.D = head_dim
@@ -34,6 +35,11 @@ class DecodeBuffers:
         self.k = torch.zeros((self.U, capacity, head_dim), dtype=td, device=device)
         self.v = torch.zeros((self.U, capacity, head_dim), dtype=td, device=device)
         self.kv = B.dc_kv(self.k.data_ptr(), self.v.data_ptr(), 0)
+        self.unit_len = None
+        if ragged:
+            # per-unit lengths on the device (units may keep different row counts)
+            self.unit_len = torch.zeros(self.U, dtype=torch.int32, device=device)
+            self.kv.unit_len = self.unit_len.data_ptr()
         self.feat = None
         if features:
             self.alpha = torch.zeros((self.U, capacity), dtype=torch.float32, device=device)
@@ -103,6 +109,8 @@ class DecodeBuffers:
 
     def feat_init(self, length: int, first_pos: int = 0, stream=None):
         self.kv.len = length
+        if self.unit_len is not None:
+            self.unit_len.fill_(length)
         B.dc_feat_init(self.dims, self.kv, self.feat, first_pos, stream_handle(stream))
 
     def decode_step(self, q, k_new=None, v_new=None, out=None, stream=None, features=True):
@@ -133,6 +141,12 @@ class DecodeBuffers:
                                  v_new, out, scores_out, kept_out, logp_out, self.ws, self.ws_bytes,
                                  stream_handle(stream))
         return out
+
+    def score_evict_units(self, policy, budgets, max_budget, gumbel=None, scores_out=None,
+                          kept_out=None, logp_out=None, stream=None):
+        B.dc_score_evict_units(self.dims, self.kv, self.feat, policy, budgets, max_budget, gumbel,
+                               scores_out, kept_out, logp_out, self.ws, self.ws_bytes,
+                               stream_handle(stream))
 
     def sample_evict(self, policy, budget, gumbel, scores_out=None, kept_out=None, logp_out=None,
                      stream=None):

@@ -10,6 +10,7 @@
 namespace {
 
 constexpr int EVICT_REG_ROWS = 8192;
+constexpr int MAX_MOVES = 16384;   // rows one compaction may move (its move list is in LDS)
 
 int64_t units_of(const dc_dims* d) { return (int64_t)d->batch * d->n_layers * d->n_kv_heads; }
 int group_of(const dc_dims* d) { return d->n_q_heads / d->n_kv_heads; }
@@ -189,8 +190,11 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   const int L = len + append;
   const int G = group_of(dims), D = dims->head_dim;
   const int U = (int)units_of(dims);
+  const bool ragged = kv->unit_len != nullptr;
+  if (ragged && dims->dtype != DC_BF16) return DC_ERR_UNSUPPORTED;
   if (dims->dtype == DC_BF16)
-    split = !dc::step_fits(L, G, D, feat != nullptr, 0) || (U < 128 && L > 2 * dc::step_chunk_rows());
+    split = ragged || !dc::step_fits(L, G, D, feat != nullptr, 0) ||
+            (U < 128 && L > 2 * dc::step_chunk_rows());
   else
     split = use_split(dims, L, feat != nullptr);
   // the matrix-core unit path parks each row's retired (cz, cn) in the workspace
@@ -211,6 +215,7 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   a.len_old = len;
   a.L = L;
   a.append = append;
+  a.unit_len = kv->unit_len;
   a.scale = scale_of(dims);
   if (feat) {
     a.alpha = feat->alpha;
@@ -290,8 +295,13 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   if (L > dc::evict_max_len()) return DC_ERR_UNSUPPORTED;
   if (T < 1) return DC_ERR_SHAPE;
   const int evict = budget < L;
-  need = ext ? align256(dc::evict_ext_ws_bytes((int)units_of(dims), L))
-             : (L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0);
+  const bool ragged = kv->unit_len != nullptr;
+  if (ragged && dims->dtype != DC_BF16) return DC_ERR_UNSUPPORTED;
+  // the compaction's move list (two ints per move) lives in LDS
+  const int moves = ragged ? (L - 1 < budget ? L - 1 : budget) : evict ? (L - budget < budget ? L - budget : budget) : 0;
+  if (moves > MAX_MOVES) return DC_ERR_UNSUPPORTED;
+  need = (ext || ragged) ? align256(dc::evict_ext_ws_bytes((int)units_of(dims), L))
+                         : (L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0);
   if (need && (!ws || ws_bytes < need)) return DC_ERR_WORKSPACE;
   memset(&e, 0, sizeof(e));
   e.k = kv->k;
@@ -309,6 +319,8 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   e.units = (int)units_of(dims);
   e.L = L;
   e.budget = evict ? budget : L;
+  e.ld_kept = e.budget;
+  e.unit_len = kv->unit_len;
   e.T = T;
   e.nh = policy->n_hidden_layers;
   e.h1 = policy->hidden[0];
@@ -319,6 +331,17 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   e.evict = evict;
   e.ws_keys = (uint64_t*)ws;
   return DC_OK;
+}
+
+// Ragged caches: each unit's length follows its append / eviction on the stream.
+dc_status ragged_after_decode(const dc_kv* kv, const dc::DecodeArgs& a, void* stream) {
+  if (!kv->unit_len || !a.append) return DC_OK;
+  return dc::launch_unit_len_add(kv->unit_len, a.units, 1, stream) ? DC_ERR_HIP : DC_OK;
+}
+dc_status ragged_after_evict(const dc_kv* kv, const dc::EvictArgs& e, const int32_t* budgets,
+                             int bmax, void* stream) {
+  if (!kv->unit_len || (!budgets && !e.evict)) return DC_OK;
+  return dc::launch_unit_len_min(kv->unit_len, budgets, bmax, e.units, stream) ? DC_ERR_HIP : DC_OK;
 }
 
 // Validate a log-partition call and fill its arguments.
@@ -365,6 +388,7 @@ dc_status dc_decode_step(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const vo
   if (st != DC_OK) return st;
   st = launch_decode_any(dims, a, feat != nullptr, split, hip_stream);
   if (st != DC_OK) return st;
+  if (ragged_after_decode(kv, a, hip_stream) != DC_OK) return DC_ERR_HIP;
   commit_decode(kv, feat, a, dims->ent_window);
   return DC_OK;
 }
@@ -379,6 +403,7 @@ dc_status dc_score_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc
                             kv->len, feat->next_pos, e, need);
   if (st != DC_OK) return st;
   if (dc::launch_evict(e, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
+  if (ragged_after_evict(kv, e, nullptr, e.budget, hip_stream) != DC_OK) return DC_ERR_HIP;
   kv->len = e.budget;
   return DC_OK;
 }
@@ -407,9 +432,11 @@ dc_status dc_sample_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
     st = prep_logz(e.units, e.L, budget, gumbel->tau, scores_out, kept_out, nullptr, logp_out, ws,
                    ws_bytes, z);
     if (st != DC_OK) return st;
+    z.unit_len = kv->unit_len;      // pre-eviction lengths: committed after the log-partition
   }
   if (dc::launch_evict(e, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
   if (logp_out && dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  if (ragged_after_evict(kv, e, nullptr, e.budget, hip_stream) != DC_OK) return DC_ERR_HIP;
   kv->len = e.budget;
   return DC_OK;
 }
@@ -445,16 +472,67 @@ dc_status dc_decode_sample_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat,
   const int G = group_of(dims), D = dims->head_dim;
   const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
   const bool fused = dims->dtype == DC_BF16 && !split && !e.ext && !feat->sigma && G >= 4 &&
-                     dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
+                     !kv->unit_len && dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
   if (fused) {
     if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
   } else {
     st = launch_decode_any(dims, a, true, split, hip_stream);
     if (st != DC_OK) return st;
+    if (ragged_after_decode(kv, a, hip_stream) != DC_OK) return DC_ERR_HIP;
     if (dc::launch_evict(e, dims->dtype, D, hip_stream) != 0) return DC_ERR_HIP;
   }
-  if (logp_out && dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  if (logp_out) {
+    z.unit_len = kv->unit_len;
+    if (dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  }
+  if (ragged_after_evict(kv, e, nullptr, e.budget, hip_stream) != DC_OK) return DC_ERR_HIP;
   commit_decode(kv, feat, a, dims->ent_window);
+  kv->len = e.budget;
+  return DC_OK;
+}
+
+dc_status dc_score_evict_units(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const dc_policy* policy,
+                               const int32_t* budgets, int32_t max_budget, const dc_gumbel* gumbel,
+                               float* scores_out, int32_t* kept_out, double* logp_out, void* ws,
+                               size_t ws_bytes, void* hip_stream) {
+  if (!kv || !feat || !budgets || !kv->unit_len) return DC_ERR_NULL;
+  if (logp_out && (!gumbel || !scores_out || !kept_out)) return DC_ERR_NULL;
+  dc::EvictArgs e;
+  size_t need = 0;
+  dc_status st = prep_evict(dims, kv, feat, policy, max_budget, scores_out, kept_out, ws, ws_bytes,
+                            kv->len, feat->next_pos, e, need);
+  if (st != DC_OK) return st;
+  e.budgets = budgets;              // per unit, clamped to [1, e.budget] by the kernels
+  if (gumbel) {
+    if (!(gumbel->tau > 0.0f) || isinf(gumbel->tau)) return DC_ERR_VALUE;
+    e.sample = 1;
+    e.tau = gumbel->tau;
+    e.seed0 = gumbel->seed[0];
+    e.seed1 = gumbel->seed[1];
+    e.draw = gumbel->draw;
+  }
+  dc::LogzArgs z;
+  if (logp_out) {
+    // K of any unit is at most min(budget, rows / 2): the kernel is chosen for that bound
+    st = prep_logz(e.units, e.L, e.budget, gumbel->tau, scores_out, kept_out, nullptr, logp_out, ws,
+                   ws_bytes, z);
+    if (st != DC_OK) return st;
+    z.unit_len = kv->unit_len;
+    z.budgets = budgets;
+    z.nk = e.ld_kept;
+    z.K = e.budget < e.L / 2 ? e.budget : e.L / 2;
+    if (z.K > dc::logz_band_entries()) {
+      // band history for that bound: 8 B per row, inside the row-key workspace
+      // the selection used (it is finished with it when the log-partition runs)
+      const size_t band = (size_t)e.units * e.L * (sizeof(float) + sizeof(int));
+      if (!ws || ws_bytes < band) return DC_ERR_WORKSPACE;
+      z.col_m = (float*)ws;
+      z.col_k = (int*)((char*)ws + (size_t)e.units * e.L * sizeof(float));
+    }
+  }
+  if (dc::launch_evict(e, dims->dtype, dims->head_dim, hip_stream) != 0) return DC_ERR_HIP;
+  if (logp_out && dc::launch_logz(z, hip_stream) != 0) return DC_ERR_HIP;
+  if (ragged_after_evict(kv, e, budgets, e.budget, hip_stream) != DC_OK) return DC_ERR_HIP;
   kv->len = e.budget;
   return DC_OK;
 }
@@ -501,8 +579,10 @@ dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   } else {
     st = launch_decode_any(dims, a, true, split, hip_stream);
     if (st != DC_OK) return st;
+    if (ragged_after_decode(kv, a, hip_stream) != DC_OK) return DC_ERR_HIP;
     if (dc::launch_evict(e, dims->dtype, D, hip_stream) != 0) return DC_ERR_HIP;
   }
+  if (ragged_after_evict(kv, e, nullptr, e.budget, hip_stream) != DC_OK) return DC_ERR_HIP;
   commit_decode(kv, feat, a, dims->ent_window);
   kv->len = e.budget;
   return DC_OK;

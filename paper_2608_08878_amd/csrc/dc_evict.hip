@@ -65,7 +65,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
       for (int r = tid; r < L; r += ENT) a.kept_out[(size_t)u * L + r] = r;
     return;
   }
-  select_compact<RegKeys<REG_KPT>, DTYPE, D>(a, u, keys, REG_KPT, sh, dyn);
+  select_compact<RegKeys<REG_KPT>, DTYPE, D>(a, u, a.L, a.budget, keys, REG_KPT, sh, dyn);
 }
 
 // Long caches: scores to keys in the workspace (grid over rows) ...
@@ -79,14 +79,15 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
   const int u = blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
-  for (int base = blockIdx.x * 256; base < a.L; base += gridDim.x * 256) {
+  const int L = unit_rows(a, u);
+  for (int base = blockIdx.x * 256; base < L; base += gridDim.x * 256) {
     const int r = base + threadIdx.x;
     float x[1][4];
     int32_t p;
-    load_features(a, ub + (r < a.L ? r : a.L - 1), invT, x[0], p);
+    load_features(a, ub + (r < L ? r : L - 1), invT, x[0], p);
     float sc[1];
     policy_scores<1, NH>(a, x, sc, 1, NH == 2 ? spl : nullptr);
-    if (r < a.L) {
+    if (r < L) {
       if (a.scores_out) a.scores_out[(size_t)u * a.L + r] = sc[0];
       keys[(size_t)u * kstride + r] = row_key(a.sample ? sampled_score(a, sc[0], p, u) : sc[0], p);
     }
@@ -98,9 +99,10 @@ __global__ void __launch_bounds__(256) score_ext_kernel(EvictArgs a, uint64_t* k
   const int u = blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
-  for (int base = blockIdx.x * 256; base < a.L; base += gridDim.x * 256) {
+  const int L = unit_rows(a, u);
+  for (int base = blockIdx.x * 256; base < L; base += gridDim.x * 256) {
     const int r = base + threadIdx.x;
-    if (r < a.L) {
+    if (r < L) {
       int32_t p;
       const float sc = ext_score(a, ub + r, invT, p);
       if (a.scores_out) a.scores_out[(size_t)u * a.L + r] = sc;
@@ -115,8 +117,17 @@ __global__ void __launch_bounds__(ENT) select_kernel(EvictArgs a, const uint64_t
   extern __shared__ int dyn[];
   __shared__ SelShared sh;
   const int u = blockIdx.x;
+  const int L = unit_rows(a, u);
+  const int Bu = unit_budget(a, u);
+  if (Bu >= L) {                        // (per-unit budgets) this unit keeps every row
+    if (a.kept_out)
+      for (int r = threadIdx.x; r < a.ld_kept; r += ENT) a.kept_out[(size_t)u * a.ld_kept + r] = r < L ? r : -1;
+    return;
+  }
   MemKeys mk{keys + (size_t)u * kstride};
-  select_compact<MemKeys, DTYPE, D>(a, u, mk, (a.L + ENT - 1) / ENT, sh, dyn);
+  select_compact<MemKeys, DTYPE, D>(a, u, L, Bu, mk, (L + ENT - 1) / ENT, sh, dyn);
+  if (a.kept_out && a.budgets)          // slots past this unit's budget
+    for (int r = Bu + threadIdx.x; r < a.ld_kept; r += ENT) a.kept_out[(size_t)u * a.ld_kept + r] = -1;
 }
 
 __global__ void identity_kept_kernel(int32_t* kept, int units, int L) {
@@ -129,15 +140,32 @@ int evict_max_len() { return MAX_LEN; }
 
 template <int DTYPE, int D>
 static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) {
-  if (!a.evict && !a.scores_out && !a.kept_out) return 0;
+  const bool rg = a.unit_len || a.budgets;
+  if (!a.evict && !rg && !a.scores_out && !a.kept_out) return 0;
+  // moves: min(L - B, B); per-unit budgets: bounded by min(L - 1, the largest budget)
   const int E = a.L - a.budget;
-  const int nmv = a.evict ? (E < a.budget ? E : a.budget) : 0;
+  const int nmv = rg ? (a.L - 1 < a.budget ? a.L - 1 : a.budget) : a.evict ? (E < a.budget ? E : a.budget) : 0;
   EvictArgs b = a;
   b.mv_ints = (2 * (nmv > 0 ? nmv : 1) + 3) / 4 * 4;   // keeps the weights after it 16-byte aligned
   const size_t pbytes = a.nh == 2 ? (size_t)policy_floats(2, a.h1, a.h2) * sizeof(float) : 0;
   const size_t dyn = (size_t)b.mv_ints * sizeof(int);
   const int kstride = (a.L + ENT - 1) / ENT * ENT;
-  if (a.ext) {
+  const bool ragged = a.unit_len || a.budgets;
+  if (ragged && !a.ext) {
+    // per-unit lengths or budgets: scores to row keys, then one select per unit
+    // that decides for itself whether the unit evicts
+    int gx = (a.L + 255) / 256;
+    if (a.nh == 2) {
+      gx = gx < 16 ? gx : 16;
+      hipFuncSetAttribute((const void*)score_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pbytes);
+      hipLaunchKernelGGL(score_kernel<2>, dim3(gx, a.units), dim3(256), pbytes, s, b, ws_keys, kstride);
+    } else {
+      hipLaunchKernelGGL(score_kernel<1>, dim3(gx, a.units), dim3(256), 0, s, b, ws_keys, kstride);
+    }
+    auto k = select_kernel<DTYPE, D>;
+    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+    hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);
+  } else if (a.ext) {
     if (a.nh == 2) {
       const int rc = launch_score_mlp2(b, ws_keys, kstride, s);
       if (rc) return rc;
@@ -145,7 +173,7 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
       hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
                          ws_keys, kstride);
     }
-    if (a.evict) {
+    if (a.evict || ragged) {
       auto k = select_kernel<DTYPE, D>;
       hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
       hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);

@@ -21,6 +21,8 @@ struct DecodeArgs {
   void* qring;          // [units][w][G][D]
   float* qstat;         // [units][w][G][3]
   float* sigma;         // [units][cap] head variance of this step's weights, or null
+  int32_t* unit_len;    // [units] rows of each unit before this step (ragged caches), or null:
+                        // then every unit has len_old rows; L, len_old are upper bounds
   int64_t cap;
   int units;
   int len_old;          // valid rows before the append
@@ -52,6 +54,9 @@ struct EvictArgs {
   int32_t* pos;
   float* vnorm;
   float* sigma;         // [units][cap] or null (moved with the rows; read by 5-input policies)
+  const int32_t* unit_len;  // [units] rows of each unit (ragged caches) or null (L rows each)
+  const int32_t* budgets;   // [units] budget of each unit, or null (budget for all)
+  int ld_kept;          // row stride of kept_out (the budget, or its bound for per-unit budgets)
   const float* params;
   float* scores_out;
   int32_t* kept_out;
@@ -76,9 +81,11 @@ struct EvictArgs {
 
 // Log-partition / log-probability of size-B subsets (one call covers every unit).
 struct LogzArgs {
-  const float* scores;      // [units][L] policy scores s_i
-  const int32_t* kept;      // [units][nk] kept rows (indices into the scores) or null
+  const float* scores;      // [units][L] policy scores s_i (row stride L)
+  const int32_t* kept;      // [units][nk] kept rows (indices into the scores) or null (row stride nk)
   int nk;                   // min(B, L)
+  const int32_t* unit_len;  // [units] rows of each unit (ragged) or null: L for all
+  const int32_t* budgets;   // [units] budget of each unit or null: B for all
   double* logz;             // [units] or null
   double* logp;             // [units] or null (needs kept)
   float* col_m;             // [units][L] band column (K > logz_band_entries()) or null
@@ -121,6 +128,9 @@ bool decode_fits_lds(int L, int G, int D);
 int decode_chunk_rows();
 int launch_evict(const EvictArgs& a, int dtype, int D, void* stream);
 int launch_logz(const LogzArgs& a, void* stream);
+// Ragged caches: len[u] += add, or len[u] = min(len[u], budgets ? budgets[u] : b).
+int launch_unit_len_add(int32_t* len, int units, int add, void* stream);
+int launch_unit_len_min(int32_t* len, const int32_t* budgets, int b, int units, void* stream);
 int launch_reinforce(const ReinforceArgs& a, void* stream);
 size_t logz_ws_bytes(int units, int L, int B);
 int logz_band_entries();

@@ -96,6 +96,23 @@ __device__ __forceinline__ void weight(double z, float& m, int& k) {
   norm(e, (int)n, m, k);
 }
 
+// Sizes of unit u (ragged caches and per-unit budgets: per unit; the host
+// chose the kernel for an upper bound of K).
+struct UnitDims {
+  int L, B, nk, K, neg;
+};
+
+__device__ __forceinline__ UnitDims unit_dims(const LogzArgs& a, int u) {
+  UnitDims d;
+  // device values clamped to the host's bounds (rows [1, L], budgets [1, B])
+  d.L = a.unit_len ? (a.unit_len[u] < 1 ? 1 : a.unit_len[u] > a.L ? a.L : a.unit_len[u]) : a.L;
+  d.B = a.budgets ? (a.budgets[u] < 1 ? 1 : a.budgets[u] > a.B ? a.B : a.budgets[u]) : a.B;
+  d.nk = d.B < d.L ? d.B : d.L;
+  d.K = d.B >= d.L ? 0 : (d.B <= d.L - d.B ? d.B : d.L - d.B);
+  d.neg = d.B < d.L && d.L - d.B < d.B;
+  return d;
+}
+
 struct UnitStats {
   double shift;    // max over rows of (neg ? -r : r)
   double sumr;     // sum of r
@@ -124,20 +141,21 @@ __device__ __forceinline__ int wave_or(int x) {
 
 __device__ __forceinline__ double r_of(const LogzArgs& a, float s) { return (double)s / (double)a.tau; }
 
-__device__ UnitStats unit_stats(const LogzArgs& a, const float* s, const int32_t* kept, int lane) {
+__device__ UnitStats unit_stats(const LogzArgs& a, const UnitDims& d, const float* s,
+                                const int32_t* kept, int lane) {
   double mx = -INFINITY, sum = 0.0, ks = 0.0;
   int bad = 0;
-  for (int i = lane; i < a.L; i += 64) {
+  for (int i = lane; i < d.L; i += 64) {
     const double r = r_of(a, s[i]);
     bad |= !isfinite(r);
-    const double x = a.neg ? -r : r;
+    const double x = d.neg ? -r : r;
     mx = x > mx ? x : mx;
     sum += r;
   }
   if (kept) {
-    for (int t = lane; t < a.nk; t += 64) {
+    for (int t = lane; t < d.nk; t += 64) {
       const int idx = kept[t];
-      if (idx < 0 || idx >= a.L) bad = 1;
+      if (idx < 0 || idx >= d.L) bad = 1;
       else ks += r_of(a, s[idx]);
     }
   }
@@ -149,17 +167,19 @@ __device__ UnitStats unit_stats(const LogzArgs& a, const float* s, const int32_t
   return st;
 }
 
-__device__ __forceinline__ void row_weight(const LogzArgs& a, float s, double shift, float& m, int& k) {
+__device__ __forceinline__ void row_weight(const LogzArgs& a, const UnitDims& d, float s,
+                                           double shift, float& m, int& k) {
   const double r = r_of(a, s);
-  weight((a.neg ? -r : r) - shift, m, k);
+  weight((d.neg ? -r : r) - shift, m, k);
 }
 
-__device__ void finish(const LogzArgs& a, int u, const UnitStats& st, float mK, int kK, int lane) {
+__device__ void finish(const LogzArgs& a, const UnitDims& d, int u, const UnitStats& st, float mK,
+                       int kK, int lane) {
   if (lane) return;
   double logz;
-  if (a.K == 0) logz = st.sumr;                  // one subset: the whole cache
-  else logz = (double)a.K * st.shift + (a.neg ? st.sumr : 0.0) + log((double)mK) + (double)kK * LN2;
-  double logp = a.B >= a.L ? 0.0 : st.kept - logz;
+  if (d.K == 0) logz = st.sumr;                  // one subset: the whole cache
+  else logz = (double)d.K * st.shift + (d.neg ? st.sumr : 0.0) + log((double)mK) + (double)kK * LN2;
+  double logp = d.B >= d.L ? 0.0 : st.kept - logz;
   if (st.bad) logz = logp = __builtin_nan("");
   if (a.logz) a.logz[u] = logz;
   if (a.logp) a.logp[u] = logp;
@@ -197,8 +217,9 @@ __device__ __forceinline__ void poly_mul(const float* lm, const int* lk, const f
 template <int KS>
 __global__ void __launch_bounds__(64) logz_rows_kernel(LogzArgs a) {
   const int u = blockIdx.x, lane = threadIdx.x;
+  const UnitDims d = unit_dims(a, u);
   const float* s = a.scores + (size_t)u * a.L;
-  const UnitStats st = unit_stats(a, s, a.kept ? a.kept + (size_t)u * a.nk : nullptr, lane);
+  const UnitStats st = unit_stats(a, d, s, a.kept ? a.kept + (size_t)u * a.nk : nullptr, lane);
   float m[KS];
   int k[KS];
 #pragma unroll
@@ -206,12 +227,12 @@ __global__ void __launch_bounds__(64) logz_rows_kernel(LogzArgs a) {
     m[j] = 0.0f;
     k[j] = KZERO;
   }
-  for (int i0 = 0; i0 < a.L; i0 += 64 * RENORM) {
-    const int iend = a.L < i0 + 64 * RENORM ? a.L : i0 + 64 * RENORM;
+  for (int i0 = 0; i0 < d.L; i0 += 64 * RENORM) {
+    const int iend = d.L < i0 + 64 * RENORM ? d.L : i0 + 64 * RENORM;
     for (int i = i0 + lane; i < iend; i += 64) {
       float xm;
       int xk;
-      row_weight(a, s[i], st.shift, xm, xk);
+      row_weight(a, d, s[i], st.shift, xm, xk);
 #pragma unroll
       for (int j = KS - 1; j >= 1; --j) upd(m[j], k[j], m[j - 1], k[j - 1], xm, xk);
       upd(m[0], k[0], 0.5f, 1, xm, xk);
@@ -239,22 +260,23 @@ __global__ void __launch_bounds__(64) logz_rows_kernel(LogzArgs a) {
   int kK = 1;
 #pragma unroll
   for (int j = 0; j < KS; ++j)
-    if (j == a.K - 1) {
+    if (j == d.K - 1) {
       mK = m[j];
       kK = k[j];
     }
-  finish(a, u, st, mK, kK, lane);
+  finish(a, d, u, st, mK, kK, lane);
 }
 
 template <int C>
 __global__ void __launch_bounds__(64) logz_col_kernel(LogzArgs a) {
   const int u = blockIdx.x, lane = threadIdx.x;
+  const UnitDims d = unit_dims(a, u);
   const float* s = a.scores + (size_t)u * a.L;
-  const UnitStats st = unit_stats(a, s, a.kept ? a.kept + (size_t)u * a.nk : nullptr, lane);
+  const UnitStats st = unit_stats(a, d, s, a.kept ? a.kept + (size_t)u * a.nk : nullptr, lane);
   float mK = 0.5f;
   int kK = 1;
-  if (a.K > 0) {
-    const int nb = (a.K + 64 * C - 1) / (64 * C);
+  if (d.K > 0) {
+    const int nb = (d.K + 64 * C - 1) / (64 * C);
     float* cm = a.col_m ? a.col_m + (size_t)u * a.L : nullptr;
     int* ck = a.col_k ? a.col_k + (size_t)u * a.L : nullptr;
     for (int band = 0; band < nb; ++band) {
@@ -266,12 +288,12 @@ __global__ void __launch_bounds__(64) logz_col_kernel(LogzArgs a) {
         m[t] = 0.0f;
         k[t] = KZERO;
       }
-      for (int i0 = 0; i0 < a.L; i0 += 64) {
-        const int n = a.L - i0 < 64 ? a.L - i0 : 64;
+      for (int i0 = 0; i0 < d.L; i0 += 64) {
+        const int n = d.L - i0 < 64 ? d.L - i0 : 64;
         float xm = 0.0f, inm = 0.5f, outm = 0.0f;
         int xk = KZERO, ink = 1, outk = KZERO;
         if (lane < n) {
-          row_weight(a, s[i0 + lane], st.shift, xm, xk);
+          row_weight(a, d, s[i0 + lane], st.shift, xm, xk);
           if (rd) {
             inm = cm[i0 + lane];
             ink = ck[i0 + lane];
@@ -317,7 +339,7 @@ __global__ void __launch_bounds__(64) logz_col_kernel(LogzArgs a) {
           ck[i0 + lane] = outk;
         }
       }
-      const int jj = a.K - 1 - band * 64 * C;     // entry K within this band
+      const int jj = d.K - 1 - band * 64 * C;     // entry K within this band
       if (jj >= 0 && jj < 64 * C) {
         float pm = 0.0f;
         int pk = KZERO;
@@ -332,7 +354,7 @@ __global__ void __launch_bounds__(64) logz_col_kernel(LogzArgs a) {
       }
     }
   }
-  finish(a, u, st, mK, kK, lane);
+  finish(a, d, u, st, mK, kK, lane);
 }
 
 template <typename F>

@@ -93,7 +93,8 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
   __syncthreads();
   const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ri = lane & 15, kg = lane >> 4;
-  const int h1 = a.h1, h2 = a.h2, ln = a.ln, L = a.L;
+  const int h1 = a.h1, h2 = a.h2, ln = a.ln;
+  const int L = unit_rows(a, u);   // this unit's rows (scores_out keeps stride a.L)
   const float fh1 = (float)h1, fh2 = (float)h2;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
@@ -205,7 +206,7 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
       for (int i = 1; i < 4; ++i) sc = ri == i ? score[i] : sc;
       if (row < L) {
         const int32_t p = a.pos[ub + row];
-        if (a.scores_out) a.scores_out[(size_t)u * L + row] = sc;
+        if (a.scores_out) a.scores_out[(size_t)u * a.L + row] = sc;
         keys[(size_t)u * kstride + row] = row_key(a.sample ? sampled_score(a, sc, p, u) : sc, p);
       }
     }

@@ -23,6 +23,20 @@ __device__ __forceinline__ uint64_t row_key(float s, int32_t pos) {
   return ((uint64_t)score_key(s) << 32) | (uint64_t)(0xFFFFFFFFu - (uint32_t)pos);
 }
 
+// Rows and budget of unit u (ragged caches, per-unit budgets), clamped to the
+// host's bounds (rows to [1, L], budgets to [1, budget]) so that a bad device
+// value cannot take an access out of the buffers.
+__device__ __forceinline__ int unit_rows(const EvictArgs& a, int u) {
+  if (!a.unit_len) return a.L;
+  const int n = a.unit_len[u];
+  return n < 1 ? 1 : n > a.L ? a.L : n;
+}
+__device__ __forceinline__ int unit_budget(const EvictArgs& a, int u) {
+  if (!a.budgets) return a.budget;
+  const int b = a.budgets[u];
+  return b < 1 ? 1 : b > a.budget ? a.budget : b;
+}
+
 // Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds of two 32x32
 // multiplies with the key advanced by the Weyl constants; only the first output
 // word is used.
@@ -423,12 +437,14 @@ __device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, 
 // Select the E smallest keys and compact the unit.  `keys` holds the keys of
 // rows k*NT + tid for k < kpt (invalid rows beyond L are ignored); NT is the
 // workgroup size.
+// Keep the top B of unit u's L rows (B < L) and compact; kept_out rows have
+// stride a.ld_kept.
 template <typename Keys, int DTYPE, int D, int NT = ENT>
-__device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int kpt, SelShared& sh,
-                               int* mv) {
+__device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Keys& keys, int kpt,
+                               SelShared& sh, int* mv) {
   constexpr int ELT = DTYPE == 0 ? 4 : 2;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int L = a.L, B = a.budget, E = L - B;
+  const int E = L - B;
   const size_t ub = (size_t)u * a.cap;
   // threshold: evicted rows are those with key <= thr
   uint64_t thr;
@@ -459,7 +475,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
     __syncthreads();
     const int ev = sh.sel[3];
     if (a.kept_out)
-      for (int r = tid; r < B; r += NT) a.kept_out[(size_t)u * B + r] = r == ev ? B : r;
+      for (int r = tid; r < B; r += NT) a.kept_out[(size_t)u * a.ld_kept + r] = r == ev ? B : r;
     if (ev < B && tid < 64) {
       const size_t gd = ub + ev, gs = ub + B;
       constexpr int N16 = D * ELT / 16;
@@ -539,7 +555,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
     block_scan2<NT>(hole, mover, rk0, rk1, t0, t1, sh);
     if (hole) mv[2 * (run0 + rk0)] = r;
     if (mover) mv[2 * (run1 + rk1) + 1] = r;
-    if (a.kept_out && r < B && !ev) a.kept_out[(size_t)u * B + r] = r;
+    if (a.kept_out && r < B && !ev) a.kept_out[(size_t)u * a.ld_kept + r] = r;
     run0 += t0;
     run1 += t1;
   }
@@ -564,7 +580,7 @@ __device__ void select_compact(const EvictArgs& a, int u, const Keys& keys, int 
       a.pos[gd] = a.pos[gs];
       a.vnorm[gd] = a.vnorm[gs];
       if (a.sigma) a.sigma[gd] = a.sigma[gs];
-      if (a.kept_out) a.kept_out[(size_t)u * B + dst] = src;
+      if (a.kept_out) a.kept_out[(size_t)u * a.ld_kept + dst] = src;
     }
   }
 }

@@ -96,6 +96,15 @@ __device__ __forceinline__ void load_ret(RetStats<G>& r, const DecodeArgs& a, in
 // the group's row l, in zr[k] / nr[k] for the wave's k-th group.
 constexpr int S_GMAX = S_KMAX;        // 64-row groups per wave, at most (L <= 5120)
 
+// Rows of unit u before this step (per unit for ragged caches).
+// (Device lengths are clamped to [0, len_old], the host's bound, so that a bad
+// value cannot take an access out of the buffers.)
+__device__ __forceinline__ int len_old_of(const DecodeArgs& a, int u) {
+  if (!a.unit_len) return a.len_old;
+  const int n = a.unit_len[u];
+  return n < 0 ? 0 : n > a.len_old ? a.len_old : n;
+}
+
 template <int D, int G, bool FEAT, bool GROUPED, int RS = G>
 __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r1, float* s_sink,
                                        float* r_sink, int sink0, const uint4 (&qa)[MG<D>::NT],
@@ -105,7 +114,7 @@ __device__ __forceinline__ void pass_a(const DecodeArgs& a, int u, int r0, int r
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, i = lane & 15, g = lane >> 4;
   const char* kc = (const char*)a.k + (size_t)u * a.cap * D * 2;
   const char* kn = a.append ? (const char*)a.k_new + (size_t)u * D * 2 : nullptr;
-  const int newrow = a.append ? a.len_old : -1;
+  const int newrow = a.append ? len_old_of(a, u) : -1;
   const int ntiles = (r1 - r0 + 15) / 16;
 #pragma unroll
   for (int r = 0; r < 4; ++r) mrun[r] = NEG_BIG;
@@ -338,7 +347,7 @@ __device__ __forceinline__ void pass_b(const DecodeArgs& a, int u, int r0, int r
   const int tid = threadIdx.x, grp = tid / LPR, lam = tid % LPR;
   const char* vc = (const char*)a.v + (size_t)u * a.cap * D * 2;
   const char* vn = a.append ? (const char*)a.v_new + (size_t)u * D * 2 : nullptr;
-  const int newrow = a.append ? a.len_old : -1;
+  const int newrow = a.append ? len_old_of(a, u) : -1;
 #pragma unroll
   for (int j = 0; j < G; ++j)
 #pragma unroll
@@ -490,7 +499,7 @@ __device__ __forceinline__ void append_rows(const DecodeArgs& a, int u) {
     const bool isv = t >= N16;
     const int c = isv ? t - N16 : t;
     const char* src = (const char*)(isv ? a.v_new : a.k_new) + (size_t)u * D * 2;
-    char* dst = (char*)(isv ? a.v : a.k) + ((size_t)u * a.cap + a.len_old) * D * 2;
+    char* dst = (char*)(isv ? a.v : a.k) + ((size_t)u * a.cap + len_old_of(a, u)) * D * 2;
     *reinterpret_cast<uint4*>(dst + c * 16) = ldg16(src + c * 16);
   }
 }
@@ -586,7 +595,7 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
   }
   if constexpr (FEAT) {
     const float newnorm = a.append ? new_row_vnorm<D>(a, u, &newnorm_slot) : 0.0f;
-    const int newrow = a.append ? a.len_old : -1;
+    const int newrow = a.append ? len_old_of(a, u) : -1;
     const float invT = 1.0f / (float)a.T;
     constexpr float invG = 1.0f / G;
     uint64_t* keys = reinterpret_cast<uint64_t*>(sbuf);   // row i's key replaces its weights
@@ -700,7 +709,7 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
       if (e.evict) {
         const int nslots = (L + SNT - 1) / SNT;
         LdsKeys<S_KMAX, SNT> lk{keys, KS};
-        select_compact<LdsKeys<S_KMAX, SNT>, 1, D, SNT>(e, u, lk, nslots, sh, mv);
+        select_compact<LdsKeys<S_KMAX, SNT>, 1, D, SNT>(e, u, L, e.budget, lk, nslots, sh, mv);
       } else if (e.kept_out) {
         for (int r = tid; r < L; r += SNT) e.kept_out[(size_t)u * L + r] = r;
       }
@@ -714,8 +723,14 @@ template <int D, int G, bool FEAT>
 __global__ void __launch_bounds__(SNT) stepc_a_kernel(DecodeArgs a) {
   __shared__ float stat[SNW * 2 * G + 2 * G];
   const int c = blockIdx.x, u = blockIdx.y;
-  const int r0 = c * a.chunk, r1 = min(a.L, r0 + a.chunk);
+  const int Lu = len_old_of(a, u) + a.append;       // this unit's rows (ragged caches: per unit)
+  const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk);
   if (c == 0 && a.append) append_rows<D>(a, u);
+  if (r0 >= r1) {
+    // a chunk past this unit's rows: neutral partials (max -inf, sums 0, no output)
+    if (threadIdx.x < G) a.ws_part[((size_t)u * a.nchunks + c) * (3 * G + G * D) + threadIdx.x] = NEG_BIG;
+    return;
+  }
   const bool retire = FEAT && a.retire;
   uint4 qa[MG<D>::NT];
   load_qfrag<D, G>(qa, a, u, retire);
@@ -754,7 +769,13 @@ __global__ void __launch_bounds__(SNT) stepc_b_kernel(DecodeArgs a) {
   __shared__ float obuf[SNW * G * D];
   __shared__ float stat[SNW * 2 * G + 2 * G];
   const int c = blockIdx.x, u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int r0 = c * a.chunk, r1 = min(a.L, r0 + a.chunk), n = r1 - r0;
+  const int Lu = len_old_of(a, u) + a.append;
+  const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk), n = r1 - r0;
+  if (n <= 0) {
+    float* part = a.ws_part + ((size_t)u * a.nchunks + c) * (3 * G + G * D);
+    for (int t = tid; t < 2 * G + G * D; t += SNT) part[G + t] = 0.0f;
+    return;
+  }
   float M[G];
   chunk_max<G>(a, u, D, M);
   const float* src = a.ws_s + ((size_t)u * a.lmax + r0) * G;
@@ -793,7 +814,8 @@ template <int D, int G, bool FEAT>
 __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
   __shared__ float newnorm_slot;
   const int c = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
-  const int r0 = c * a.chunk, r1 = min(a.L, r0 + a.chunk);
+  const int Lu = len_old_of(a, u) + a.append;
+  const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk);
   const int PART = 3 * G + G * D;
   const float* parts = a.ws_part + (size_t)u * a.nchunks * PART;
   float M[G], ls[G], us[G], invl[G], H[G];
@@ -811,7 +833,7 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
     H[j] = __logf(l) - uu * invl[j];
   }
   if constexpr (FEAT) {
-    const int newrow = a.append ? a.len_old : -1;
+    const int newrow = a.append ? len_old_of(a, u) : -1;
     const float newnorm = (a.append && newrow >= r0 && newrow < r1)
                               ? new_row_vnorm<D>(a, u, &newnorm_slot) : 0.0f;
     const float* s_src = a.ws_s + (size_t)u * a.lmax * G;
@@ -840,6 +862,33 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
     ((uint16_t*)a.out)[(size_t)u * G * D + t] = (uint16_t)f32_to_bf16_bits(acc * il);
   }
   if (FEAT && a.window > 0) write_ring2<D, G>(a, u, M, invl, H);
+}
+
+// ---------------------------------------------------------------- ragged caches
+__global__ void unit_len_add_kernel(int32_t* len, int units, int add) {
+  const int u = blockIdx.x * 256 + threadIdx.x;
+  if (u < units) len[u] += add;
+}
+
+__global__ void unit_len_min_kernel(int32_t* len, const int32_t* budgets, int b, int units) {
+  const int u = blockIdx.x * 256 + threadIdx.x;
+  if (u < units) {
+    int bu = budgets ? budgets[u] : b;
+    bu = bu < 1 ? 1 : bu > b ? b : bu;            // the clamp the selection applies
+    len[u] = bu < len[u] ? bu : len[u];
+  }
+}
+
+int launch_unit_len_add(int32_t* len, int units, int add, void* stream) {
+  hipLaunchKernelGGL(unit_len_add_kernel, dim3((units + 255) / 256), dim3(256), 0,
+                     (hipStream_t)stream, len, units, add);
+  return (int)hipGetLastError();
+}
+
+int launch_unit_len_min(int32_t* len, const int32_t* budgets, int b, int units, void* stream) {
+  hipLaunchKernelGGL(unit_len_min_kernel, dim3((units + 255) / 256), dim3(256), 0,
+                     (hipStream_t)stream, len, budgets, b, units);
+  return (int)hipGetLastError();
 }
 
 // ---------------------------------------------------------------- dispatch

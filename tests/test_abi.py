@@ -226,3 +226,43 @@ def test_dynamic_budget_matches_the_oracle():
     assert B.dc_dynamic_budget(float("nan"), 100, 32) == -1
     assert B.dc_dynamic_budget(0.25, -1, 32) == -1
     assert B.dc_dynamic_budget(0.25, 100, 0) == -1
+
+
+def test_score_evict_units_rejects_bad_arguments():
+    L = B.lib()
+    pol = B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)
+    g = B.make_gumbel(1.0, 1, 0)
+
+    def call(kv=None, budgets=FAKE, maxb=64, gum=None, sc=FAKE, kp=FAKE, lp=None, ws=None, wsb=0,
+             dims=None):
+        kv = kv or B.dc_kv(FAKE, FAKE, 50, FAKE)
+        return L.dc_score_evict_units(ctypes.byref(dims or _dims()), ctypes.byref(kv),
+                                      ctypes.byref(_feat()), ctypes.byref(pol), budgets, maxb,
+                                      None if gum is None else ctypes.byref(gum), sc, kp, lp, ws, wsb,
+                                      None)
+
+    assert call(budgets=None) == 1
+    assert call(kv=B.dc_kv(FAKE, FAKE, 50, None)) == 1          # per-unit lengths are required
+    assert call(lp=FAKE) == 1                                   # log pi needs the gumbel draw
+    assert call(gum=g, lp=FAKE, kp=None) == 1
+    assert call(maxb=0) == 5
+    assert call() == 6                                          # row keys need the workspace
+    assert call(dims=_dims(dtype=B.DC_F32)) == 3                # ragged caches are bf16
+    kv = B.dc_kv(FAKE, FAKE, 50, FAKE)
+    assert call(kv=kv, gum=B.make_gumbel(0.0, 1, 0), ws=FAKE, wsb=1 << 40) == 8
+    assert kv.len == 50
+
+
+def test_ragged_decode_needs_bf16_and_moves_fit_on_chip():
+    L = B.lib()
+    kv = B.dc_kv(FAKE, FAKE, 10, FAKE)
+    feat = _feat()
+    assert _decode(_dims(dtype=B.DC_F32), kv, feat) == 3
+    assert kv.len == 10
+    # a compaction that would move more than 16384 rows is refused (the move list is in LDS)
+    big = _dims(capacity=40960, n_layers=1)
+    kvb = B.dc_kv(FAKE, FAKE, 40000, None)
+    pol = B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)
+    assert L.dc_score_evict(ctypes.byref(big), ctypes.byref(kvb), ctypes.byref(_feat()),
+                            ctypes.byref(pol), 20000, None, None, FAKE, 1 << 40, None) == 3
+    assert kvb.len == 40000

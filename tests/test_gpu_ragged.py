@@ -1,0 +1,124 @@
+"""GPU parity of per-unit budgets on ragged caches (the head-level hybrid of
+the appendix: some heads keep their full cache, the others a budget; Sec. 3.2
+per-unit top-B): every unit keeps its own row count on the device, decode runs
+the chunked kernels per unit, and each unit's selection follows its budget.
+Free-running device and oracle trajectories until a selection lands in the
+near-tie band."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import sampling as osmp
+from oracle import unit as ounit
+from paper_2608_08878_amd import binding as B
+from paper_2608_08878_amd.buffers import DecodeBuffers
+from synth import gpu as sg
+from synth import workloads as W
+
+from . import harness as H
+from .test_gpu_sampling import _logz_tol, _sampled_check
+from .test_gpu_step import _check_decode, _policy, _step_tensors
+
+pytestmark = pytest.mark.gpu
+
+
+def _download(buf, u, L):
+    d = {"k": H.to_np(buf.k[u, :L]).astype(np.float64), "v": H.to_np(buf.v[u, :L]).astype(np.float64),
+         "pos": H.to_np(buf.pos[u, :L]).astype(np.int64), "alpha": H.to_np(buf.alpha[u, :L]),
+         "num": H.to_np(buf.num[u, :L]), "den": H.to_np(buf.den[u, :L]),
+         "vnorm": H.to_np(buf.vnorm[u, :L])}
+    return d
+
+
+def _ragged_run(budgets, steps, n0=700, gumbel=None, tau=1.0):
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=len(budgets), n_q_heads=4 * len(budgets), n0=n0,
+                               budget=max(budgets), steps=steps)
+    U = wl.units
+    buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                        wl.capacity, wl.dtype, wl.ent_window, 0.0, True, ragged=True)
+    buf.reserve_workspace(wl.capacity)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(n0, 0)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    bud = torch.tensor(budgets, dtype=torch.int32, device="cuda")
+    maxb = max(budgets)
+    sts = [H.oracle_student(wl, u) for u in range(U)]
+    q, kn, vn = _step_tensors(wl)
+    for t in range(steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        out = buf.decode_step(q, kn, vn)
+        torch.cuda.synchronize()
+        lens = H.to_np(buf.unit_len).astype(int)
+        outn = H.to_np(out)
+        pre = [_download(buf, u, lens[u]) for u in range(U)]
+        Lb = buf.kv.len
+        scores = torch.empty((U, Lb), dtype=torch.float32, device="cuda")
+        kept = torch.empty((U, min(maxb, Lb)), dtype=torch.int32, device="cuda")
+        logp = torch.empty(U, dtype=torch.float64, device="cuda") if gumbel else None
+        g = B.make_gumbel(tau, gumbel, t) if gumbel else None
+        buf.score_evict_units(pol, bud, maxb, g, scores, kept, logp)
+        torch.cuda.synchronize()
+        sc, kp = H.to_np(scores), H.to_np(kept)
+        post_lens = H.to_np(buf.unit_len).astype(int)
+        lp = logp.cpu().numpy() if gumbel else None
+        diverged = False
+        for u in range(U):
+            att = ounit.decode_step(sts[u], *H.step_inputs_np(wl, t, u))
+            assert lens[u] == sts[u].L, (t, u, lens[u], sts[u].L)
+            order = np.argsort(pre[u]["pos"])            # device slots -> oracle (position) order
+            _check_decode(wl, outn[u], {k: v[order] for k, v in pre[u].items()}, sts[u], att, (t, u))
+            s_or = ounit.scores(sts[u], pnp, wl.hidden)
+            ok, worst = H.vec_ok(sc[u, :lens[u]][order], s_or)
+            assert ok, (t, u, worst)
+            Bu = budgets[u]
+            nk = min(Bu, lens[u])
+            assert post_lens[u] == nk, (t, u)
+            assert np.all(kp[u, nk:] == -1) and np.all(kp[u, :nk] >= 0), (t, u)
+            post = _download(buf, u, nk)
+            # documented compaction for this unit's own budget
+            kmask = np.zeros(lens[u], bool)
+            kmask[kp[u, :nk]] = True
+            layout = H.hole_fill_layout(pre[u]["pos"], kmask, nk)
+            assert np.array_equal(kp[u, :nk], layout), (t, u)
+            for name in ("k", "v", "pos", "alpha", "num", "den", "vnorm"):
+                assert np.array_equal(post[name], pre[u][name][layout]), (t, u, name)
+            if gumbel:
+                ok, kept_o, amb, flips = _sampled_check(s_or, sts[u].pos, post["pos"], Bu, tau,
+                                                        gumbel, u, t)
+                assert ok, (t, u, amb, flips)
+                if flips == 0:
+                    ref = osmp.log_prob(s_or, kept_o, Bu, tau)
+                    ds = float(np.abs(sc[u, :lens[u]].astype(np.float64) - s_or).max()) / tau
+                    tol = _logz_tol(lens[u], Bu) + 2 * nk * ds + 1e-9 * abs(ref)
+                    assert abs(lp[u] - ref) <= tol, (t, u, lp[u], ref)
+                keep_rows = np.sort(kept_o)
+                flips_u = flips
+            else:
+                ok, amb, flips_u = H.selection_check(s_or, sts[u].pos, post["pos"], Bu)
+                assert ok, (t, u, amb, flips_u)
+                keep_rows = None
+            if keep_rows is not None:
+                ounit.evict(sts[u], np.where(np.isin(np.arange(sts[u].L), keep_rows), 1.0, 0.0), Bu)
+            else:
+                ounit.evict(sts[u], s_or, Bu)
+            diverged |= flips_u > 0
+        assert buf.kv.len == min(maxb, Lb)
+        if diverged:
+            print("trajectories parted at a near-tie at step", t)
+            return t
+    return steps
+
+
+def test_per_unit_budgets_and_a_full_cache_head():
+    # unit 1 never evicts (the hybrid's full-cache head); the others keep 200, 150, 320
+    assert _ragged_run([200, 10 ** 6, 150, 320], steps=6) >= 1
+
+
+def test_equal_budgets_reduce_to_the_fixed_budget():
+    assert _ragged_run([180, 180, 180], steps=5) >= 1
+
+
+def test_per_unit_budgets_sampled_with_log_prob():
+    assert _ragged_run([120, 700, 90], steps=4, gumbel=55, tau=0.8) >= 1
