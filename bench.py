@@ -417,6 +417,69 @@ def bench_paper_policy(args, wl, dev, log):
             "note": "paper-faithful state and policy; decode + separate scoring pass, timed apart"}
 
 
+def bench_hybrid(args, wl, dev, log):
+    """The appendix's head-level hybrid on a decode workload: a fraction of the
+    KV heads keeps its full cache, the others keep the workload's budget
+    (per-unit budgets on a ragged cache: chunked decode per unit, then the
+    per-unit selection), every step."""
+    import torch
+    from paper_2608_08878_amd.buffers import DecodeBuffers, make_policy
+    from synth import gpu as sg
+    from synth import workloads as W
+
+    U, G, D = wl.units, wl.group, wl.head_dim
+    nsteps = 1 + args.warmup + args.steps
+    cap = wl.n0 + nsteps
+    buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, D, cap, wl.dtype,
+                        wl.ent_window, ragged=True)
+    buf.reserve_workspace(cap)
+    sg.init_cache(wl, buf.k, buf.v, U, cap)
+    buf.feat_init(wl.n0, 0)
+    params = torch.empty(wl.n_params, dtype=torch.float32, device=dev)
+    sg.fill_normal(params, wl, W.S_POLICY, 0, 0.1)
+    pol = make_policy(params, wl.hidden)
+    # every k-th KV head of a layer keeps its full cache (k = 1 / fraction)
+    every = max(1, round(1.0 / args.hybrid))
+    full = np.array([(u % wl.n_kv_heads) % every == 0 for u in range(U)])
+    big = cap + 1
+    budgets = torch.tensor(np.where(full, big, wl.budget), dtype=torch.int32, device=dev)
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    q = torch.empty((U, G, D), dtype=td, device=dev)
+    kn = torch.empty((U, D), dtype=td, device=dev)
+    vn = torch.empty_like(kn)
+    out = torch.empty_like(q)
+    parts = {"decode": [], "evict": [], "step": []}
+    first_ms = None
+    for t in range(nsteps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        ev = _events(3)
+        ev[0].record()
+        buf.decode_step(q, kn, vn, out)
+        ev[1].record()
+        buf.score_evict_units(pol, budgets, big)
+        ev[2].record()
+        torch.cuda.synchronize()
+        if t == 0:
+            first_ms = ev[0].elapsed_time(ev[2])
+        elif t > args.warmup:
+            parts["decode"].append(ev[0].elapsed_time(ev[1]))
+            parts["evict"].append(ev[1].elapsed_time(ev[2]))
+            parts["step"].append(ev[0].elapsed_time(ev[2]))
+    m = {k: float(np.mean(v)) for k, v in parts.items()}
+    lens = buf.unit_len.cpu().numpy().astype(np.int64)
+    kvb = int(lens.sum()) * 2 * D * 2
+    return {"value": round(1e3 / m["step"], 3), "unit": "decode steps/s",
+            "ms_per_step": round(m["step"], 4), "decode_ms": round(m["decode"], 4),
+            "evict_ms": round(m["evict"], 4), "first_step_ms": round(first_ms, 3),
+            "full_cache_units": int(full.sum()), "rows_full": int(lens[full].max()),
+            "rows_budgeted": int(lens[~full].max()),
+            "kv_gbps": round(kvb / (m["step"] * 1e-3) / 1e9, 1),
+            "kv_frac_of_8TBps": round(kvb / (m["step"] * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+            "note": f"head-level hybrid: 1 of every {every} KV heads keeps its full cache, "
+                    "ragged cache (chunked decode + per-unit selection)"}
+
+
 LOGZ_OPS_PER_UPDATE = 7     # VALU instructions of one recursion update (see the design notes)
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # lane-instructions/s without packed math
 
@@ -470,6 +533,9 @@ def main():
     ap.add_argument("--policy", choices=["workload", "paper"], default="workload",
                     help="paper: five features (sigma included) and a 5->128->128->1 LayerNorm "
                          "MLP every step (workloads 2 and 3)")
+    ap.add_argument("--hybrid", type=float, default=0.0,
+                    help="fraction of KV heads that keep their full cache (head-level hybrid; "
+                         "per-unit budgets on a ragged cache), workloads 2 and 3")
     ap.add_argument("--train-select", action="store_true",
                     help="workload 5: the student keeps a Gumbel-sampled top-B and computes "
                          "log pi (training mode) instead of the deterministic selection")
@@ -505,10 +571,12 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
-    if args.config in (1, 4, 5) or args.policy == "paper":
+    if args.config in (1, 4, 5) or args.policy == "paper" or args.hybrid > 0:
         fn = {1: bench_single_step, 4: bench_periodic_evict, 5: bench_teacher_student_kl}.get(args.config)
         if args.policy == "paper":
             fn = bench_paper_policy
+        if args.hybrid > 0:
+            fn = bench_hybrid
         res = fn(args, wl, dev, log)
         result = {"metric": f"decode steps/s, workload {args.config}", "n_gpus": 1,
                   "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,

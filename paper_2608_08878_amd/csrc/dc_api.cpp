@@ -298,7 +298,8 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   const bool ragged = kv->unit_len != nullptr;
   if (ragged && dims->dtype != DC_BF16) return DC_ERR_UNSUPPORTED;
   // the compaction's move list (two ints per move) lives in LDS
-  const int moves = ragged ? (L - 1 < budget ? L - 1 : budget) : evict ? (L - budget < budget ? L - budget : budget) : 0;
+  // (per unit min(L_u - B_u, B_u) <= L_u / 2)
+  const int moves = ragged ? (L / 2 < budget ? L / 2 : budget) : evict ? (L - budget < budget ? L - budget : budget) : 0;
   if (moves > MAX_MOVES) return DC_ERR_UNSUPPORTED;
   need = (ext || ragged) ? align256(dc::evict_ext_ws_bytes((int)units_of(dims), L))
                          : (L > EVICT_REG_ROWS ? evict_bytes(dims, L) : 0);

@@ -142,9 +142,9 @@ template <int DTYPE, int D>
 static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) {
   const bool rg = a.unit_len || a.budgets;
   if (!a.evict && !rg && !a.scores_out && !a.kept_out) return 0;
-  // moves: min(L - B, B); per-unit budgets: bounded by min(L - 1, the largest budget)
+  // moves: min(L - B, B); per-unit budgets: at most min(L / 2, the largest budget)
   const int E = a.L - a.budget;
-  const int nmv = rg ? (a.L - 1 < a.budget ? a.L - 1 : a.budget) : a.evict ? (E < a.budget ? E : a.budget) : 0;
+  const int nmv = rg ? (a.L / 2 < a.budget ? a.L / 2 : a.budget) : a.evict ? (E < a.budget ? E : a.budget) : 0;
   EvictArgs b = a;
   b.mv_ints = (2 * (nmv > 0 ? nmv : 1) + 3) / 4 * 4;   // keeps the weights after it 16-byte aligned
   const size_t pbytes = a.nh == 2 ? (size_t)policy_floats(2, a.h1, a.h2) * sizeof(float) : 0;
