@@ -14,6 +14,8 @@
 //   the accumulators hold row 4 (l / 16) + i, column 16 cb + l % 16: LayerNorm
 //     moments, ReLU and the output dot product reduce over the 16 lanes of a
 //     DPP row.
+// 512-thread workgroups: the 78 KB of staged weights allow two per CU, so eight
+// waves share each copy (four per SIMD).
 // Padded units (k >= h1, n >= h2) are exact zeros and are left out of the
 // LayerNorm moments.
 #include <hip/hip_runtime.h>
@@ -27,18 +29,20 @@ namespace dc {
 
 namespace {
 
-constexpr int MT = 256;              // 4 waves
+constexpr int MT = 512;              // 8 waves share one staged copy of the weights
+constexpr int MW = MT / 64;
 constexpr int HP = 128;              // padded hidden width
 constexpr int W2S = HP + 16;         // LDS row stride of W2 (floats)
 constexpr int NX = 5;                // padded input width
 typedef float f32x4_v __attribute__((ext_vector_type(4)));
 
-// LDS layout (floats)
-constexpr int O_W2 = 0;                        // [HP][W2S]  W2 as [k][n]
-constexpr int O_B2 = O_W2 + HP * W2S;          // b2, g2, be2, wo   [HP] each
-constexpr int O_W1 = O_B2 + 4 * HP;            // [HP][NX]
+// LDS layout (floats); the small arrays first, so that every per-lane read of
+// them is a constant offset within the 64 KB reach of an LDS instruction
+constexpr int O_W1 = 0;                        // [NX][HP]  W1 transposed (unit-contiguous)
 constexpr int O_B1 = O_W1 + HP * NX;           // b1, g1, be1       [HP] each
-constexpr int LDS_FLOATS = O_B1 + 3 * HP;
+constexpr int O_B2 = O_B1 + 3 * HP;            // b2, g2, be2, wo   [HP] each
+constexpr int O_W2 = O_B2 + 4 * HP;            // [HP][W2S]  W2 as [k][n]
+constexpr int LDS_FLOATS = O_W2 + HP * W2S;
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
@@ -83,7 +87,7 @@ __device__ void stage(const EvictArgs& a, float* sm) {
     sm[O_B1 + HP + i] = v1 ? (ln ? g1[i] : 1.0f) : 0.0f;
     sm[O_B1 + 2 * HP + i] = v1 && ln ? be1[i] : 0.0f;
 #pragma unroll
-    for (int x = 0; x < NX; ++x) sm[O_W1 + i * NX + x] = (v1 && x < nin) ? W1[i * nin + x] : 0.0f;
+    for (int x = 0; x < NX; ++x) sm[O_W1 + x * HP + i] = (v1 && x < nin) ? W1[i * nin + x] : 0.0f;
   }
 }
 
@@ -100,7 +104,7 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
   const float invT = 1.0f / (float)a.T;
   const float bout = const_params(a.params)[h1 * a.n_in + h1 + (ln ? 2 * h1 : 0) + h2 * h1 + h2 +
                                             (ln ? 2 * h2 : 0) + h2];
-  for (int rb = (blockIdx.x * 4 + wave) * 16; rb < L; rb += gridDim.x * 64) {
+  for (int rb = (blockIdx.x * MW + wave) * 16; rb < L; rb += gridDim.x * MW * 16) {
     // features of this lane's A row (the four lanes of a row load the same row)
     const int r = rb + ri;
     const size_t gi = ub + (r < L ? r : L - 1);
@@ -123,16 +127,16 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
     }
     // layer 1: units k = 4 s + kg (the weights are re-read from LDS per row
     // block: held across blocks they would take 256 registers)
-    const float* p1 = sm;
-    asm volatile("" : "+v"(p1));
+    const lfloat* p1 = (const lfloat*)sm + kg;  // LDS, this lane's unit offset; all reads below
+    asm volatile("" : "+v"(p1));                // are constant offsets from it
     float h[32];
     float s1 = 0.0f;
 #pragma unroll
     for (int s = 0; s < 32; ++s) {
       const int k = 4 * s + kg;
-      float z = p1[O_B1 + k];
+      float z = p1[O_B1 + 4 * s];
 #pragma unroll
-      for (int i = 0; i < NX; ++i) z = __builtin_fmaf(p1[O_W1 + k * NX + i], x[i], z);
+      for (int i = 0; i < NX; ++i) z = __builtin_fmaf(p1[O_W1 + i * HP + 4 * s], x[i], z);
       h[s] = z;
       s1 += k < h1 ? z : 0.0f;
     }
@@ -148,7 +152,7 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
 #pragma unroll
       for (int s = 0; s < 32; ++s) {
         const int k = 4 * s + kg;
-        h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + k], p1[O_B1 + 2 * HP + k]);
+        h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + 4 * s], p1[O_B1 + 2 * HP + 4 * s]);
       }
     }
 #pragma unroll
@@ -157,13 +161,26 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
     f32x4_v acc[8];
 #pragma unroll
     for (int cb = 0; cb < 8; ++cb) acc[cb] = (f32x4_v){0.0f, 0.0f, 0.0f, 0.0f};
+    // B of step s + 1 is read while step s's MFMAs run (an opaque pointer per step
+    // keeps the reads from being hoisted further ahead: 256 values would not fit)
+    float bq[2][8];
+    {
+      const lfloat* br = (const lfloat*)sm + O_W2 + kg * W2S + ri;
+      asm volatile("" : "+v"(br));
+#pragma unroll
+      for (int cb = 0; cb < 8; ++cb) bq[0][cb] = br[16 * cb];
+    }
 #pragma unroll
     for (int s = 0; s < 32; ++s) {
-      const float* brow = sm + O_W2 + (4 * s + kg) * W2S + ri;
-      asm volatile("" : "+v"(brow));   // keeps each step's B reads in the step (no 256-value prefetch)
+      if (s + 1 < 32) {
+        const lfloat* br = (const lfloat*)sm + O_W2 + (4 * (s + 1) + kg) * W2S + ri;
+        asm volatile("" : "+v"(br));
+#pragma unroll
+        for (int cb = 0; cb < 8; ++cb) bq[(s + 1) & 1][cb] = br[16 * cb];
+      }
 #pragma unroll
       for (int cb = 0; cb < 8; ++cb)
-        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[s], brow[16 * cb], acc[cb], 0, 0, 0);
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[s], bq[s & 1][cb], acc[cb], 0, 0, 0);
     }
     // rows 4 kg + i of the block, columns 16 cb + ri
     float score[4];
@@ -218,7 +235,7 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
 size_t mlp2_lds_bytes() { return (size_t)LDS_FLOATS * sizeof(float); }
 
 int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* stream) {
-  const int nblk = (a.L + 63) / 64;
+  const int nblk = (a.L + MW * 16 - 1) / (MW * 16);
   const int gx = nblk < 8 ? nblk : 8;
   const size_t lds = mlp2_lds_bytes();
   hipFuncSetAttribute((const void*)score_mlp2_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
