@@ -134,11 +134,11 @@ typedef struct {
  * the layer's units (population variance), then h = relu(z); s = w_out . h + b_out.
  * Inputs: n_in = 4 takes [alpha, ||v||, H, pos/T]; n_in = 5 takes the paper's
  * [alpha, ||v||, sigma, H, pos/T] and needs dc_feat.sigma.
- * Supported: n_in in {4, 5}, n_hidden_layers in {1, 2}, hidden widths 1..128
- * (the first width at most 64 for a two-layer policy with n_in = 4 and no
- * layer_norm, whose weights are staged on chip).  Four-input policies without
- * layer_norm run inside the fused decode step; the others run in a separate
- * scoring pass. */
+ * Supported: n_in in {4, 5}, n_hidden_layers in {1, 2}, hidden widths 1..128.
+ * The four-input one-hidden-layer policy without layer_norm runs inside the
+ * fused decode step; every other policy runs in a separate scoring pass (two
+ * hidden layers on the matrix cores) that ranks through row keys in the
+ * workspace, so it needs dc_workspace_bytes scratch at any length. */
 typedef struct {
   int32_t n_in;
   int32_t n_hidden_layers;
@@ -193,8 +193,9 @@ dc_status dc_decode_step(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const vo
  *   kept_out    [units][min(budget, len)] int32: pre-eviction slot of the row
  *               that ends in each slot, or NULL.
  * Errors: DC_ERR_NULL, DC_ERR_BUDGET (budget < 1), DC_ERR_UNSUPPORTED (policy
- * shape, len > 40960), DC_ERR_SHAPE, DC_ERR_WORKSPACE (len > 8192 needs
- * dc_workspace_bytes scratch). */
+ * shape, len > 40960), DC_ERR_SHAPE, DC_ERR_WORKSPACE (dc_workspace_bytes
+ * scratch is needed for len > 8192, ragged caches and every policy but the
+ * four-input one-hidden-layer one without layer_norm). */
 dc_status dc_score_evict(const dc_dims *dims, dc_kv *kv, dc_feat *feat, const dc_policy *policy,
                          int32_t budget, float *scores_out, int32_t *kept_out, void *ws,
                          size_t ws_bytes, void *hip_stream);

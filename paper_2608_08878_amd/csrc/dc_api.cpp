@@ -285,10 +285,9 @@ dc_status prep_evict(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   if (policy->hidden[0] < 1 || policy->hidden[0] > 128) return DC_ERR_UNSUPPORTED;
   if (policy->n_hidden_layers == 2 && (policy->hidden[1] < 1 || policy->hidden[1] > 128))
     return DC_ERR_UNSUPPORTED;
-  // outside the fixed fast paths: a fifth input, LayerNorm, or a wide first layer
-  // of a two-layer policy run through the out-of-line MLP
-  const int ext = policy->n_in == 5 || policy->layer_norm ||
-                  (policy->n_hidden_layers == 2 && policy->hidden[0] > 64);
+  // outside the fused one-hidden-layer path: a fifth input, LayerNorm, or a
+  // second hidden layer (a dense contraction: the matrix-core scoring pass)
+  const int ext = policy->n_in == 5 || policy->layer_norm || policy->n_hidden_layers == 2;
   if (policy->n_in == 5 && !feat->sigma) return DC_ERR_NULL;
   if (budget < 1) return DC_ERR_BUDGET;
   if (L < 1 || L > dims->capacity) return DC_ERR_SHAPE;
@@ -473,7 +472,7 @@ dc_status dc_decode_sample_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat,
   const int G = group_of(dims), D = dims->head_dim;
   const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
   const bool fused = dims->dtype == DC_BF16 && !split && !e.ext && !feat->sigma && G >= 4 &&
-                     !kv->unit_len && dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
+                     !kv->unit_len && dc::step_fits(a.L, G, D, true, nm);
   if (fused) {
     if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
   } else {
@@ -574,7 +573,7 @@ dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   // the single-launch step serves four-input policies without LayerNorm and
   // does not produce sigma
   const bool fused = dims->dtype == DC_BF16 && !split && !e.ext && !feat->sigma &&
-                     dc::step_fits(a.L, G, D, true, nm, dc::policy_lds_bytes(e));
+                     dc::step_fits(a.L, G, D, true, nm);
   if (fused) {
     if (dc::launch_step(a, &e, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
   } else {

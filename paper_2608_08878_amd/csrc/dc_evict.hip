@@ -24,7 +24,7 @@
 namespace dc {
 
 // Caches up to ENT * REG_KPT rows: scores in registers, one workgroup per unit.
-template <int DTYPE, int D, int NH>
+template <int DTYPE, int D>
 __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
   extern __shared__ int dyn[];
   __shared__ SelShared sh;
@@ -33,12 +33,6 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
   const float invT = 1.0f / (float)a.T;
   const int L = a.L;
   const int kact = L > wave * 64 ? (L - wave * 64 + ENT - 1) / ENT : 0;
-  // two hidden layers: the weights go to LDS after the move list
-  float* pl = NH == 2 ? reinterpret_cast<float*>(dyn) + a.mv_ints : nullptr;
-  if constexpr (NH == 2) {
-    stage_params(a, pl);
-    __syncthreads();
-  }
   float x[REG_KPT][4];
   int32_t pk[REG_KPT];
 #pragma unroll
@@ -49,7 +43,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
     }
   }
   float sc[REG_KPT];
-  policy_scores<REG_KPT, NH>(a, x, sc, kact, pl);
+  policy_scores<REG_KPT>(a, x, sc, kact);
   RegKeys<REG_KPT> keys;
 #pragma unroll
   for (int k = 0; k < REG_KPT; ++k) {
@@ -69,13 +63,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
 }
 
 // Long caches: scores to keys in the workspace (grid over rows) ...
-template <int NH>
 __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys, int kstride) {
-  extern __shared__ float spl[];
-  if constexpr (NH == 2) {
-    stage_params(a, spl);
-    __syncthreads();
-  }
   const int u = blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
@@ -86,7 +74,7 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
     int32_t p;
     load_features(a, ub + (r < L ? r : L - 1), invT, x[0], p);
     float sc[1];
-    policy_scores<1, NH>(a, x, sc, 1, NH == 2 ? spl : nullptr);
+    policy_scores<1>(a, x, sc, 1);
     if (r < L) {
       if (a.scores_out) a.scores_out[(size_t)u * a.L + r] = sc[0];
       keys[(size_t)u * kstride + r] = row_key(a.sample ? sampled_score(a, sc[0], p, u) : sc[0], p);
@@ -94,7 +82,8 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
   }
 }
 
-// Extended policies: the same grid over rows, the out-of-line MLP per row.
+// Extended one-hidden-layer policies: the same grid over rows, the out-of-line
+// MLP per row.
 __global__ void __launch_bounds__(256) score_ext_kernel(EvictArgs a, uint64_t* keys, int kstride) {
   const int u = blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
@@ -146,62 +135,35 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
   const int E = a.L - a.budget;
   const int nmv = rg ? (a.L / 2 < a.budget ? a.L / 2 : a.budget) : a.evict ? (E < a.budget ? E : a.budget) : 0;
   EvictArgs b = a;
-  b.mv_ints = (2 * (nmv > 0 ? nmv : 1) + 3) / 4 * 4;   // keeps the weights after it 16-byte aligned
-  const size_t pbytes = a.nh == 2 ? (size_t)policy_floats(2, a.h1, a.h2) * sizeof(float) : 0;
+  b.mv_ints = (2 * (nmv > 0 ? nmv : 1) + 3) / 4 * 4;
   const size_t dyn = (size_t)b.mv_ints * sizeof(int);
   const int kstride = (a.L + ENT - 1) / ENT * ENT;
   const bool ragged = a.unit_len || a.budgets;
-  if (ragged && !a.ext) {
-    // per-unit lengths or budgets: scores to row keys, then one select per unit
-    // that decides for itself whether the unit evicts
-    int gx = (a.L + 255) / 256;
-    if (a.nh == 2) {
-      gx = gx < 16 ? gx : 16;
-      hipFuncSetAttribute((const void*)score_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pbytes);
-      hipLaunchKernelGGL(score_kernel<2>, dim3(gx, a.units), dim3(256), pbytes, s, b, ws_keys, kstride);
-    } else {
-      hipLaunchKernelGGL(score_kernel<1>, dim3(gx, a.units), dim3(256), 0, s, b, ws_keys, kstride);
-    }
+  if (!a.ext && !ragged && a.L <= ENT * REG_KPT) {
+    // the one-hidden-layer policy on a short cache: scores in registers
+    auto k = score_select_kernel<DTYPE, D>;
+    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
+    hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b);
+    return (int)hipGetLastError();
+  }
+  // scores to row keys in the workspace (grid over rows), then one select per
+  // unit (with per-unit lengths or budgets each unit decides whether it evicts)
+  if (a.ext && a.nh == 2) {
+    const int rc = launch_score_mlp2(b, ws_keys, kstride, s);
+    if (rc) return rc;
+  } else if (a.ext) {
+    hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
+                       ws_keys, kstride);
+  } else {
+    hipLaunchKernelGGL(score_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
+                       ws_keys, kstride);
+  }
+  if (a.evict || ragged) {
     auto k = select_kernel<DTYPE, D>;
     hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
     hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);
-  } else if (a.ext) {
-    if (a.nh == 2) {
-      const int rc = launch_score_mlp2(b, ws_keys, kstride, s);
-      if (rc) return rc;
-    } else {
-      hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
-                         ws_keys, kstride);
-    }
-    if (a.evict || ragged) {
-      auto k = select_kernel<DTYPE, D>;
-      hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-      hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);
-    } else if (a.kept_out) {
-      hipLaunchKernelGGL(identity_kept_kernel, dim3(1024), dim3(256), 0, s, a.kept_out, a.units, a.L);
-    }
-  } else if (a.L <= ENT * REG_KPT) {
-    auto k = a.nh == 2 ? score_select_kernel<DTYPE, D, 2> : score_select_kernel<DTYPE, D, 1>;
-    hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)(dyn + pbytes));
-    hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn + pbytes, s, b);
-  } else {
-    // two hidden layers: each workgroup stages the weights once and scores
-    // several row blocks with them
-    int gx = (a.L + 255) / 256;
-    if (a.nh == 2) {
-      gx = gx < 16 ? gx : 16;
-      hipFuncSetAttribute((const void*)score_kernel<2>, hipFuncAttributeMaxDynamicSharedMemorySize, (int)pbytes);
-      hipLaunchKernelGGL(score_kernel<2>, dim3(gx, a.units), dim3(256), pbytes, s, b, ws_keys, kstride);
-    } else {
-      hipLaunchKernelGGL(score_kernel<1>, dim3(gx, a.units), dim3(256), 0, s, b, ws_keys, kstride);
-    }
-    if (a.evict) {
-      auto k = select_kernel<DTYPE, D>;
-      hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-      hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b, (const uint64_t*)ws_keys, kstride);
-    } else if (a.kept_out) {
-      hipLaunchKernelGGL(identity_kept_kernel, dim3(1024), dim3(256), 0, s, a.kept_out, a.units, a.L);
-    }
+  } else if (a.kept_out) {
+    hipLaunchKernelGGL(identity_kept_kernel, dim3(1024), dim3(256), 0, s, a.kept_out, a.units, a.L);
   }
   return (int)hipGetLastError();
 }

@@ -141,8 +141,7 @@ int launch_kl(const KLArgs& a, void* stream);
 // bf16 matrix-core step (dc_step.hip); e != nullptr fuses scoring and eviction.
 int launch_step(const DecodeArgs& a, const EvictArgs* e, int D, int G, bool feat, bool chunked,
                 void* stream);
-bool step_fits(int L, int G, int D, bool feat, int nmoves, size_t extra_lds = 0);
-size_t policy_lds_bytes(const EvictArgs& e);   // LDS of the two-hidden-layer policy's weights
+bool step_fits(int L, int G, int D, bool feat, int nmoves);
 int step_chunk_rows();
 int kl_tile_cols();
 

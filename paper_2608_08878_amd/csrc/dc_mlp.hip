@@ -1,21 +1,22 @@
 // Two-hidden-layer policy on matrix cores (Sec. 3.1.2 scoring with the App. D
 // network: n_in -> h1 -> h2 -> 1, optional LayerNorm, widths up to 128), gfx950.
 //
-// Scoring every cached row with a 128 x 128 hidden layer is a dense
+// Scoring every cached row with a wide second hidden layer is a dense
 // contraction, [rows x h1] x [h1 x h2], so it runs on v_mfma_f32_16x16x4_f32
 // (float32 operands and accumulation: the same precision as the scalar path).
-// One wave takes 16 rows at a time:
+// The hidden widths are padded to HP = 64 (both at most 64) or 128.  One wave
+// takes 16 rows at a time:
 //   layer 1 (VALU): lane l computes, for row l % 16, the units k = 4 s + l / 16
-//     (s < 32) -- exactly the A operand MFMA step s needs from that lane --
+//     (s < HP / 4) -- exactly the A operand MFMA step s needs from that lane --
 //     with LayerNorm moments reduced over the four lanes that share the row;
-//   layer 2 (MFMA): 8 column blocks x 32 k-steps; B comes from W2 staged in
-//     LDS as [k][n] with a row stride of 144 floats (the four k rows one
-//     instruction reads fall in different bank halves);
+//   layer 2 (MFMA): HP / 16 column blocks x HP / 4 k-steps; B comes from W2
+//     staged in LDS as [k][n] with a row stride of HP + 16 floats (the four k
+//     rows one instruction reads fall in different bank quarters);
 //   the accumulators hold row 4 (l / 16) + i, column 16 cb + l % 16: LayerNorm
 //     moments, ReLU and the output dot product reduce over the 16 lanes of a
 //     DPP row.
-// 512-thread workgroups: the 78 KB of staged weights allow two per CU, so eight
-// waves share each copy (four per SIMD).
+// 512-thread workgroups: at HP = 128 the 78 KB of staged weights allow two per
+// CU, so eight waves share each copy (four per SIMD); at HP = 64 (23 KB) three.
 // Padded units (k >= h1, n >= h2) are exact zeros and are left out of the
 // LayerNorm moments.
 #include <hip/hip_runtime.h>
@@ -31,18 +32,21 @@ namespace {
 
 constexpr int MT = 512;              // 8 waves share one staged copy of the weights
 constexpr int MW = MT / 64;
-constexpr int HP = 128;              // padded hidden width
-constexpr int W2S = HP + 16;         // LDS row stride of W2 (floats)
 constexpr int NX = 5;                // padded input width
 typedef float f32x4_v __attribute__((ext_vector_type(4)));
 
-// LDS layout (floats); the small arrays first, so that every per-lane read of
-// them is a constant offset within the 64 KB reach of an LDS instruction
-constexpr int O_W1 = 0;                        // [NX][HP]  W1 transposed (unit-contiguous)
-constexpr int O_B1 = O_W1 + HP * NX;           // b1, g1, be1       [HP] each
-constexpr int O_B2 = O_B1 + 3 * HP;            // b2, g2, be2, wo   [HP] each
-constexpr int O_W2 = O_B2 + 4 * HP;            // [HP][W2S]  W2 as [k][n]
-constexpr int LDS_FLOATS = O_W2 + HP * W2S;
+// LDS layout (floats) for hidden widths padded to HP (64 or 128); the small
+// arrays first, so that every per-lane read of them is a constant offset within
+// the 64 KB reach of an LDS instruction
+template <int HP>
+struct Lay {
+  static constexpr int W2S = HP + 16;                 // row stride of W2
+  static constexpr int O_W1 = 0;                      // [NX][HP]  W1 transposed (unit-contiguous)
+  static constexpr int O_B1 = O_W1 + HP * NX;         // b1, g1, be1       [HP] each
+  static constexpr int O_B2 = O_B1 + 3 * HP;          // b2, g2, be2, wo   [HP] each
+  static constexpr int O_W2 = O_B2 + 4 * HP;          // [HP][W2S]  W2 as [k][n]
+  static constexpr int FLOATS = O_W2 + HP * W2S;
+};
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
@@ -61,7 +65,10 @@ __device__ __forceinline__ float sum4rows(float x) {  // over lanes l, l^16, l^3
   return x;
 }
 
+template <int HP>
 __device__ void stage(const EvictArgs& a, float* sm) {
+  using Y = Lay<HP>;
+  constexpr int W2S = Y::W2S, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2, O_W2 = Y::O_W2;
   const cfloat* P = const_params(a.params);
   const int h1 = a.h1, h2 = a.h2, nin = a.n_in, ln = a.ln;
   const cfloat* W1 = P;
@@ -91,9 +98,14 @@ __device__ void stage(const EvictArgs& a, float* sm) {
   }
 }
 
-__global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
+template <int HP, int MINB>
+__global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
+  using Y = Lay<HP>;
+  constexpr int W2S = Y::W2S, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2, O_W2 = Y::O_W2;
+  constexpr int NS = HP / 4;     // MFMA k-steps (4 units each)
+  constexpr int NC = HP / 16;    // 16-column blocks of layer 2
   extern __shared__ float sm[];
-  stage(a, sm);
+  stage<HP>(a, sm);
   __syncthreads();
   const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ri = lane & 15, kg = lane >> 4;
@@ -129,10 +141,10 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
     // block: held across blocks they would take 256 registers)
     const lfloat* p1 = (const lfloat*)sm + kg;  // LDS, this lane's unit offset; all reads below
     asm volatile("" : "+v"(p1));                // are constant offsets from it
-    float h[32];
+    float h[NS];
     float s1 = 0.0f;
 #pragma unroll
-    for (int s = 0; s < 32; ++s) {
+    for (int s = 0; s < NS; ++s) {
       const int k = 4 * s + kg;
       float z = p1[O_B1 + 4 * s];
 #pragma unroll
@@ -144,52 +156,52 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
       const float mean = sum4rows(s1) / fh1;
       float s2 = 0.0f;
 #pragma unroll
-      for (int s = 0; s < 32; ++s) {
+      for (int s = 0; s < NS; ++s) {
         const float d = h[s] - mean;
         s2 += (4 * s + kg) < h1 ? d * d : 0.0f;
       }
       const float rs = 1.0f / __builtin_sqrtf(sum4rows(s2) / fh1 + LN_EPS);
 #pragma unroll
-      for (int s = 0; s < 32; ++s) {
+      for (int s = 0; s < NS; ++s) {
         const int k = 4 * s + kg;
         h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + 4 * s], p1[O_B1 + 2 * HP + 4 * s]);
       }
     }
 #pragma unroll
-    for (int s = 0; s < 32; ++s) h[s] = (4 * s + kg) < h1 ? fmaxf(h[s], 0.0f) : 0.0f;
+    for (int s = 0; s < NS; ++s) h[s] = (4 * s + kg) < h1 ? fmaxf(h[s], 0.0f) : 0.0f;
     // layer 2 on MFMA
-    f32x4_v acc[8];
+    f32x4_v acc[NC];
 #pragma unroll
-    for (int cb = 0; cb < 8; ++cb) acc[cb] = (f32x4_v){0.0f, 0.0f, 0.0f, 0.0f};
+    for (int cb = 0; cb < NC; ++cb) acc[cb] = (f32x4_v){0.0f, 0.0f, 0.0f, 0.0f};
     // B of step s + 1 is read while step s's MFMAs run (an opaque pointer per step
-    // keeps the reads from being hoisted further ahead: 256 values would not fit)
-    float bq[2][8];
+    // keeps the reads from being hoisted further ahead: the whole of W2 would not fit)
+    float bq[2][NC];
     {
       const lfloat* br = (const lfloat*)sm + O_W2 + kg * W2S + ri;
       asm volatile("" : "+v"(br));
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) bq[0][cb] = br[16 * cb];
+      for (int cb = 0; cb < NC; ++cb) bq[0][cb] = br[16 * cb];
     }
 #pragma unroll
-    for (int s = 0; s < 32; ++s) {
-      if (s + 1 < 32) {
+    for (int s = 0; s < NS; ++s) {
+      if (s + 1 < NS) {
         const lfloat* br = (const lfloat*)sm + O_W2 + (4 * (s + 1) + kg) * W2S + ri;
         asm volatile("" : "+v"(br));
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb) bq[(s + 1) & 1][cb] = br[16 * cb];
+        for (int cb = 0; cb < NC; ++cb) bq[(s + 1) & 1][cb] = br[16 * cb];
       }
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb)
+      for (int cb = 0; cb < NC; ++cb)
         acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[s], bq[s & 1][cb], acc[cb], 0, 0, 0);
     }
     // rows 4 kg + i of the block, columns 16 cb + ri
     float score[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float z[8];
+      float z[NC];
       float t1 = 0.0f;
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) {
+      for (int cb = 0; cb < NC; ++cb) {
         const int n = 16 * cb + ri;
         z[cb] = acc[cb][i] + sm[O_B2 + n];
         t1 += n < h2 ? z[cb] : 0.0f;
@@ -199,7 +211,7 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
         mean = sum16(t1) / fh2;
         float t2 = 0.0f;
 #pragma unroll
-        for (int cb = 0; cb < 8; ++cb) {
+        for (int cb = 0; cb < NC; ++cb) {
           const float d = z[cb] - mean;
           t2 += (16 * cb + ri) < h2 ? d * d : 0.0f;
         }
@@ -207,7 +219,7 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
       }
       float o = 0.0f;
 #pragma unroll
-      for (int cb = 0; cb < 8; ++cb) {
+      for (int cb = 0; cb < NC; ++cb) {
         const int n = 16 * cb + ri;
         float y = ln ? __builtin_fmaf((z[cb] - mean) * rs, sm[O_B2 + HP + n], sm[O_B2 + 2 * HP + n])
                      : z[cb];
@@ -232,16 +244,22 @@ __global__ void __launch_bounds__(MT, 2) score_mlp2_kernel(EvictArgs a, uint64_t
 
 }  // namespace
 
-size_t mlp2_lds_bytes() { return (size_t)LDS_FLOATS * sizeof(float); }
+size_t mlp2_lds_bytes() { return (size_t)Lay<128>::FLOATS * sizeof(float); }
 
 int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* stream) {
   const int nblk = (a.L + MW * 16 - 1) / (MW * 16);
   const int gx = nblk < 8 ? nblk : 8;
-  const size_t lds = mlp2_lds_bytes();
-  hipFuncSetAttribute((const void*)score_mlp2_kernel, hipFuncAttributeMaxDynamicSharedMemorySize,
-                      (int)lds);
-  hipLaunchKernelGGL(score_mlp2_kernel, dim3(gx, a.units), dim3(MT), lds, (hipStream_t)stream, a,
-                     keys, kstride);
+  // hidden widths up to 64 pad to 64: a quarter of the layer-2 work of 128
+  const bool narrow = a.h1 <= 64 && a.h2 <= 64;
+  const void* k = narrow ? (const void*)score_mlp2_kernel<64, 3> : (const void*)score_mlp2_kernel<128, 2>;
+  const size_t lds = (size_t)(narrow ? Lay<64>::FLOATS : Lay<128>::FLOATS) * sizeof(float);
+  hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (narrow)
+    hipLaunchKernelGGL((score_mlp2_kernel<64, 3>), dim3(gx, a.units), dim3(MT), lds,
+                       (hipStream_t)stream, a, keys, kstride);
+  else
+    hipLaunchKernelGGL((score_mlp2_kernel<128, 2>), dim3(gx, a.units), dim3(MT), lds,
+                       (hipStream_t)stream, a, keys, kstride);
   return (int)hipGetLastError();
 }
 

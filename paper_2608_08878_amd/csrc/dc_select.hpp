@@ -10,7 +10,6 @@ constexpr int ENT = 1024;            // threads of the stand-alone select workgr
 constexpr int ENW_MAX = 16;          // waves per workgroup, at most
 constexpr int REG_KPT = 8;           // rows per thread kept in registers (L <= 8192)
 constexpr int MAX_LEN = 40960;
-constexpr int MAX_H1_2L = 64;        // first hidden width supported with two hidden layers
 
 __device__ __forceinline__ uint32_t score_key(float s) {
   uint32_t b = __float_as_uint(s);
@@ -92,21 +91,20 @@ __device__ __forceinline__ const cfloat* const_params(const float* p) {
   return (const cfloat*)p;
 }
 
-// Extended policy (any of: a fifth input sigma_i, LayerNorm, widths up to 128
-// for two layers): x has n_in inputs in the paper's order, each hidden layer is
-// z = W h + b, [z = gain (z - mean) / sqrt(var + 1e-5) + bias over the layer],
-// h = relu(z); s = w_out . h + b_out.  Float32 with fixed evaluation order
-// (bias first, inputs / units in order); LayerNorm moments accumulated in
-// binary64.  The first hidden layer lives in registers (128 slots); the second
-// is evaluated one unit at a time, twice with LayerNorm (moments, then values).
-// Out of line: its 128-register hidden vector must not share the caller's
-// register budget.
+// Extended one-hidden-layer policy (a fifth input sigma_i and/or LayerNorm,
+// width up to 128): x has n_in inputs in the paper's order; z = W x + b,
+// [z = gain (z - mean) / sqrt(var + 1e-5) + bias over the layer], h = relu(z);
+// s = w_out . h + b_out.  Float32 with fixed evaluation order (bias first,
+// inputs / units in order); LayerNorm moments accumulated in binary64.  The
+// hidden layer lives in registers (128 slots); out of line so that they do not
+// share the caller's register budget.  (Two hidden layers run on the matrix
+// cores: dc_mlp.hip.)
 constexpr int EXT_HMAX = 128;
 constexpr float LN_EPS = 1e-5f;
 
-__device__ __attribute__((noinline)) float mlp_ext(const float* params, int n_in, int nh, int h1,
-                                                   int h2, int ln, float x0, float x1, float x2,
-                                                   float x3, float x4) {
+__device__ __attribute__((noinline)) float mlp_ext(const float* params, int n_in, int h1, int ln,
+                                                   float x0, float x1, float x2, float x3,
+                                                   float x4) {
   const cfloat* W = const_params(params);
   const cfloat* b = W + h1 * n_in;
   const float xin[5] = {x0, x1, x2, x3, x4};
@@ -140,50 +138,11 @@ __device__ __attribute__((noinline)) float mlp_ext(const float* params, int n_in
   }
 #pragma unroll
   for (int i = 0; i < EXT_HMAX; ++i) h[i] = fmaxf(h[i], 0.0f);
-  if (nh == 1) {
-    const cfloat* wo = next;
-    float out = wo[h1];
-#pragma unroll
-    for (int i = 0; i < EXT_HMAX; ++i)
-      if (i < h1) out = __builtin_fmaf(wo[i], h[i], out);
-    return out;
-  }
-  const cfloat* W2 = next;
-  const cfloat* b2 = W2 + h2 * h1;
-  next = b2 + h2;
-  const cfloat* g2 = next;
-  const cfloat* be2 = next + h2;
-  if (ln) next += 2 * h2;
   const cfloat* wo = next;
-  auto unit = [&](int o) {
-    const cfloat* w = W2 + o * h1;
-    float z = b2[o];
+  float out = wo[h1];
 #pragma unroll
-    for (int i = 0; i < EXT_HMAX; ++i)
-      if (i < h1) z = __builtin_fmaf(w[i], h[i], z);
-    return z;
-  };
-  float m2 = 0.0f, rs2 = 1.0f;
-  if (ln) {
-    double t1 = 0.0, t2 = 0.0;
-#pragma unroll 1
-    for (int o = 0; o < h2; ++o) {
-      const float z = unit(o);
-      t1 += (double)z;
-      t2 += (double)z * (double)z;
-    }
-    const double mean = t1 / h2;
-    const double var = t2 / h2 - mean * mean;
-    m2 = (float)mean;
-    rs2 = (float)(1.0 / sqrt((var > 0.0 ? var : 0.0) + (double)LN_EPS));
-  }
-  float out = wo[h2];
-#pragma unroll 1
-  for (int o = 0; o < h2; ++o) {
-    float z = unit(o);
-    if (ln) z = __builtin_fmaf((z - m2) * rs2, g2[o], be2[o]);
-    out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
-  }
+  for (int i = 0; i < EXT_HMAX; ++i)
+    if (i < h1) out = __builtin_fmaf(wo[i], h[i], out);
   return out;
 }
 
@@ -195,110 +154,13 @@ __device__ __forceinline__ float ext_score(const EvictArgs& a, size_t gi, float 
   const float H = den > 0.0 ? (float)(num / den) : 0.0f;
   const float al = a.alpha[gi], vn = a.vnorm[gi], ps = (float)p * invT;
   if (a.n_in == 5)
-    return mlp_ext(a.params, 5, a.nh, a.h1, a.h2, a.ln, al, vn, a.sigma[gi], H, ps);
-  return mlp_ext(a.params, 4, a.nh, a.h1, a.h2, a.ln, al, vn, H, ps, 0.0f);
+    return mlp_ext(a.params, 5, a.h1, a.ln, al, vn, a.sigma[gi], H, ps);
+  return mlp_ext(a.params, 4, a.h1, a.ln, al, vn, H, ps, 0.0f);
 }
 
-// Floats of the packed policy blob (W1, b1, [W2, b2,] w_out, b_out).
-__host__ __device__ inline int policy_floats(int nh, int h1, int h2) {
-  return nh == 1 ? 4 * h1 + h1 + h1 + 1 : 4 * h1 + h1 + h2 * h1 + h2 + h2 + 1;
-}
-
-// Copy the policy blob to LDS (block-cooperative; a barrier must follow before
-// any thread reads it).
-__device__ __forceinline__ void stage_params(const EvictArgs& a, float* dst) {
-  const int n = policy_floats(a.nh, a.h1, a.h2);
-  for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = a.params[i];
-}
-
-// s = f_phi(x) for a 4 -> h1 -> h2 -> 1 ReLU MLP (two hidden layers), float32,
-// fixed evaluation order (bias first, then the inputs in order; output units
-// in order), with the weights in LDS (every lane reads the same address:
-// broadcast reads).
+// Policy weights staged in LDS are read through LDS-typed pointers, so the
+// reads stay ds_read instructions even behind an optimisation barrier.
 typedef __attribute__((address_space(3))) const float lfloat;
-typedef float f32x4v __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) const f32x4v lfloat4;
-
-// The 64 x 64 shape: no width tests.  The LDS pointer is made opaque on entry
-// so that the weight reads stay inside the caller's loops (hoisted out, the
-// first layer's 320 weights would occupy 320 registers).
-__device__ __forceinline__ float mlp2_lds_64(const float* params, const float x[4]) {
-  constexpr int H = MAX_H1_2L;
-  const lfloat* P = (const lfloat*)params;
-  asm volatile("" : "+v"(P));
-  const lfloat* W1 = P;
-  const lfloat* b1 = P + 4 * H;
-  const lfloat* W2 = b1 + H;
-  const lfloat* b2 = W2 + H * H;
-  const lfloat* wo = b2 + H;
-  float hv[H];
-#pragma unroll
-  for (int h = 0; h < H; ++h) {
-    const f32x4v w = *reinterpret_cast<const lfloat4*>(W1 + 4 * h);
-    float z = b1[h];
-    z = __builtin_fmaf(w.x, x[0], z);
-    z = __builtin_fmaf(w.y, x[1], z);
-    z = __builtin_fmaf(w.z, x[2], z);
-    z = __builtin_fmaf(w.w, x[3], z);
-    hv[h] = fmaxf(z, 0.0f);
-  }
-  float out = wo[H];
-#pragma unroll 1
-  for (int o = 0; o < H; ++o) {
-    const lfloat4* w = reinterpret_cast<const lfloat4*>(W2 + o * H);
-    float z = b2[o];
-#pragma unroll
-    for (int q = 0; q < H / 4; ++q) {
-      const f32x4v w4 = w[q];
-      z = __builtin_fmaf(w4.x, hv[4 * q + 0], z);
-      z = __builtin_fmaf(w4.y, hv[4 * q + 1], z);
-      z = __builtin_fmaf(w4.z, hv[4 * q + 2], z);
-      z = __builtin_fmaf(w4.w, hv[4 * q + 3], z);
-    }
-    out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
-  }
-  return out;
-}
-
-// Any widths up to 64 (kept out of line: its per-width tests would otherwise
-// share registers with the fixed-shape code).
-__device__ __attribute__((noinline)) float mlp2_lds_any(const float* params, int h1, int h2,
-                                                         float x0, float x1, float x2, float x3) {
-  const lfloat* P = (const lfloat*)params;
-  const lfloat* W1 = P;
-  const lfloat* b1 = P + 4 * h1;
-  const lfloat* W2 = b1 + h1;
-  const lfloat* b2 = W2 + h2 * h1;
-  const lfloat* wo = b2 + h2;
-  float hv[MAX_H1_2L];
-#pragma unroll
-  for (int h = 0; h < MAX_H1_2L; ++h) {
-    float z = 0.0f;
-    if (h < h1) {
-      z = b1[h];
-      z = __builtin_fmaf(W1[4 * h + 0], x0, z);
-      z = __builtin_fmaf(W1[4 * h + 1], x1, z);
-      z = __builtin_fmaf(W1[4 * h + 2], x2, z);
-      z = __builtin_fmaf(W1[4 * h + 3], x3, z);
-    }
-    hv[h] = fmaxf(z, 0.0f);
-  }
-  float out = wo[h2];
-  for (int o = 0; o < h2; ++o) {
-    const lfloat* w = W2 + o * h1;
-    float z = b2[o];
-#pragma unroll
-    for (int h = 0; h < MAX_H1_2L; ++h)
-      if (h < h1) z = __builtin_fmaf(w[h], hv[h], z);
-    out = __builtin_fmaf(wo[o], fmaxf(z, 0.0f), out);
-  }
-  return out;
-}
-
-__device__ __forceinline__ float mlp2_lds(const float* params, int h1, int h2, const float x[4]) {
-  if (h1 == MAX_H1_2L && h2 == MAX_H1_2L) return mlp2_lds_64(params, x);
-  return mlp2_lds_any(params, h1, h2, x[0], x[1], x[2], x[3]);
-}
 
 // One hidden unit of the one-hidden-layer MLP for KP rows.
 template <int KP>
@@ -320,37 +182,30 @@ __device__ __forceinline__ void mlp1_unit(const cfloat* W1, const cfloat* b1, co
   }
 }
 
-// Scores of KP rows per thread, s = f_phi(x) in float32 with a fixed evaluation
-// order: out = b_out, then for every hidden unit h in order
-// out += w_out[h] relu(b1[h] + W1[h,0] x0 + W1[h,1] x1 + W1[h,2] x2 + W1[h,3] x3)
-// (for two hidden layers see mlp2_lds).  Row slots k >= kact (uniform over the
-// wave) are skipped.  The loops over the hidden units are uniform, so every
-// weight is read once per wave and reused for all row slots.
-template <int KP, int NH>
+// Scores of KP rows per thread, s = f_phi(x) for the one-hidden-layer policy
+// in float32 with a fixed evaluation order: out = b_out, then for every hidden
+// unit h in order
+// out += w_out[h] relu(b1[h] + W1[h,0] x0 + W1[h,1] x1 + W1[h,2] x2 + W1[h,3] x3).
+// Row slots k >= kact (uniform over the wave) are skipped.  The loops over the
+// hidden units are uniform, so every weight is read once per wave and reused
+// for all row slots.
+template <int KP>
 __device__ __forceinline__ void policy_scores(const EvictArgs& a, const float (&x)[KP][4],
-                                              float (&out)[KP], int kact,
-                                              const float* lds_params = nullptr) {
+                                              float (&out)[KP], int kact) {
   const cfloat* P = const_params(a.params);
-  if constexpr (NH == 1) {
-    const int h1 = a.h1;
-    const cfloat* W1 = P;
-    const cfloat* b1 = P + 4 * h1;
-    const cfloat* wo = b1 + h1;
-    const float bo = wo[h1];
+  const int h1 = a.h1;
+  const cfloat* W1 = P;
+  const cfloat* b1 = P + 4 * h1;
+  const cfloat* wo = b1 + h1;
+  const float bo = wo[h1];
 #pragma unroll
-    for (int k = 0; k < KP; ++k) out[k] = bo;
-    int h = 0;
-    for (; h + 4 <= h1; h += 4) {       // four units per trip: the scalar loads batch up
+  for (int k = 0; k < KP; ++k) out[k] = bo;
+  int h = 0;
+  for (; h + 4 <= h1; h += 4) {       // four units per trip: the scalar loads batch up
 #pragma unroll
-      for (int q = 0; q < 4; ++q) mlp1_unit<KP>(W1, b1, wo, h + q, x, out, kact);
-    }
-    for (; h < h1; ++h) mlp1_unit<KP>(W1, b1, wo, h, x, out, kact);
-  } else {
-    // two hidden layers: the caller staged the weights in LDS (stage_params)
-#pragma unroll
-    for (int k = 0; k < KP; ++k)
-      if (k < kact) out[k] = mlp2_lds(lds_params, a.h1, a.h2, x[k]);
+    for (int q = 0; q < 4; ++q) mlp1_unit<KP>(W1, b1, wo, h + q, x, out, kact);
   }
+  for (; h < h1; ++h) mlp1_unit<KP>(W1, b1, wo, h, x, out, kact);
 }
 
 // ---------------------------------------------------------------- key sources

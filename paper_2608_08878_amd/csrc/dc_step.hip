@@ -518,8 +518,8 @@ struct RowStride {
 
 // SMP: training-mode ranking by the Gumbel-perturbed score; the unperturbed
 // score is kept in the row's LDS slot beside its key (needs RS >= 4, G >= 4).
-template <int D, int G, bool FEAT, bool EVICT, int NH, bool SIG = false, bool SMP = false>
-__global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_kernel(DecodeArgs a, EvictArgs e) {
+template <int D, int G, bool FEAT, bool EVICT, bool SIG = false, bool SMP = false>
+__global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArgs a, EvictArgs e) {
   static_assert(!SIG || (FEAT && !EVICT), "sigma is stored by the decode-only variant");
   static_assert(!SMP || (EVICT && RowStride<G>::RS >= 4), "sampling keeps the score beside the key");
   constexpr int LPR = MG<D>::LPR;
@@ -533,9 +533,6 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
   float* sbuf = lds;                                  // row stride RS
   float* obuf = lds + (size_t)L * RS;                 // (SNW / 2) * G * D
   int* mv = (int*)(obuf + (SNW / 2) * G * D);
-  // two hidden layers: the policy weights sit in LDS after the move list
-  float* pl = (EVICT && NH == 2) ? reinterpret_cast<float*>(mv + e.mv_ints) : nullptr;
-  if constexpr (EVICT && NH == 2) stage_params(e, pl);     // read after the barriers below
   const size_t ub = (size_t)u * a.cap;
 
   if (a.append) append_rows<D>(a, u);
@@ -663,7 +660,7 @@ __global__ void __launch_bounds__(SNT, (NH == 2 || G > 4) ? 2 : 4) step_unit_ker
       if constexpr (EVICT) {
         float f[1][4], sc[1];
         make_features(al, vn, nu, de, ps, invT, f[0]);
-        policy_scores<1, NH>(e, f, sc, 1, pl);
+        policy_scores<1>(e, f, sc, 1);
         if constexpr (SMP) {
           const float ks = sampled_score(e, sc[0], ps, u);
           if (!guard || valid) {
@@ -902,13 +899,8 @@ size_t step_lds_bytes(int L, int G, int D, bool feat, int nmoves) {
   return b + (size_t)move_list_ints(nmoves) * sizeof(int);
 }
 
-size_t policy_lds_bytes(const EvictArgs& e) {
-  return e.nh == 2 ? (size_t)policy_floats(2, e.h1, e.h2) * sizeof(float) : 0;
-}
-
-bool step_fits(int L, int G, int D, bool feat, int nmoves, size_t extra_lds) {
-  return (!feat || L <= S_KMAX * SNT) &&
-         step_lds_bytes(L, G, D, feat, nmoves) + extra_lds <= (size_t)S_LDS;
+bool step_fits(int L, int G, int D, bool feat, int nmoves) {
+  return (!feat || L <= S_KMAX * SNT) && step_lds_bytes(L, G, D, feat, nmoves) <= (size_t)S_LDS;
 }
 
 int step_chunk_rows() { return SCHUNK; }
@@ -922,24 +914,20 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
     if (e) ee = *e;
     else __builtin_memset(&ee, 0, sizeof(ee));
     ee.mv_ints = move_list_ints(nm);
-    const size_t lds = step_lds_bytes(a.L, G, D, feat, nm) + (e ? policy_lds_bytes(*e) : 0);
+    const size_t lds = step_lds_bytes(a.L, G, D, feat, nm);
     auto pick = [&](auto kern) {
       hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
       hipLaunchKernelGGL(kern, dim3(a.units), dim3(SNT), lds, s, a, ee);
     };
-    if (!feat) pick(step_unit_kernel<D, G, false, false, 1>);
+    // (the fused evicting variants serve the one-hidden-layer four-input policy)
+    if (!feat) pick(step_unit_kernel<D, G, false, false>);
     else if (e && e->sample) {
-      if constexpr (RowStride<G>::RS >= 4) {
-        if (e->nh == 2) pick(step_unit_kernel<D, G, true, true, 2, false, true>);
-        else pick(step_unit_kernel<D, G, true, true, 1, false, true>);
-      } else {
-        return (int)hipErrorInvalidValue;     // the caller takes the separate path
-      }
+      if constexpr (RowStride<G>::RS >= 4) pick(step_unit_kernel<D, G, true, true, false, true>);
+      else return (int)hipErrorInvalidValue;     // the caller takes the separate path
     }
-    else if (e && e->nh == 2) pick(step_unit_kernel<D, G, true, true, 2>);
-    else if (e) pick(step_unit_kernel<D, G, true, true, 1>);
-    else if (a.sigma) pick(step_unit_kernel<D, G, true, false, 1, true>);
-    else pick(step_unit_kernel<D, G, true, false, 1>);
+    else if (e) pick(step_unit_kernel<D, G, true, true>);
+    else if (a.sigma) pick(step_unit_kernel<D, G, true, false, true>);
+    else pick(step_unit_kernel<D, G, true, false>);
   } else {
     dim3 grid(a.nchunks, a.units);
     if (feat) hipLaunchKernelGGL((stepc_a_kernel<D, G, true>), grid, dim3(SNT), 0, s, a);
