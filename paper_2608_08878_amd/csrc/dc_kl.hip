@@ -200,6 +200,179 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   }
 }
 
+// Many rows (a rollout's deferred rewards): a blocked GEMM.  A workgroup of 4
+// waves computes a 128 x NT block of logits -- 64 kl rows, full and compressed
+// interleaved per 16 (rows 8 b .. 8 b + 7 full, then the same rows compressed)
+// -- against NT = 2 TW vocabulary columns, over the hidden dimension in stages
+// of 64 elements staged in LDS (row stride 144 bytes: the 16 rows one fragment
+// read touches start 16 bytes apart in the banks).  The global loads of the
+// next PF stages are in flight in registers while the current stage feeds the
+// matrix cores.  Wave (wm, wn) owns rows 64 wm.. x columns TW wn.. (4 x TW/16
+// MFMA 16x16x32 bf16 blocks).  The epilogue forms the same per (row, 64-column
+// tile) statistics as kl_tile_kernel, for kl_merge_kernel.  Workgroup g runs on
+// XCD g mod 8; the row blocks of one vocabulary block are consecutive on one
+// XCD, so its lm-head slab comes from HBM once and then from that XCD's L2.
+// Two shapes: TW = 64 with two stages in flight (twice the workgroups: the
+// better one up to a few hundred rows, where parallelism and latency decide)
+// and TW = 128 with one (more work per staged byte, for many rows).
+constexpr int KG_M = 128;                       // logit rows per workgroup (64 kl rows)
+constexpr int KG_BK = 64;                       // hidden elements per stage
+constexpr int KG_RS = KG_BK * 2 + 16;           // LDS row stride (bytes)
+constexpr int KG_MIN_ROWS = 16;                 // fewer rows: kl_tile_kernel
+constexpr int KG_WIDE_ROWS = 256;               // from here on the TW = 128 shape
+
+template <int TW>
+constexpr int kg_lds() { return (KG_M + 2 * TW) * KG_RS; }
+
+template <int TW, int PF>
+__global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
+  constexpr int NT = 2 * TW;            // vocabulary columns per workgroup
+  constexpr int CB = TW / 16;           // 16-column MFMA blocks per wave
+  constexpr int BJ = NT / 32;           // lm-head chunks per thread per stage
+  extern __shared__ __attribute__((aligned(16))) char kls[];
+  char* As = kls;
+  char* Bs = kls + KG_M * KG_RS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nM = (a.rows + 63) / 64, nN = (a.vocab + NT - 1) / NT;
+  const int slot = blockIdx.x >> 3;
+  const int nt = (blockIdx.x & 7) + 8 * (slot / nM), mt = slot % nM;
+  if (nt >= nN) return;                 // whole workgroup: no barrier is skipped
+  // global -> LDS: thread t copies 16-byte chunk t % 8 of rows t / 8 + 32 j
+  const int lr = tid >> 3, lc = tid & 7;
+  const char* hsrc = (const char*)((lr & 15) < 8 ? a.h_full : a.h_comp);
+  int arow[4], vrow[BJ];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int r = mt * 64 + 8 * ((lr >> 4) + 2 * j) + (lr & 7);     // kl row of logit row lr + 32 j
+    arow[j] = r < a.rows ? r : a.rows - 1;                            // past the end: re-read, unused
+  }
+#pragma unroll
+  for (int j = 0; j < BJ; ++j) {
+    const int v = nt * NT + lr + 32 * j;
+    vrow[j] = v < a.vocab ? v : a.vocab - 1;
+  }
+  uint4 ra[PF][4], rb[PF][BJ];
+  auto gload = [&](int k0, uint4 (&xa)[4], uint4 (&xb)[BJ]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) xa[j] = ldg16(hsrc + ((size_t)arow[j] * a.hidden + k0 + 8 * lc) * 2);
+#pragma unroll
+    for (int j = 0; j < BJ; ++j)
+      xb[j] = ldg16((const char*)a.w + ((size_t)vrow[j] * a.hidden + k0 + 8 * lc) * 2);
+  };
+  auto sstore = [&](const uint4 (&xa)[4], const uint4 (&xb)[BJ]) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) *reinterpret_cast<uint4*>(As + (lr + 32 * j) * KG_RS + 16 * lc) = xa[j];
+#pragma unroll
+    for (int j = 0; j < BJ; ++j) *reinterpret_cast<uint4*>(Bs + (lr + 32 * j) * KG_RS + 16 * lc) = xb[j];
+  };
+  const int wm = wave >> 1, wn = wave & 1;
+  const int i = lane & 15, kg = lane >> 4;
+  f32x4_t acc[4][CB];
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int c = 0; c < CB; ++c) acc[b][c] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
+  auto compute = [&]() {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      // lane (i, kg) holds elements 32 t + 8 kg .. + 8 of its row in both operands
+      uint4 af[4];
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        af[b] = *reinterpret_cast<const uint4*>(As + (64 * wm + 16 * b + i) * KG_RS + 16 * (kg + 4 * t));
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        const uint4 bf =
+            *reinterpret_cast<const uint4*>(Bs + (TW * wn + 16 * c + i) * KG_RS + 16 * (kg + 4 * t));
+#pragma unroll
+        for (int b = 0; b < 4; ++b)
+          acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[b]),
+                                                              __builtin_bit_cast(bf16x8_t, bf),
+                                                              acc[b][c], 0, 0, 0);
+      }
+    }
+  };
+  // every load is unconditional: past the last stage a load re-reads the last one
+  const int last = a.hidden - KG_BK;
+  if constexpr (PF == 1) {
+    gload(0, ra[0], rb[0]);
+    for (int k0 = 0; k0 < a.hidden; k0 += KG_BK) {
+      __syncthreads();                  // the previous stage's readers are done
+      sstore(ra[0], rb[0]);
+      __syncthreads();
+      gload(k0 + KG_BK <= last ? k0 + KG_BK : last, ra[0], rb[0]);
+      compute();
+    }
+  } else {
+    static_assert(PF == 2, "one or two stages in flight");
+    // (the stage count hidden / 64 is even: hidden is a multiple of 128)
+    gload(0, ra[0], rb[0]);
+    gload(KG_BK, ra[1], rb[1]);
+    for (int k0 = 0; k0 < a.hidden; k0 += 2 * KG_BK) {
+      __syncthreads();
+      sstore(ra[0], rb[0]);
+      __syncthreads();
+      gload(k0 + 2 * KG_BK <= last ? k0 + 2 * KG_BK : last, ra[0], rb[0]);
+      compute();
+      __syncthreads();
+      sstore(ra[1], rb[1]);
+      __syncthreads();
+      gload(k0 + 3 * KG_BK <= last ? k0 + 3 * KG_BK : last, ra[1], rb[1]);
+      compute();
+    }
+  }
+  // acc[b][c][r] = logit of row 16 b + 4 kg + r (of the wave's 64), column 16 c + i:
+  // lanes kg = 0, 1 the full rows 4 kg + r of block b, lanes kg = 2, 3 the same
+  // rows compressed.  Lanes 0..31 form the statistics of kl row 8 b + 4 kg + r
+  // over each 64-column tile g (blocks c = 4 g .. 4 g + 3).
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+#pragma unroll
+    for (int g = 0; g < TW / 64; ++g) {
+      float lf[4][4], dl[4][4];
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const float x = acc[b][4 * g + c][r];
+          lf[c][r] = x;
+          dl[c][r] = x - __shfl_xor(x, 32);     // delta = full - compressed logit
+        }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float m = fmaxf(fmaxf(lf[0][r], lf[1][r]), fmaxf(lf[2][r], lf[3][r]));
+        m = max16(m);
+        float p[4], S = 0.0f, T = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          p[c] = __expf(lf[c][r] - m);
+          S = S + p[c];
+          T = T + p[c] * dl[c][r];
+        }
+        S = sum16(S);
+        const float mu = sum16(T) / S;
+        float A = 0.0f;
+#pragma unroll
+        for (int c = 0; c < 4; ++c) A = A + p[c] * gfun(mu - dl[c][r]);
+        A = sum16(A);
+        const int row = mt * 64 + 32 * wm + 8 * b + 4 * kg + r;
+        const int tile = (nt * NT + TW * wn) / 64 + g;
+        if (lane < 32 && i == 0 && row < a.rows && tile < a.ntiles)
+          *reinterpret_cast<float4*>(a.part + ((size_t)row * a.ntiles + tile) * 4) =
+              make_float4(m, S, mu, A / S);
+      }
+    }
+  }
+}
+
+template <int TW, int PF>
+static void launch_kl_gemm(const KLArgs& a, hipStream_t s) {
+  const int nM = (a.rows + 63) / 64, nN = (a.vocab + 2 * TW - 1) / (2 * TW);
+  hipFuncSetAttribute((const void*)kl_gemm_kernel<TW, PF>, hipFuncAttributeMaxDynamicSharedMemorySize,
+                      kg_lds<TW>());
+  hipLaunchKernelGGL((kl_gemm_kernel<TW, PF>), dim3(8 * nM * ((nN + 7) / 8)), dim3(256), kg_lds<TW>(), s, a);
+}
+
 // One workgroup per row: merge the tile statistics (fixed reduction order).
 __global__ void __launch_bounds__(256) kl_merge_kernel(KLArgs a) {
   __shared__ float red[256];
@@ -263,11 +436,17 @@ int kl_tile_cols() { return KL_TILE; }
 
 int launch_kl(const KLArgs& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  const int nrb = (a.rows + 7) / 8;
-  const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
-  const int lds = 16 * KL_AROW;
-  hipFuncSetAttribute((const void*)kl_tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), lds, s, a);
+  if (a.rows >= KG_WIDE_ROWS) {
+    launch_kl_gemm<128, 1>(a, s);
+  } else if (a.rows >= KG_MIN_ROWS) {
+    launch_kl_gemm<64, 2>(a, s);
+  } else {
+    const int nrb = (a.rows + 7) / 8;
+    const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
+    const int lds = 16 * KL_AROW;
+    hipFuncSetAttribute((const void*)kl_tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), lds, s, a);
+  }
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();
 }

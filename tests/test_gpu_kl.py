@@ -59,7 +59,11 @@ def test_kl_reward_full_size(which):
     assert np.all(got >= 0)
 
 
-@pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (13, 256, 1024), (64, 512, 4096)])
+# row counts below 16 take the per-step kernel, 16 and more the blocked GEMM
+# (partial row blocks, vocabularies that end inside a 256-column block)
+@pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (13, 256, 1024), (15, 128, 4160),
+                                          (16, 128, 256), (64, 512, 4096), (100, 256, 4160),
+                                          (523, 128, 640)])
 def test_kl_reward_shapes(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 7 + hid)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
@@ -68,3 +72,24 @@ def test_kl_reward_shapes(rows, hid, voc):
     got = _kl_gpu(rows, hid, voc, hf.cuda(), hc.cuda(), w.cuda())
     ref = okl.kl_reward(hf.float().numpy(), hc.float().numpy(), w.float().numpy())
     assert _kl_ok(got, ref), (got, ref)
+
+
+def test_kl_reward_deferred_rollout_full_size():
+    """A rollout's rewards deferred to one call: 256 rows (32 steps x batch 8)
+    at hidden 4096, vocab 32768 through the blocked GEMM; sampled rows (first
+    and last of row blocks) against the oracle, one unpruned step exactly 0."""
+    wl = W.WORKLOADS[5]
+    hid, voc = wl.kl_hidden, wl.kl_vocab
+    rows = 256
+    w = torch.empty((voc, hid), dtype=torch.bfloat16, device="cuda")
+    sg.fill_normal(w, wl, W.S_WLM, 0, 0.02)
+    g = torch.Generator(device="cpu").manual_seed(2608)
+    hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
+    hc = (hf.float() + 0.05 * torch.randn(rows, hid, generator=g)).to(torch.bfloat16)
+    hc[7] = hf[7]
+    got = _kl_gpu(rows, hid, voc, hf.cuda(), hc.cuda(), w)
+    idx = [0, 7, 63, 64, 127, 128, 200, 255]
+    ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], _lm_head_np())
+    assert got[7] == 0.0
+    assert _kl_ok(got[idx], ref), (got[idx], ref)
+    assert np.all(got >= 0)

@@ -30,9 +30,10 @@ def _download(buf, u, L):
     return d
 
 
-def _ragged_run(budgets, steps, n0=700, gumbel=None, tau=1.0):
+def _ragged_run(budgets, steps, n0=700, gumbel=None, tau=1.0, hidden=None):
+    kw = {"hidden": tuple(hidden)} if hidden else {}
     wl = W.WORKLOADS[2].scaled(n_kv_heads=len(budgets), n_q_heads=4 * len(budgets), n0=n0,
-                               budget=max(budgets), steps=steps)
+                               budget=max(budgets), steps=steps, **kw)
     U = wl.units
     buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
                         wl.capacity, wl.dtype, wl.ent_window, 0.0, True, ragged=True)
@@ -122,3 +123,14 @@ def test_equal_budgets_reduce_to_the_fixed_budget():
 
 def test_per_unit_budgets_sampled_with_log_prob():
     assert _ragged_run([120, 700, 90], steps=4, gumbel=55, tau=0.8) >= 1
+
+
+def test_two_layer_policy_on_ragged_caches():
+    # the matrix-core scoring pass with per-unit lengths and budgets (widths
+    # padded to 64, then to 128)
+    assert _ragged_run([200, 10 ** 6, 150], steps=4, hidden=(64, 64)) >= 1
+    assert _ragged_run([260, 90], steps=3, hidden=(96, 40)) >= 1
+
+
+def test_two_layer_policy_sampled_on_ragged_caches():
+    assert _ragged_run([120, 700, 90], steps=3, gumbel=77, tau=0.7, hidden=(64, 64)) >= 1
