@@ -8,7 +8,11 @@ order: x_i = [alpha_i, ||v_i||_2, H_i, pos_i].  Readings of the text:
 
 * alpha_i — attention mass received by token i, averaged over the G query heads
   that share the token's KV head, accumulated over decode steps since the state
-  was initialised (the ablation table calls it "cumulative attention").
+  was initialised (the ablation table calls it "cumulative attention").  The
+  state definition itself (Sec. 3.1.1) takes the mass of the most recent
+  forward pass averaged over all heads and layers: ``alpha_recent`` keeps only
+  the step's mass, and ``global_alpha`` averages it over every KV unit of the
+  sequence (all layers and KV heads), position by position.
 * H_i — for the queries of the last w decode steps (current step included;
   every (step, query head) pair is one query; w = 64):
       Z_i = sum_q a_q(i),  N_i = sum_q a_q(i) H(a_q),  H_i = N_i / Z_i,
@@ -106,6 +110,23 @@ def head_variance(a) -> np.ndarray:
     G = a.shape[0]
     mean = a.sum(axis=0) / G
     return ((a - mean[None, :]) ** 2).sum(axis=0) / G
+
+
+def global_alpha(alphas, positions, n_units: int):
+    """The paper's alpha (Sec. 3.1.1): the attention mass token p received in
+    the most recent forward pass, averaged over all heads and layers.  Input:
+    for each of the ``n_units`` KV units of one sequence (every layer and KV
+    head), its rows' step masses (group means over the unit's G query heads)
+    and positions.  Every unit has the same number of query heads, so the mean
+    over all heads is the mean over units of the group means; a unit that no
+    longer holds p contributes 0 (its heads cannot attend to p).  Returns, per
+    unit, that average at each of its rows' positions."""
+    total = {}
+    for al, ps in zip(alphas, positions):
+        for a_i, p_i in zip(np.asarray(al, np.float64), np.asarray(ps, np.int64)):
+            total[int(p_i)] = total.get(int(p_i), 0.0) + float(a_i)
+    return [np.array([total[int(p_i)] / n_units for p_i in np.asarray(ps, np.int64)], np.float64)
+            for ps in positions]
 
 
 def feature_matrix5(alpha, V, sigma, Z, N, pos, T: int) -> np.ndarray:

@@ -54,6 +54,7 @@ class StudentState:
     scale: float
     records: dict = field(default_factory=dict)
     sigma: np.ndarray | None = None    # per-row head variance of the last step's attention
+    alpha_recent: bool = False         # alpha = the last step's mass only (not accumulated)
 
     @property
     def L(self) -> int:
@@ -70,7 +71,7 @@ class TeacherState:
 
 
 def new_student(K, V, positions, *, G: int, scale: float, window: int = 64,
-                next_pos: int | None = None) -> StudentState:
+                next_pos: int | None = None, alpha_recent: bool = False) -> StudentState:
     """State for a cache whose rows carry no attention history yet (features zero)."""
     K = np.asarray(K, np.float64)
     V = np.asarray(V, np.float64)
@@ -79,7 +80,8 @@ def new_student(K, V, positions, *, G: int, scale: float, window: int = 64,
     return StudentState(K=K.copy(), V=V.copy(), pos=pos.copy(), alpha=np.zeros(L),
                         hist=features.WindowHistory(L, window), N=np.zeros(L), Z=np.zeros(L),
                         step=0, next_pos=int(pos.max()) + 1 if next_pos is None else next_pos,
-                        window=window, G=G, scale=scale, sigma=np.zeros(L))
+                        window=window, G=G, scale=scale, sigma=np.zeros(L),
+                        alpha_recent=alpha_recent)
 
 
 def new_teacher(K, V, positions, *, scale: float, next_pos: int | None = None) -> TeacherState:
@@ -115,7 +117,7 @@ def decode_step(st: StudentState, q, k_new=None, v_new=None) -> attention.Attent
     cz, cn = features.step_contributions(att.a, att.H)
     st.sigma = features.head_variance(att.a)
     t = st.step
-    st.alpha = st.alpha + cz / st.G
+    st.alpha = (0.0 if st.alpha_recent else st.alpha) + cz / st.G
     st.hist.record(t, cz, cn)
     # add/retire form of the same window (cross-check only)
     if st.window > 0 and t >= st.window:

@@ -244,8 +244,6 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
 
 }  // namespace
 
-size_t mlp2_lds_bytes() { return (size_t)Lay<128>::FLOATS * sizeof(float); }
-
 int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* stream) {
   const int nblk = (a.L + MW * 16 - 1) / (MW * 16);
   const int gx = nblk < 8 ? nblk : 8;

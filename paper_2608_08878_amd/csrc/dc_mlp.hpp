@@ -4,7 +4,6 @@
 
 namespace dc {
 
-size_t mlp2_lds_bytes();
 // Scores and ranking keys of every row of every unit (keys[u * kstride + r]).
 int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* stream);
 
