@@ -417,6 +417,69 @@ def bench_paper_policy(args, wl, dev, log):
             "note": "paper-faithful state and policy; decode + separate scoring pass, timed apart"}
 
 
+def bench_global_alpha(args, wl, dev, log):
+    """The paper's alpha on a decode workload: every step leaves each row's
+    most recent mass (alpha_recent), the cross-unit average over all heads and
+    layers of each sequence replaces it, then the workload's policy scores
+    and the selection evicts.  Decode, the average and scoring + selection are
+    timed apart."""
+    import torch
+    from paper_2608_08878_amd.buffers import DecodeBuffers, make_policy
+    from synth import gpu as sg
+    from synth import workloads as W
+
+    U, G, D = wl.units, wl.group, wl.head_dim
+    cap = max(wl.n0 + 1, wl.budget + 1)
+    buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, D, cap, wl.dtype,
+                        wl.ent_window, alpha_recent=True)
+    buf.reserve_workspace(cap)
+    sg.init_cache(wl, buf.k, buf.v, U, cap)
+    buf.feat_init(wl.n0, 0)
+    params = torch.empty(wl.n_params, dtype=torch.float32, device=dev)
+    sg.fill_normal(params, wl, W.S_POLICY, 0, 0.1)
+    pol = make_policy(params, wl.hidden)
+    nsteps = 1 + args.warmup + args.steps
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    q = torch.empty((U, G, D), dtype=td, device=dev)
+    kn = torch.empty((U, D), dtype=td, device=dev)
+    vn = torch.empty_like(kn)
+    out = torch.empty_like(q)
+    parts = {"decode": [], "global_alpha": [], "score_select": [], "step": []}
+    first_ms = None
+    for t in range(nsteps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        ev = _events(4)
+        ev[0].record()
+        buf.decode_step(q, kn, vn, out)
+        ev[1].record()
+        buf.global_alpha()
+        ev[2].record()
+        buf.score_evict(pol, wl.budget)
+        ev[3].record()
+        torch.cuda.synchronize()
+        if t == 0:
+            first_ms = ev[0].elapsed_time(ev[3])
+            if not args.no_shrink:
+                buf.shrink(wl.budget + 1)
+        elif t > args.warmup:
+            parts["decode"].append(ev[0].elapsed_time(ev[1]))
+            parts["global_alpha"].append(ev[1].elapsed_time(ev[2]))
+            parts["score_select"].append(ev[2].elapsed_time(ev[3]))
+            parts["step"].append(ev[0].elapsed_time(ev[3]))
+    m = {k: float(np.mean(v)) for k, v in parts.items()}
+    L = wl.budget + 1
+    # the average reads alpha and pos and writes alpha (12 B per row), plus the sums
+    ga_bytes = U * L * 12 + wl.batch * (wl.n0 + nsteps) * 8 * 2
+    return {"value": round(1e3 / m["step"], 3), "unit": "decode steps/s",
+            "ms_per_step": round(m["step"], 4), "decode_ms": round(m["decode"], 4),
+            "global_alpha_ms": round(m["global_alpha"], 4),
+            "global_alpha_gbps": round(ga_bytes / (m["global_alpha"] * 1e-3) / 1e9, 1),
+            "score_select_ms": round(m["score_select"], 4), "first_step_ms": round(first_ms, 3),
+            "note": "alpha = the most recent step's mass averaged over all heads and layers of "
+                    "each sequence; decode + average + scoring pass, timed apart"}
+
+
 def bench_hybrid(args, wl, dev, log):
     """The appendix's head-level hybrid on a decode workload: a fraction of the
     KV heads keeps its full cache, the others keep the workload's budget
@@ -536,6 +599,10 @@ def main():
     ap.add_argument("--hybrid", type=float, default=0.0,
                     help="fraction of KV heads that keep their full cache (head-level hybrid; "
                          "per-unit budgets on a ragged cache), workloads 2 and 3")
+    ap.add_argument("--global-alpha", action="store_true",
+                    help="alpha as the most recent step's mass averaged over all heads and "
+                         "layers of each sequence (decode, the average, then scoring), "
+                         "workloads 2 and 3")
     ap.add_argument("--train-select", action="store_true",
                     help="workload 5: the student keeps a Gumbel-sampled top-B and computes "
                          "log pi (training mode) instead of the deterministic selection")
@@ -571,12 +638,14 @@ def main():
         torch.cuda.synchronize()
         del a, b
 
-    if args.config in (1, 4, 5) or args.policy == "paper" or args.hybrid > 0:
+    if args.config in (1, 4, 5) or args.policy == "paper" or args.hybrid > 0 or args.global_alpha:
         fn = {1: bench_single_step, 4: bench_periodic_evict, 5: bench_teacher_student_kl}.get(args.config)
         if args.policy == "paper":
             fn = bench_paper_policy
         if args.hybrid > 0:
             fn = bench_hybrid
+        if args.global_alpha:
+            fn = bench_global_alpha
         res = fn(args, wl, dev, log)
         result = {"metric": f"decode steps/s, workload {args.config}", "n_gpus": 1,
                   "steps": args.steps, "warmup": args.warmup, "higher_is_better": True,

@@ -123,6 +123,9 @@ typedef struct {
   float   *sigma;      /* [units][capacity] sigma_i of the last step, or NULL; written by
                           every decode step and dc_feat_init (0) when present, moved by
                           eviction; required by five-input policies */
+  int32_t alpha_recent; /* 0: alpha accumulates over steps (cumulative attention);
+                          1: every decode step replaces alpha by that step's mass (the
+                          paper's "most recent forward pass"; see dc_global_alpha) */
 } dc_feat;
 
 /* Policy MLP f_phi (Sec. 3.1.2; a small ReLU MLP per App. D).  params is a
@@ -307,6 +310,30 @@ dc_status dc_subset_log_prob(int32_t units, int32_t len, int32_t budget, float t
 
 /* Workspace bytes of dc_subset_log_prob (0 for invalid sizes). */
 size_t dc_subset_log_prob_workspace_bytes(int32_t units, int32_t len, int32_t budget);
+
+/* The paper's alpha_i (Sec. 3.1.1, state space): the attention mass token i
+ * received in the most recent forward pass, averaged over all heads and
+ * layers.  With feat->alpha_recent = 1 every decode step leaves in alpha each
+ * row's mass of that step averaged over the G query heads of its unit; this
+ * call replaces it, for every row of every unit, by the mean over all units of
+ * the same sequence (its n_layers x n_kv_heads KV units, which hold equally
+ * many query heads) of those values at the row's position, a unit that no
+ * longer holds the position counting 0.  Call it after dc_decode_step and
+ * before dc_score_evict (dc_decode_evict scores inside the step, with each
+ * unit's own recent mass).  The sums are 64-bit fixed point (2^-52 per unit
+ * of alpha): integer sums do not depend on the order of their terms, so the
+ * result is deterministic; alpha is clamped to [0, 1] first (recent masses lie
+ * there).  Ragged caches are read through kv->unit_len.
+ *   ws: dc_global_alpha_workspace_bytes(dims, feat->next_pos) bytes.
+ * Errors: DC_ERR_NULL, DC_ERR_SHAPE (len outside 1..capacity, next_pos < 1),
+ * DC_ERR_UNSUPPORTED (alpha_recent != 1, more than 2048 units per sequence),
+ * DC_ERR_WORKSPACE. */
+dc_status dc_global_alpha(const dc_dims *dims, const dc_kv *kv, dc_feat *feat, void *ws,
+                          size_t ws_bytes, void *hip_stream);
+
+/* Workspace bytes of dc_global_alpha for sequences of up to `positions` tokens
+ * (0 for invalid sizes). */
+size_t dc_global_alpha_workspace_bytes(const dc_dims *dims, int32_t positions);
 
 /* Largest row count of one dc_kl_reward call. */
 #define DC_KL_MAX_ROWS 16384

@@ -35,7 +35,7 @@ class dc_feat(ctypes.Structure):
                 ("vnorm", ctypes.c_void_p), ("qring", ctypes.c_void_p),
                 ("qstat", ctypes.c_void_p), ("step", ctypes.c_int32),
                 ("next_pos", ctypes.c_int32), ("ring_pmax", ctypes.c_int32 * MAX_WINDOW),
-                ("sigma", ctypes.c_void_p)]
+                ("sigma", ctypes.c_void_p), ("alpha_recent", ctypes.c_int32)]
 
 
 class dc_policy(ctypes.Structure):
@@ -63,7 +63,8 @@ EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evi
            "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_score_evict_units",
            "dc_subset_log_prob",
            "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_reinforce_terms",
-           "dc_dynamic_budget", "dc_status_str")
+           "dc_dynamic_budget", "dc_global_alpha", "dc_global_alpha_workspace_bytes",
+           "dc_status_str")
 
 _lib = None
 
@@ -115,6 +116,11 @@ def lib() -> ctypes.CDLL:
         L.dc_reinforce_terms.argtypes = [i32, i32, ctypes.POINTER(dc_reinforce_cfg), vp, vp, vp,
                                          vp, vp, vp, vp, vp, vp]
         L.dc_reinforce_terms.restype = ctypes.c_int
+        L.dc_global_alpha.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                      ctypes.POINTER(dc_feat), vp, sz, vp]
+        L.dc_global_alpha.restype = ctypes.c_int
+        L.dc_global_alpha_workspace_bytes.argtypes = [ctypes.POINTER(dc_dims), i32]
+        L.dc_global_alpha_workspace_bytes.restype = sz
         L.dc_dynamic_budget.argtypes = [ctypes.c_float, i32, i32]
         L.dc_dynamic_budget.restype = i32
         L.dc_status_str.argtypes = [ctypes.c_int]
@@ -177,6 +183,15 @@ def dc_decode_evict(dims, kv, feat, policy, budget: int, q, k_new, v_new, out, s
     _check(lib().dc_decode_evict(ctypes.byref(dims), ctypes.byref(kv), _ref(feat), _ref(policy),
                                  budget, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(out),
                                  _ptr(scores_out), _ptr(kept_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_global_alpha(dims, kv, feat, ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_global_alpha(ctypes.byref(dims), ctypes.byref(kv), ctypes.byref(feat),
+                                 _ptr(ws), ws_bytes, stream))
+
+
+def dc_global_alpha_workspace_bytes(dims, positions: int) -> int:
+    return int(lib().dc_global_alpha_workspace_bytes(ctypes.byref(dims), positions))
 
 
 def dc_kl_reward(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_out, ws=None,

@@ -22,7 +22,7 @@ class DecodeBuffers:
 
     def __init__(self, batch, n_layers, n_q_heads, n_kv_heads, head_dim, capacity, dtype="bf16",
                  ent_window=64, scale=0.0, features=True, device="cuda", sigma=False,
-                 ragged=False):
+                 ragged=False, alpha_recent=False):
         self.G = n_q_heads // n_kv_heads
         self.U = batch * n_layers * n_kv_heads
         self.D = head_dim
@@ -53,6 +53,8 @@ class DecodeBuffers:
             self.feat = B.dc_feat(self.alpha.data_ptr(), self.num.data_ptr(), self.den.data_ptr(),
                                   self.pos.data_ptr(), self.vnorm.data_ptr(),
                                   self.qring.data_ptr(), self.qstat.data_ptr(), 0, 0)
+            self.feat.alpha_recent = int(alpha_recent)
+            self.ga_ws = None
             self.sigma = None
             if sigma:
                 # the fifth feature (needed by five-input policies)
@@ -127,6 +129,15 @@ class DecodeBuffers:
         B.dc_decode_evict(self.dims, self.kv, self.feat, policy, budget, q, k_new, v_new, out,
                           scores_out, kept_out, self.ws, self.ws_bytes, stream_handle(stream))
         return out
+
+    def global_alpha(self, stream=None):
+        """Replace every row's recent alpha by its average over the sequence's
+        units (all layers and KV heads) at the row's position."""
+        need = B.dc_global_alpha_workspace_bytes(self.dims, self.feat.next_pos)
+        if self.ga_ws is None or self.ga_ws.numel() < need:
+            self.ga_ws = torch.empty(need, dtype=torch.uint8, device=self.k.device)
+        B.dc_global_alpha(self.dims, self.kv, self.feat, self.ga_ws, self.ga_ws.numel(),
+                          stream_handle(stream))
 
     def score_evict(self, policy, budget, scores_out=None, kept_out=None, stream=None):
         B.dc_score_evict(self.dims, self.kv, self.feat, policy, budget, scores_out, kept_out,

@@ -12,7 +12,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libdistillcache.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 SOURCES = ["dc_api.cpp", "dc_decode.hip", "dc_step.hip", "dc_evict.hip", "dc_kl.hip",
-           "dc_logz.hip", "dc_reinforce.hip", "dc_mlp.hip"]
+           "dc_logz.hip", "dc_reinforce.hip", "dc_mlp.hip", "dc_alpha.hip"]
 # -ffp-contract=off: every fused multiply-add in the kernels is written explicitly, so the
 # retire step can reproduce the arithmetic of the step that added a contribution.
 # packed-fp32-ops is disabled: the compiler must not emit packed float32 arithmetic.

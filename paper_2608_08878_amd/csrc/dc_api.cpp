@@ -181,6 +181,7 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
       return DC_ERR_NULL;
     if (W > 0 && (!feat->qring || !feat->qstat)) return DC_ERR_NULL;
     if (feat->step < 0 || feat->next_pos < 0) return DC_ERR_SHAPE;
+    if (feat->alpha_recent != 0 && feat->alpha_recent != 1) return DC_ERR_VALUE;
   }
   const int len = kv->len;
   const int append = k_new != nullptr;
@@ -227,6 +228,7 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
     a.qring = feat->qring;
     a.qstat = feat->qstat;
     a.T = feat->next_pos + append;
+    a.arec = feat->alpha_recent;
     a.window = W;
     if (W > 0) {
       a.slot = feat->step % W;
@@ -586,6 +588,37 @@ dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   commit_decode(kv, feat, a, dims->ent_window);
   kv->len = e.budget;
   return DC_OK;
+}
+
+size_t dc_global_alpha_workspace_bytes(const dc_dims* dims, int32_t positions) {
+  if (!dims || dims->batch < 1 || dims->n_layers < 1 || dims->n_kv_heads < 1 || positions < 1)
+    return 0;
+  // the sums, then every unit group's partial sums
+  const size_t groups = (size_t)dc::global_alpha_groups(dims->n_layers * dims->n_kv_heads);
+  return align256((size_t)dims->batch * (size_t)positions * (1 + groups) * sizeof(uint64_t));
+}
+
+dc_status dc_global_alpha(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, void* ws,
+                          size_t ws_bytes, void* hip_stream) {
+  dc_status st = check_dims(dims);
+  if (st != DC_OK) return st;
+  if (!kv || !feat || !feat->alpha || !feat->pos) return DC_ERR_NULL;
+  if (kv->len < 1 || kv->len > dims->capacity || feat->next_pos < 1) return DC_ERR_SHAPE;
+  const int per_seq = dims->n_layers * dims->n_kv_heads;
+  if (feat->alpha_recent != 1 || per_seq > 2048) return DC_ERR_UNSUPPORTED;
+  const size_t need = dc_global_alpha_workspace_bytes(dims, feat->next_pos);
+  if (!ws || ws_bytes < need) return DC_ERR_WORKSPACE;
+  dc::GlobalAlphaArgs a;
+  a.alpha = feat->alpha;
+  a.pos = feat->pos;
+  a.unit_len = kv->unit_len;
+  a.acc = (uint64_t*)ws;
+  a.cap = dims->capacity;
+  a.units = (int)units_of(dims);
+  a.len = kv->len;
+  a.per_seq = per_seq;
+  a.T = feat->next_pos;
+  return dc::launch_global_alpha(a, hip_stream) == 0 ? DC_OK : DC_ERR_HIP;
 }
 
 dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,

@@ -269,7 +269,7 @@ __device__ __forceinline__ void phase_d(const DecodeArgs& a, int u, int r0, int 
       a.num[gi] = (double)cn;
       a.pos[gi] = a.T - 1;
     } else {
-      a.alpha[gi] = a.alpha[gi] + cz * invG;
+      a.alpha[gi] = (a.arec ? 0.0f : a.alpha[gi]) + cz * invG;
       double z = a.den[gi] + (double)cz;
       double n = a.num[gi] + (double)cn;
       if (a.retire && a.pos[gi] <= a.pmax_ret) {

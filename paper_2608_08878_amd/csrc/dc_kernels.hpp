@@ -33,6 +33,7 @@ struct DecodeArgs {
   int window;           // w (0 = unbounded)
   int slot;             // ring slot written by this step
   int retire;           // the step leaving the window has a ring record
+  int arec;             // alpha = this step's mass only (not accumulated)
   int pmax_ret;         // largest position present at that step
   // chunked (split) path scratch
   float* ws_s;          // [units][lmax][G] logits
@@ -119,6 +120,19 @@ struct KLArgs {
   int rows, hidden, vocab, ntiles;
 };
 
+// The cross-unit alpha average of one decode step (dc_alpha.hip).
+struct GlobalAlphaArgs {
+  float* alpha;             // [units][cap]
+  const int32_t* pos;       // [units][cap]
+  const int32_t* unit_len;  // [units] (ragged caches) or null
+  uint64_t* acc;            // [sequences][T] fixed-point sums, then the groups' partial sums
+  int64_t cap;
+  int units;
+  int len;                  // rows per unit (bound with unit_len)
+  int per_seq;              // units per sequence (n_layers x n_kv_heads)
+  int T;                    // positions 0..T-1
+};
+
 // Launchers return a hipError_t value (0 on success).
 int launch_decode(const DecodeArgs& a, int dtype, int D, int G, bool feat, bool split,
                   void* stream);
@@ -138,6 +152,8 @@ int evict_max_len();
 size_t evict_ws_bytes(int units, int L);
 size_t evict_ext_ws_bytes(int units, int L);
 int launch_kl(const KLArgs& a, void* stream);
+int launch_global_alpha(const GlobalAlphaArgs& a, void* stream);
+int global_alpha_groups(int per_seq);    // unit groups of one sequence (workspace sizing)
 // bf16 matrix-core step (dc_step.hip); e != nullptr fuses scoring and eviction.
 int launch_step(const DecodeArgs& a, const EvictArgs* e, int D, int G, bool feat, bool chunked,
                 void* stream);

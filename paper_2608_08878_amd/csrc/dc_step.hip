@@ -451,7 +451,7 @@ __device__ __forceinline__ void update_row(const DecodeArgs& a, size_t gi, bool 
     a.pos[gi] = pos;
     a.vnorm[gi] = vn;
   } else {
-    alpha = a.alpha[gi] + cz * invG;
+    alpha = (a.arec ? 0.0f : a.alpha[gi]) + cz * invG;
     double z = a.den[gi] + (double)cz;
     double n = a.num[gi] + (double)cn;
     pos = a.pos[gi];
@@ -635,7 +635,7 @@ __global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArg
         rz = s2 == k ? zr[s2] : rz;
         rn = s2 == k ? nr[s2] : rn;
       }
-      float al = x.al + cz * invG;
+      float al = (a.arec ? 0.0f : x.al) + cz * invG;
       double de = x.de + (double)cz;
       double nu = x.nu + (double)cn;
       int32_t ps = x.p;

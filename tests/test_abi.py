@@ -266,3 +266,36 @@ def test_ragged_decode_needs_bf16_and_moves_fit_on_chip():
     assert L.dc_score_evict(ctypes.byref(big), ctypes.byref(kvb), ctypes.byref(_feat()),
                             ctypes.byref(pol), 20000, None, None, FAKE, 1 << 40, None) == 3
     assert kvb.len == 40000
+
+
+def test_global_alpha_rejects_bad_arguments():
+    L = B.lib()
+    dims = _dims()
+    kv = B.dc_kv(FAKE, FAKE, 50)
+
+    def call(d=dims, k=kv, f=None, ws=FAKE, wsb=1 << 30):
+        f = f if f is not None else _feat(alpha_recent=1)
+        return L.dc_global_alpha(ctypes.byref(d), ctypes.byref(k) if k is not None else None,
+                                 ctypes.byref(f), ws, wsb, None)
+
+    assert call(k=None) == 1
+    assert call(f=_feat(alpha=None, alpha_recent=1)) == 1
+    assert call(f=_feat(pos=None, alpha_recent=1)) == 1
+    assert call(k=B.dc_kv(FAKE, FAKE, 0)) == 2                       # no rows
+    assert call(k=B.dc_kv(FAKE, FAKE, 101)) == 2                     # beyond the capacity
+    assert call(f=_feat(next_pos=0, alpha_recent=1)) == 2
+    assert call(f=_feat()) == 3                                      # alpha accumulates: not this mode
+    assert call(d=_dims(n_layers=300, n_kv_heads=8, n_q_heads=8)) == 3   # 2400 units per sequence
+    need = B.dc_global_alpha_workspace_bytes(dims, 50)
+    assert need >= 1 * 50 * 8 and need % 256 == 0
+    assert call(wsb=need - 1) == 6
+    assert call(ws=None) == 6
+    assert B.dc_global_alpha_workspace_bytes(_dims(batch=3), 1000) >= 3 * 1000 * 8
+    assert B.dc_global_alpha_workspace_bytes(dims, 0) == 0
+
+
+def test_decode_rejects_an_alpha_mode_outside_its_two_values():
+    dims = _dims()
+    kv = B.dc_kv(FAKE, FAKE, 50)
+    assert _decode(dims, kv, _feat(alpha_recent=2), ws=FAKE, wsb=1 << 40) == 8
+    assert _decode(dims, kv, _feat(alpha_recent=-1), ws=FAKE, wsb=1 << 40) == 8

@@ -2,9 +2,8 @@
 received in the most recent forward pass, averaged over all heads and layers)
 and of the most-recent-step alpha it is built from."""
 import numpy as np
-import pytest
 
-from oracle import attention, features
+from oracle import features
 from oracle import unit as ounit
 
 
