@@ -208,8 +208,11 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
 // read touches start 16 bytes apart in the banks).  The global loads of the
 // next PF stages are in flight in registers while the current stage feeds the
 // matrix cores.  Wave (wm, wn) owns rows 64 wm.. x columns TW wn.. (4 x TW/16
-// MFMA 16x16x32 bf16 blocks).  The epilogue forms the same per (row, 64-column
-// tile) statistics as kl_tile_kernel, for kl_merge_kernel.  Workgroup g runs on
+// MFMA 16x16x32 bf16 blocks).  Every logit sees the same MFMA sequence over the
+// hidden dimension as in kl_tile_kernel (same k split, same order), and the
+// epilogue forms the same per (row, 64-column tile) statistics in the same
+// reduction order, for kl_merge_kernel: the KL of a row is bit-identical
+// whichever kernel and row count served it.  Workgroup g runs on
 // XCD g mod 8; the row blocks of one vocabulary block are consecutive on one
 // XCD, so its lm-head slab comes from HBM once and then from that XCD's L2.
 // Two shapes: TW = 64 with two stages in flight (twice the workgroups: the
@@ -324,9 +327,12 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
   // acc[b][c][r] = logit of row 16 b + 4 kg + r (of the wave's 64), column 16 c + i:
   // lanes kg = 0, 1 the full rows 4 kg + r of block b, lanes kg = 2, 3 the same
   // rows compressed.  Lanes 0..31 form the statistics of kl row 8 b + 4 kg + r
-  // over each 64-column tile g (blocks c = 4 g .. 4 g + 3).
-#pragma unroll
-  for (int b = 0; b < 4; ++b) {
+  // over each 64-column tile g (blocks c = 4 g .. 4 g + 3), in the per-step
+  // kernel's reduction order (16-lane sums per 16-column block, then the blocks
+  // in column order), so a row's statistics, and its KL, do not depend on how
+  // many rows share the call.  One call per row block b, so that every index
+  // into the accumulators is a constant.
+  auto epilogue = [&](const f32x4_t (&ab)[CB], int b) {
 #pragma unroll
     for (int g = 0; g < TW / 64; ++g) {
       float lf[4][4], dl[4][4];
@@ -334,7 +340,7 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
       for (int c = 0; c < 4; ++c)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const float x = acc[b][4 * g + c][r];
+          const float x = ab[4 * g + c][r];
           lf[c][r] = x;
           dl[c][r] = x - __shfl_xor(x, 32);     // delta = full - compressed logit
         }
@@ -346,15 +352,13 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
 #pragma unroll
         for (int c = 0; c < 4; ++c) {
           p[c] = __expf(lf[c][r] - m);
-          S = S + p[c];
-          T = T + p[c] * dl[c][r];
+          S = S + sum16(p[c]);
+          T = T + sum16(p[c] * dl[c][r]);
         }
-        S = sum16(S);
-        const float mu = sum16(T) / S;
+        const float mu = T / S;
         float A = 0.0f;
 #pragma unroll
-        for (int c = 0; c < 4; ++c) A = A + p[c] * gfun(mu - dl[c][r]);
-        A = sum16(A);
+        for (int c = 0; c < 4; ++c) A = A + sum16(p[c] * gfun(mu - dl[c][r]));
         const int row = mt * 64 + 32 * wm + 8 * b + 4 * kg + r;
         const int tile = (nt * NT + TW * wn) / 64 + g;
         if (lane < 32 && i == 0 && row < a.rows && tile < a.ntiles)
@@ -362,7 +366,11 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
               make_float4(m, S, mu, A / S);
       }
     }
-  }
+  };
+  epilogue(acc[0], 0);
+  epilogue(acc[1], 1);
+  epilogue(acc[2], 2);
+  epilogue(acc[3], 3);
 }
 
 template <int TW, int PF>

@@ -93,3 +93,20 @@ def test_kl_reward_deferred_rollout_full_size():
     assert got[7] == 0.0
     assert _kl_ok(got[idx], ref), (got[idx], ref)
     assert np.all(got >= 0)
+
+
+def test_kl_reward_does_not_depend_on_the_rows_per_call():
+    """The per-step kernel (under 16 rows) and both GEMM shapes (16..255 rows,
+    256 and more) give every row the same bits."""
+    wl = W.WORKLOADS[5]
+    hid, voc = wl.kl_hidden, wl.kl_vocab
+    w = torch.empty((voc, hid), dtype=torch.bfloat16, device="cuda")
+    sg.fill_normal(w, wl, W.S_WLM, 0, 0.02)
+    g = torch.Generator(device="cpu").manual_seed(55)
+    hf = torch.randn(300, hid, generator=g).to(torch.bfloat16).cuda()
+    hc = (hf.float().cpu() + 0.05 * torch.randn(300, hid, generator=g)).to(torch.bfloat16).cuda()
+    wide = _kl_gpu(300, hid, voc, hf, hc, w)
+    narrow = _kl_gpu(100, hid, voc, hf[:100], hc[:100], w)
+    step = _kl_gpu(8, hid, voc, hf[96:104].contiguous(), hc[96:104].contiguous(), w)
+    assert np.array_equal(wide[:100], narrow)
+    assert np.array_equal(wide[96:104], step)
