@@ -123,3 +123,38 @@ def test_global_alpha_on_ragged_caches_with_per_unit_budgets():
 
 def test_global_alpha_of_a_single_unit_sequence_is_its_own_mass():
     assert _global_run(steps=3, batch=3, n_layers=1, n_kv=1) >= 1
+
+
+def test_recent_and_global_alpha_on_the_float32_path():
+    """The float32 / d = 64 kernels (workload 1's shape, no append): three steps
+    with alpha_recent, each followed by the cross-unit mean."""
+    wl = W.WORKLOADS[1].scaled(batch=2, n_layers=2, n_kv_heads=2, n_q_heads=4, steps=3)
+    U, per_seq = wl.units, wl.n_layers * wl.n_kv_heads
+    buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                        wl.capacity, wl.dtype, wl.ent_window, 0.0, True, alpha_recent=True)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(wl.n0, 0)
+    sts = []
+    for u in range(U):
+        st = H.oracle_student(wl, u)
+        st.alpha_recent = True
+        sts.append(st)
+    q, _, _ = _step_tensors(wl)
+    for t in range(3):
+        sg.queries(wl, t, q)
+        buf.decode_step(q)
+        torch.cuda.synchronize()
+        for u in range(U):
+            att = ounit.decode_step(sts[u], W.queries(wl, t, u))
+            ok, worst = H.vec_ok(H.to_np(buf.alpha[u, :wl.n0]), sts[u].alpha)
+            assert ok, (t, u, "recent alpha", worst)
+            assert np.allclose(sts[u].alpha, att.a.mean(axis=0), rtol=1e-14, atol=0)
+        buf.global_alpha()
+        torch.cuda.synchronize()
+        for b in range(wl.batch):
+            us = range(b * per_seq, (b + 1) * per_seq)
+            g = ofeat.global_alpha([sts[u].alpha for u in us], [sts[u].pos for u in us], per_seq)
+            for u, gu in zip(us, g):
+                sts[u].alpha = gu
+                ok, worst = H.vec_ok(H.to_np(buf.alpha[u, :wl.n0]), gu)
+                assert ok, (t, u, "global alpha", worst)
