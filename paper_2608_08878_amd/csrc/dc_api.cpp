@@ -572,8 +572,8 @@ dc_status dc_decode_evict(const dc_dims* dims, dc_kv* kv, dc_feat* feat, const d
   if (st != DC_OK) return st;
   const int G = group_of(dims), D = dims->head_dim;
   const int nm = e.evict ? (a.L - e.budget < e.budget ? a.L - e.budget : e.budget) : 0;
-  // the single-launch step serves four-input policies without LayerNorm and
-  // does not produce sigma
+  // the single-launch step serves the four-input one-hidden-layer policy
+  // without LayerNorm and does not produce sigma
   const bool fused = dims->dtype == DC_BF16 && !split && !e.ext && !feat->sigma &&
                      dc::step_fits(a.L, G, D, true, nm);
   if (fused) {
