@@ -564,3 +564,59 @@ def test_dynamic_budget_trajectory():
             print("trajectories parted at a near-tie at step", t)
             break
     assert lens[0] == 75 and max(lens) <= 95
+
+
+@pytest.mark.parametrize("n_q,n_kv,d", [(2, 2, 128), (4, 2, 128), (16, 2, 128), (8, 2, 64),
+                                        (16, 2, 64)])
+def test_fused_step_across_head_groups_and_dims(n_q, n_kv, d):
+    """The single-launch step (dc_decode_evict) at G = 1, 2, 8 and head_dim 64,
+    in lockstep with the oracle through the window retire: 70 steps, step 0
+    compresses 701 -> 256 rows; every step starts from the oracle's state."""
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=n_kv, n_q_heads=n_q, head_dim=d, n0=700, budget=256,
+                               steps=70)
+    U = wl.units
+    buf = _buffers(wl)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    sts = [H.oracle_student(wl, u) for u in range(U)]
+    q, kn, vn = _step_tensors(wl)
+    amb_total = 0
+    for t in range(wl.steps):
+        for u in range(U):
+            H.upload_unit(buf, u, sts[u])
+        H.set_host_fields(buf, sts[0])
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        L = buf.kv.len + 1
+        scores = torch.empty((U, L), dtype=torch.float32, device="cuda")
+        kept = torch.empty((U, min(L, wl.budget)), dtype=torch.int32, device="cuda")
+        out = buf.decode_evict(pol, wl.budget, q, kn, vn, scores_out=scores, kept_out=kept)
+        torch.cuda.synchronize()
+        outn, sc, kp = H.to_np(out), H.to_np(scores), H.to_np(kept)
+        for u in range(U):
+            att = ounit.decode_step(sts[u], *H.step_inputs_np(wl, t, u))
+            assert H.rel_err_rows(outn[u], att.o) <= H.OUT_TOL, (t, u)
+            s_or = ounit.scores(sts[u], pnp, wl.hidden)
+            ok, worst = H.vec_ok(sc[u], s_or)        # uploaded rows are in the oracle's order
+            assert ok, (t, u, "scores", worst)
+            post = H.download_unit(buf, u)
+            ok, amb, flips = H.selection_check(s_or, sts[u].pos, post["pos"], wl.budget)
+            assert ok, (t, u, amb, flips)
+            amb_total += amb
+            pre_pos = sts[u].pos.copy()
+            Z, N = sts[u].hist.sums()
+            pre = {"alpha": sts[u].alpha.copy(), "den": Z, "num": N}
+            ounit.evict(sts[u], s_or, wl.budget)
+            if flips == 0:
+                # the kept rows carry the oracle's post-step features
+                assert np.array_equal(np.sort(post["pos"]), sts[u].pos), (t, u)
+                src = np.searchsorted(pre_pos, post["pos"])
+                for name in ("alpha", "den", "num"):
+                    ok, worst = H.vec_ok(post[name], pre[name][src])
+                    assert ok, (t, u, name, worst)
+            # the slot map is the documented hole-filling compaction of the kept set
+            nk = min(wl.budget, len(pre_pos))
+            kmask = np.zeros(len(pre_pos), bool)
+            kmask[kp[u, :nk]] = True
+            assert np.array_equal(kp[u, :nk], H.hole_fill_layout(pre_pos, kmask, nk)), (t, u)
+    print("ambiguous selections excluded:", amb_total)
