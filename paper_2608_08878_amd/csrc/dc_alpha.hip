@@ -42,7 +42,8 @@ __global__ void __launch_bounds__(GA_AT) ga_add_kernel(GlobalAlphaArgs a, uint64
                                                        int ngrp) {
   extern __shared__ unsigned long long hist[];
   const int tid = threadIdx.x;
-  const int b = blockIdx.y / ngrp, g = blockIdx.y - b * ngrp;
+  const int y = a.y0 + blockIdx.y;
+  const int b = y / ngrp, g = y - b * ngrp;
   const int p0 = blockIdx.x * pw;
   for (int i = tid; i < pw; i += GA_AT) hist[i] = 0ull;
   __syncthreads();
@@ -89,7 +90,7 @@ __global__ void __launch_bounds__(GA_T) ga_sum_kernel(GlobalAlphaArgs a, const u
 }
 
 __global__ void __launch_bounds__(GA_T) ga_write_kernel(GlobalAlphaArgs a) {
-  const int u = blockIdx.y;
+  const int u = a.y0 + blockIdx.y;
   const int L = ga_rows(a, u);
   const uint64_t* acc = a.acc + (size_t)(u / a.per_seq) * a.T;
   const double inv = 1.0 / (GA_ONE * (double)a.per_seq);
@@ -115,13 +116,21 @@ int launch_global_alpha(const GlobalAlphaArgs& a, void* stream) {
   const int pw = ((a.T + nwin - 1) / nwin + 255) / 256 * 256;     // <= GA_PWMAX
   const int lds = pw * (int)sizeof(unsigned long long);
   hipFuncSetAttribute((const void*)ga_add_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-  hipLaunchKernelGGL(ga_add_kernel, dim3(nwin, nseq * ngrp), dim3(GA_AT), lds, s, a, part, pw, ngrp);
+  for_grid_y(nseq * ngrp, [&](int y0, int ny) {
+    GlobalAlphaArgs b = a;
+    b.y0 = y0;
+    hipLaunchKernelGGL(ga_add_kernel, dim3(nwin, ny), dim3(GA_AT), lds, s, b, part, pw, ngrp);
+  });
   const size_t n = (size_t)nseq * a.T;
   const size_t nb = (n + GA_T - 1) / GA_T;
   hipLaunchKernelGGL(ga_sum_kernel, dim3(nb < 8192 ? nb : 8192), dim3(GA_T), 0, s, a,
                      (const uint64_t*)part, ngrp);
   const int gx = (a.len + GA_T - 1) / GA_T;
-  hipLaunchKernelGGL(ga_write_kernel, dim3(gx < 64 ? gx : 64, a.units), dim3(GA_T), 0, s, a);
+  for_grid_y(a.units, [&](int y0, int ny) {
+    GlobalAlphaArgs b = a;
+    b.y0 = y0;
+    hipLaunchKernelGGL(ga_write_kernel, dim3(gx < 64 ? gx : 64, ny), dim3(GA_T), 0, s, b);
+  });
   return (int)hipGetLastError();
 }
 

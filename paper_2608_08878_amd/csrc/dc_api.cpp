@@ -618,6 +618,7 @@ dc_status dc_global_alpha(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, v
   a.len = kv->len;
   a.per_seq = per_seq;
   a.T = feat->next_pos;
+  a.y0 = 0;
   return dc::launch_global_alpha(a, hip_stream) == 0 ? DC_OK : DC_ERR_HIP;
 }
 

@@ -385,7 +385,7 @@ __global__ void __launch_bounds__(NTH) decode_split1_kernel(DecodeArgs a) {
   __shared__ float lds[NWAVE * 3 * G + 3 * G + NWAVE * G * D];
   float* stat = lds;
   float* obuf = lds + NWAVE * 3 * G + 3 * G;
-  const int c = blockIdx.x, u = blockIdx.y;
+  const int c = blockIdx.x, u = a.y0 + blockIdx.y;
   const int r0 = c * a.chunk, r1 = min(a.L, r0 + a.chunk);
   if (c == 0 && a.append) write_append<DTYPE, D>(a, u);
   float* s_sink = FEAT ? a.ws_s + (size_t)u * a.lmax * G : nullptr;
@@ -427,7 +427,7 @@ __global__ void __launch_bounds__(NTH) decode_split1_kernel(DecodeArgs a) {
 template <int DTYPE, int D, int G, bool FEAT>
 __global__ void __launch_bounds__(NTH) decode_split2_kernel(DecodeArgs a) {
   using Q = Geo<DTYPE, D, G>;
-  const int c = blockIdx.x, u = blockIdx.y;
+  const int c = blockIdx.x, u = a.y0 + blockIdx.y;
   const float* parts = a.ws_part + (size_t)u * a.nchunks * Q::PART;
   float fm[G], fl[G], fu[G], invl[G], H[G];
 #pragma unroll
@@ -472,7 +472,7 @@ template <int DTYPE, int D>
 __global__ void __launch_bounds__(256) feat_init_kernel(DecodeArgs a, int first_pos) {
   using R = RowT<DTYPE, D>;
   constexpr int LPR = R::LPR, EPL = R::EPL, ELT = R::ELT;
-  const int u = blockIdx.y;
+  const int u = a.y0 + blockIdx.y;
   const int grp = (blockIdx.x * 256 + threadIdx.x) / LPR, lam = threadIdx.x % LPR;
   const int ngrp = gridDim.x * 256 / LPR;
   for (int i = grp; i < a.L; i += ngrp) {
@@ -520,14 +520,19 @@ static int launch_t(const DecodeArgs& a, bool feat, bool split, hipStream_t s) {
       hipLaunchKernelGGL(k, dim3(a.units), dim3(NTH), lds, s, a);
     }
   } else {
-    dim3 grid(a.nchunks, a.units);
-    if (feat) {
-      hipLaunchKernelGGL((decode_split1_kernel<DTYPE, D, G, true>), grid, dim3(NTH), 0, s, a);
-      hipLaunchKernelGGL((decode_split2_kernel<DTYPE, D, G, true>), grid, dim3(NTH), 0, s, a);
-    } else {
-      hipLaunchKernelGGL((decode_split1_kernel<DTYPE, D, G, false>), grid, dim3(NTH), 0, s, a);
-      hipLaunchKernelGGL((decode_split2_kernel<DTYPE, D, G, false>), grid, dim3(NTH), 0, s, a);
-    }
+    // every slice of pass 1 before pass 2 (stream order)
+    for_grid_y(a.units, [&](int y0, int ny) {
+      DecodeArgs b = a;
+      b.y0 = y0;
+      if (feat) hipLaunchKernelGGL((decode_split1_kernel<DTYPE, D, G, true>), dim3(a.nchunks, ny), dim3(NTH), 0, s, b);
+      else hipLaunchKernelGGL((decode_split1_kernel<DTYPE, D, G, false>), dim3(a.nchunks, ny), dim3(NTH), 0, s, b);
+    });
+    for_grid_y(a.units, [&](int y0, int ny) {
+      DecodeArgs b = a;
+      b.y0 = y0;
+      if (feat) hipLaunchKernelGGL((decode_split2_kernel<DTYPE, D, G, true>), dim3(a.nchunks, ny), dim3(NTH), 0, s, b);
+      else hipLaunchKernelGGL((decode_split2_kernel<DTYPE, D, G, false>), dim3(a.nchunks, ny), dim3(NTH), 0, s, b);
+    });
   }
   return (int)hipGetLastError();
 }
@@ -558,12 +563,16 @@ int launch_feat_init(const DecodeArgs& a, int dtype, int D, int first_pos, void*
   int gx = (a.L + 255) / 256;
   if (gx > 64) gx = 64;
   if (gx < 1) gx = 1;
-  dim3 grid(gx, a.units);
-  if (dtype == 1 && D == 128) hipLaunchKernelGGL((feat_init_kernel<1, 128>), grid, dim3(256), 0, s, a, first_pos);
-  else if (dtype == 1 && D == 64) hipLaunchKernelGGL((feat_init_kernel<1, 64>), grid, dim3(256), 0, s, a, first_pos);
-  else if (dtype == 0 && D == 128) hipLaunchKernelGGL((feat_init_kernel<0, 128>), grid, dim3(256), 0, s, a, first_pos);
-  else if (dtype == 0 && D == 64) hipLaunchKernelGGL((feat_init_kernel<0, 64>), grid, dim3(256), 0, s, a, first_pos);
-  else return (int)hipErrorInvalidValue;
+  if (!((dtype == 0 || dtype == 1) && (D == 64 || D == 128))) return (int)hipErrorInvalidValue;
+  for_grid_y(a.units, [&](int y0, int ny) {
+    DecodeArgs b = a;
+    b.y0 = y0;
+    const dim3 grid(gx, ny);
+    if (dtype == 1 && D == 128) hipLaunchKernelGGL((feat_init_kernel<1, 128>), grid, dim3(256), 0, s, b, first_pos);
+    else if (dtype == 1 && D == 64) hipLaunchKernelGGL((feat_init_kernel<1, 64>), grid, dim3(256), 0, s, b, first_pos);
+    else if (dtype == 0 && D == 128) hipLaunchKernelGGL((feat_init_kernel<0, 128>), grid, dim3(256), 0, s, b, first_pos);
+    else hipLaunchKernelGGL((feat_init_kernel<0, 64>), grid, dim3(256), 0, s, b, first_pos);
+  });
   return (int)hipGetLastError();
 }
 

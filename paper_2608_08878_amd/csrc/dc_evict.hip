@@ -64,7 +64,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
 
 // Long caches: scores to keys in the workspace (grid over rows) ...
 __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys, int kstride) {
-  const int u = blockIdx.y;
+  const int u = a.y0 + blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = unit_rows(a, u);
@@ -85,7 +85,7 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
 // Extended one-hidden-layer policies: the same grid over rows, the out-of-line
 // MLP per row.
 __global__ void __launch_bounds__(256) score_ext_kernel(EvictArgs a, uint64_t* keys, int kstride) {
-  const int u = blockIdx.y;
+  const int u = a.y0 + blockIdx.y;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = unit_rows(a, u);
@@ -151,12 +151,14 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
   if (a.ext && a.nh == 2) {
     const int rc = launch_score_mlp2(b, ws_keys, kstride, s);
     if (rc) return rc;
-  } else if (a.ext) {
-    hipLaunchKernelGGL(score_ext_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
-                       ws_keys, kstride);
   } else {
-    hipLaunchKernelGGL(score_kernel, dim3((a.L + 255) / 256, a.units), dim3(256), 0, s, b,
-                       ws_keys, kstride);
+    for_grid_y(a.units, [&](int y0, int ny) {
+      EvictArgs c = b;
+      c.y0 = y0;
+      const dim3 grid((a.L + 255) / 256, ny);
+      if (a.ext) hipLaunchKernelGGL(score_ext_kernel, grid, dim3(256), 0, s, c, ws_keys, kstride);
+      else hipLaunchKernelGGL(score_kernel, grid, dim3(256), 0, s, c, ws_keys, kstride);
+    });
   }
   if (a.evict || ragged) {
     auto k = select_kernel<DTYPE, D>;

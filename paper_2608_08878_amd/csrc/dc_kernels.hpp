@@ -40,6 +40,7 @@ struct DecodeArgs {
   float* ws_r;          // [units][lmax][2] retired contributions
   float* ws_v;          // [units][lmax] value norms
   float* ws_part;       // [units][nchunks][3G + G*D] per-chunk softmax partials
+  int y0;               // first unit of a launch whose grid rows are units (see for_grid_y)
   int lmax;             // row stride of the scratch per unit: L + 8 rounded up to 32 (rows
                         // past L are padding that absorbs the stores of lanes without a row)
   int chunk;
@@ -74,6 +75,7 @@ struct EvictArgs {
   int evict;            // 1 if rows are removed
   uint64_t* ws_keys;    // [units][kstride] row keys (long caches only)
   int mv_ints;          // ints of the compaction move list at the start of the dynamic LDS
+  int y0;               // first unit of a launch whose grid rows are units (see for_grid_y)
                         // (the two-hidden-layer policy's weights follow it); set by the launchers
   int sample;           // 1: rank by the Gumbel-perturbed score s / tau + g (training mode)
   float tau;            // sampling temperature
@@ -131,7 +133,17 @@ struct GlobalAlphaArgs {
   int len;                  // rows per unit (bound with unit_len)
   int per_seq;              // units per sequence (n_layers x n_kv_heads)
   int T;                    // positions 0..T-1
+  int y0;                   // first grid row of the launch (see for_grid_y)
 };
+
+// Grids whose rows are units (or unit groups) are launched in slices of at
+// most MAX_GRID_Y rows (the hardware limit of a grid's y dimension): f(y0, ny)
+// launches rows y0 .. y0 + ny - 1, the kernel adding y0 to blockIdx.y.
+constexpr int MAX_GRID_Y = 65535;
+template <typename F>
+inline void for_grid_y(int n, F&& f) {
+  for (int y0 = 0; y0 < n; y0 += MAX_GRID_Y) f(y0, n - y0 < MAX_GRID_Y ? n - y0 : MAX_GRID_Y);
+}
 
 // Launchers return a hipError_t value (0 on success).
 int launch_decode(const DecodeArgs& a, int dtype, int D, int G, bool feat, bool split,

@@ -107,7 +107,7 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
   extern __shared__ float sm[];
   stage<HP>(a, sm);
   __syncthreads();
-  const int u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ri = lane & 15, kg = lane >> 4;
   const int h1 = a.h1, h2 = a.h2, ln = a.ln;
   const int L = unit_rows(a, u);   // this unit's rows (scores_out keeps stride a.L)
@@ -252,12 +252,16 @@ int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* str
   const void* k = narrow ? (const void*)score_mlp2_kernel<64, 3> : (const void*)score_mlp2_kernel<128, 2>;
   const size_t lds = (size_t)(narrow ? Lay<64>::FLOATS : Lay<128>::FLOATS) * sizeof(float);
   hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (narrow)
-    hipLaunchKernelGGL((score_mlp2_kernel<64, 3>), dim3(gx, a.units), dim3(MT), lds,
-                       (hipStream_t)stream, a, keys, kstride);
-  else
-    hipLaunchKernelGGL((score_mlp2_kernel<128, 2>), dim3(gx, a.units), dim3(MT), lds,
-                       (hipStream_t)stream, a, keys, kstride);
+  for_grid_y(a.units, [&](int y0, int ny) {
+    EvictArgs b = a;
+    b.y0 = y0;
+    if (narrow)
+      hipLaunchKernelGGL((score_mlp2_kernel<64, 3>), dim3(gx, ny), dim3(MT), lds, (hipStream_t)stream,
+                         b, keys, kstride);
+    else
+      hipLaunchKernelGGL((score_mlp2_kernel<128, 2>), dim3(gx, ny), dim3(MT), lds, (hipStream_t)stream,
+                         b, keys, kstride);
+  });
   return (int)hipGetLastError();
 }
 

@@ -719,7 +719,7 @@ __global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArg
 template <int D, int G, bool FEAT>
 __global__ void __launch_bounds__(SNT) stepc_a_kernel(DecodeArgs a) {
   __shared__ float stat[SNW * 2 * G + 2 * G];
-  const int c = blockIdx.x, u = blockIdx.y;
+  const int c = blockIdx.x, u = a.y0 + blockIdx.y;
   const int Lu = len_old_of(a, u) + a.append;       // this unit's rows (ragged caches: per unit)
   const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk);
   if (c == 0 && a.append) append_rows<D>(a, u);
@@ -765,7 +765,7 @@ __global__ void __launch_bounds__(SNT) stepc_b_kernel(DecodeArgs a) {
   __shared__ float pbuf[SCHUNK * G];
   __shared__ float obuf[SNW * G * D];
   __shared__ float stat[SNW * 2 * G + 2 * G];
-  const int c = blockIdx.x, u = blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int c = blockIdx.x, u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Lu = len_old_of(a, u) + a.append;
   const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk), n = r1 - r0;
   if (n <= 0) {
@@ -810,7 +810,7 @@ __global__ void __launch_bounds__(SNT) stepc_b_kernel(DecodeArgs a) {
 template <int D, int G, bool FEAT>
 __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
   __shared__ float newnorm_slot;
-  const int c = blockIdx.x, u = blockIdx.y, tid = threadIdx.x;
+  const int c = blockIdx.x, u = a.y0 + blockIdx.y, tid = threadIdx.x;
   const int Lu = len_old_of(a, u) + a.append;
   const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk);
   const int PART = 3 * G + G * D;
@@ -929,12 +929,24 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
     else if (a.sigma) pick(step_unit_kernel<D, G, true, false, true>);
     else pick(step_unit_kernel<D, G, true, false>);
   } else {
-    dim3 grid(a.nchunks, a.units);
-    if (feat) hipLaunchKernelGGL((stepc_a_kernel<D, G, true>), grid, dim3(SNT), 0, s, a);
-    else hipLaunchKernelGGL((stepc_a_kernel<D, G, false>), grid, dim3(SNT), 0, s, a);
-    hipLaunchKernelGGL((stepc_b_kernel<D, G>), grid, dim3(SNT), 0, s, a);
-    if (feat) hipLaunchKernelGGL((stepc_d_kernel<D, G, true>), grid, dim3(SNT), 0, s, a);
-    else hipLaunchKernelGGL((stepc_d_kernel<D, G, false>), grid, dim3(SNT), 0, s, a);
+    // every slice of one pass before the next (stream order)
+    for_grid_y(a.units, [&](int y0, int ny) {
+      DecodeArgs b = a;
+      b.y0 = y0;
+      if (feat) hipLaunchKernelGGL((stepc_a_kernel<D, G, true>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      else hipLaunchKernelGGL((stepc_a_kernel<D, G, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+    });
+    for_grid_y(a.units, [&](int y0, int ny) {
+      DecodeArgs b = a;
+      b.y0 = y0;
+      hipLaunchKernelGGL((stepc_b_kernel<D, G>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+    });
+    for_grid_y(a.units, [&](int y0, int ny) {
+      DecodeArgs b = a;
+      b.y0 = y0;
+      if (feat) hipLaunchKernelGGL((stepc_d_kernel<D, G, true>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      else hipLaunchKernelGGL((stepc_d_kernel<D, G, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+    });
   }
   return (int)hipGetLastError();
 }
