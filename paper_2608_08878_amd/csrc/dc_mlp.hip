@@ -116,19 +116,39 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
   const float invT = 1.0f / (float)a.T;
   const float bout = const_params(a.params)[h1 * a.n_in + h1 + (ln ? 2 * h1 : 0) + h2 * h1 + h2 +
                                             (ln ? 2 * h2 : 0) + h2];
-  for (int rb = (blockIdx.x * MW + wave) * 16; rb < L; rb += gridDim.x * MW * 16) {
-    // features of this lane's A row (the four lanes of a row load the same row)
-    const int r = rb + ri;
-    const size_t gi = ub + (r < L ? r : L - 1);
+  // features of this lane's A row (the four lanes of a row load the same row);
+  // the next row block's are requested while the current one is computed
+  struct Feat {
+    double num, den;
+    int32_t pos;
+    float al, vn, sg;
+  };
+  const float* sig = a.n_in == 5 ? a.sigma : a.alpha;   // (a dummy read for four inputs)
+  auto fetch = [&](int rbx, Feat& f) {
+    const int r = rbx + ri;
+    const size_t gi = ub + (r < L ? r : L - 1);             // past the end: re-read, unused
+    f.num = a.num[gi];
+    f.den = a.den[gi];
+    f.pos = a.pos[gi];
+    f.al = a.alpha[gi];
+    f.vn = a.vnorm[gi];
+    f.sg = sig[gi];
+  };
+  const int stride = gridDim.x * MW * 16;
+  int rb = (blockIdx.x * MW + wave) * 16;
+  Feat nxt;
+  fetch(rb, nxt);
+  for (; rb < L; rb += stride) {
+    const Feat f = nxt;
+    fetch(rb + stride, nxt);
     float x[NX];
     {
-      const double num = a.num[gi], den = a.den[gi];
-      const float H = den > 0.0 ? (float)(num / den) : 0.0f;
-      const float ps = (float)a.pos[gi] * invT;
-      x[0] = a.alpha[gi];
-      x[1] = a.vnorm[gi];
+      const float H = f.den > 0.0 ? (float)(f.num / f.den) : 0.0f;
+      const float ps = (float)f.pos * invT;
+      x[0] = f.al;
+      x[1] = f.vn;
       if (a.n_in == 5) {
-        x[2] = a.sigma[gi];
+        x[2] = f.sg;
         x[3] = H;
         x[4] = ps;
       } else {
