@@ -247,14 +247,15 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
       }
       score[i] = sum16(o) + bout;
     }
-    // lanes ri < 4 of each row group write rows 4 kg + ri
+    // lanes ri < 4 of each row group write rows 4 kg + ri; lane 4 kg + ri
+    // loaded that row's position with its features
+    const int32_t p = __shfl(f.pos, 4 * kg + (ri & 3));
     if (ri < 4) {
       const int row = rb + 4 * kg + ri;
       float sc = score[0];
 #pragma unroll
       for (int i = 1; i < 4; ++i) sc = ri == i ? score[i] : sc;
       if (row < L) {
-        const int32_t p = a.pos[ub + row];
         if (a.scores_out) a.scores_out[(size_t)u * a.L + row] = sc;
         keys[(size_t)u * kstride + row] = row_key(a.sample ? sampled_score(a, sc, p, u) : sc, p);
       }
