@@ -1,6 +1,8 @@
 // Scoring, top-B selection and hole-filling compaction shared by the
 // stand-alone score/evict kernels and the fused decode+evict kernel.
 #pragma once
+#include <type_traits>
+
 #include "dc_device.hpp"
 #include "dc_kernels.hpp"
 
@@ -223,6 +225,21 @@ struct MemKeys {
   __device__ uint64_t get(int k) const { return key[k * ENT + threadIdx.x]; }
 };
 
+// The keys of rows k*NT + tid for k in [k0, k0 + 8) from the workspace, requested
+// together (eight loads in flight instead of one at a time); rows past L (and k
+// past kpt) read as ~0, which no selection takes.
+template <typename Keys, int NT>
+__device__ __forceinline__ void key_batch(const Keys& keys, int k0, int kpt, int L, uint64_t (&x)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int r = (k0 + j) * NT + (int)threadIdx.x;
+    x[j] = keys.key[r < L ? r : L - 1];                // unconditional, in bounds
+  }
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+    if (k0 + j >= kpt || (k0 + j) * NT + (int)threadIdx.x >= L) x[j] = ~0ull;
+}
+
 // ... or in LDS (fused decode+evict kernel).
 // Keys in LDS at a row stride of `stride` u64 (rows k * NT + tid).
 template <int KM, int NT>
@@ -298,6 +315,7 @@ template <typename Keys, int DTYPE, int D, int NT = ENT>
 __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Keys& keys, int kpt,
                                SelShared& sh, int* mv) {
   constexpr int ELT = DTYPE == 0 ? 4 : 2;
+  constexpr bool GLOBAL_KEYS = std::is_same<Keys, MemKeys>::value;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int E = L - B;
   const size_t ub = (size_t)u * a.cap;
@@ -305,27 +323,46 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
   uint64_t thr;
   if (E == 1) {
     uint64_t m = ~0ull;
+    int mr = -1;                        // (global keys) the row of this thread's minimum
+    if constexpr (GLOBAL_KEYS) {
+      for (int k0 = 0; k0 < kpt; k0 += 8) {
+        uint64_t x[8];
+        key_batch<Keys, NT>(keys, k0, kpt, L, x);
 #pragma unroll
-    for (int k = 0; k < Keys::KMAX; ++k) {
-      if (k >= kpt) break;
-      const int r = k * NT + tid;
-      if (r < L) {
-        const uint64_t x = keys.get(k);
-        m = x < m ? x : m;
+        for (int j = 0; j < 8; ++j)
+          if (x[j] < m) {
+            m = x[j];
+            mr = (k0 + j) * NT + tid;
+          }
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < Keys::KMAX; ++k) {
+        if (k >= kpt) break;
+        const int r = k * NT + tid;
+        if (r < L) {
+          const uint64_t x = keys.get(k);
+          m = x < m ? x : m;
+        }
       }
     }
+    const uint64_t mine = m;
     m = wave_min(m);
     if (lane == 0) sh.wmin[wave] = m;
     __syncthreads();
     thr = sh.wmin[0];
     for (int w = 1; w < NT / 64; ++w) thr = sh.wmin[w] < thr ? sh.wmin[w] : thr;
     // one row leaves: if it sits below B, the row in slot B (the only slot >= B)
-    // fills it; no scans needed
+    // fills it; no scans needed.  Keys are unique, so exactly one row holds thr.
+    if constexpr (GLOBAL_KEYS) {
+      if (mr >= 0 && mine == thr) sh.sel[3] = mr;
+    } else {
 #pragma unroll
-    for (int k = 0; k < Keys::KMAX; ++k) {
-      if (k >= kpt) break;
-      const int r = k * NT + tid;
-      if (r < L && keys.get(k) == thr) sh.sel[3] = r;
+      for (int k = 0; k < Keys::KMAX; ++k) {
+        if (k >= kpt) break;
+        const int r = k * NT + tid;
+        if (r < L && keys.get(k) == thr) sh.sel[3] = r;
+      }
     }
     __syncthreads();
     const int ev = sh.sel[3];
@@ -359,13 +396,24 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
       const uint64_t hmask = shift + 8 >= 64 ? 0ull : (~0ull << (shift + 8));
       for (int i = tid; i < 256; i += NT) sh.hist[i] = 0;
       __syncthreads();
+      if constexpr (GLOBAL_KEYS) {
+        for (int k0 = 0; k0 < kpt; k0 += 8) {
+          uint64_t x[8];
+          key_batch<Keys, NT>(keys, k0, kpt, L, x);
 #pragma unroll
-      for (int k = 0; k < Keys::KMAX; ++k) {
-        if (k >= kpt) break;
-        const int r = k * NT + tid;
-        if (r < L) {
-          const uint64_t x = keys.get(k);
-          if ((x & hmask) == prefix) atomicAdd(&sh.hist[(int)((x >> shift) & 255u)], 1);
+          for (int j = 0; j < 8; ++j)
+            if (k0 + j < kpt && (k0 + j) * NT + tid < L && (x[j] & hmask) == prefix)
+              atomicAdd(&sh.hist[(int)((x[j] >> shift) & 255u)], 1);
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < Keys::KMAX; ++k) {
+          if (k >= kpt) break;
+          const int r = k * NT + tid;
+          if (r < L) {
+            const uint64_t x = keys.get(k);
+            if ((x & hmask) == prefix) atomicAdd(&sh.hist[(int)((x >> shift) & 255u)], 1);
+          }
         }
       }
       __syncthreads();
@@ -398,12 +446,7 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
   // plan: holes (evicted, slot < B) take movers (kept, slot >= B) in order
   if (tid == 0) sh.nmoves = 0;
   int run0 = 0, run1 = 0;
-#pragma unroll
-  for (int k = 0; k < Keys::KMAX; ++k) {
-    if (k >= kpt || k * NT >= L) break;
-    const int r = k * NT + tid;
-    bool ev = false;
-    if (r < L) ev = keys.get(k) <= thr;
+  auto plan_row = [&](int r, bool ev) {
     const bool hole = r < B && ev;
     const bool mover = r >= B && r < L && !ev;
     int rk0, rk1, t0, t1;
@@ -413,29 +456,85 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
     if (a.kept_out && r < B && !ev) a.kept_out[(size_t)u * a.ld_kept + r] = r;
     run0 += t0;
     run1 += t1;
+  };
+  if constexpr (GLOBAL_KEYS) {
+    for (int k0 = 0; k0 < kpt && k0 * NT < L; k0 += 8) {
+      uint64_t x[8];
+      key_batch<Keys, NT>(keys, k0, kpt, L, x);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = k0 + j;
+        if (k >= kpt || k * NT >= L) break;
+        const int r = k * NT + tid;
+        plan_row(r, r < L && x[j] <= thr);
+      }
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < Keys::KMAX; ++k) {
+      if (k >= kpt || k * NT >= L) break;
+      const int r = k * NT + tid;
+      bool ev = false;
+      if (r < L) ev = keys.get(k) <= thr;
+      plan_row(r, ev);
+    }
   }
   __syncthreads();
   const int nm = run0;  // == run1
-  // copy rows: one 16-lane group per move
-  constexpr int N16 = D * ELT / 16;  // 16-byte chunks per row (8 or 16)
+  // copy rows: one 16-lane group per move, MB moves per trip with every load
+  // issued before the stores (moves are independent: sources and destinations
+  // are disjoint); lane gl of a group also carries state field gl
+  constexpr int N16 = D * ELT / 16;        // 16-byte chunks per row (8, 16 or 32)
+  constexpr int CPL = (N16 + 15) / 16;     // chunks per lane
+  constexpr int MB = 4;
   const int grp = tid / 16, gl = tid % 16, ngrp = NT / 16;
-  for (int j = grp; j < nm; j += ngrp) {
-    const int dst = mv[2 * j], src = mv[2 * j + 1];
-    const size_t gd = ub + dst, gs = ub + src;
-    char* kb = (char*)a.k;
-    char* vb = (char*)a.v;
-    for (int c = gl; c < N16; c += 16) {
-      *reinterpret_cast<uint4*>(kb + gd * D * ELT + c * 16) = ldg16(kb + gs * D * ELT + c * 16);
-      *reinterpret_cast<uint4*>(vb + gd * D * ELT + c * 16) = ldg16(vb + gs * D * ELT + c * 16);
+  char* kb = (char*)a.k;
+  char* vb = (char*)a.v;
+  for (int j0 = grp; j0 < nm; j0 += MB * ngrp) {
+    size_t gd[MB], gs[MB];
+    bool ok[MB];
+    uint4 kx[MB][CPL], vx[MB][CPL];
+    uint64_t sv[MB];
+#pragma unroll
+    for (int q = 0; q < MB; ++q) {
+      const int j = j0 + q * ngrp;
+      ok[q] = j < nm;
+      const int jj = ok[q] ? j : j0;         // past the list: re-read a listed move, no store
+      gd[q] = ub + mv[2 * jj];
+      gs[q] = ub + mv[2 * jj + 1];
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = gl + 16 * cc < N16 ? gl + 16 * cc : N16 - 1;
+        kx[q][cc] = ldg16(kb + gs[q] * D * ELT + c * 16);
+        vx[q][cc] = ldg16(vb + gs[q] * D * ELT + c * 16);
+      }
+      sv[q] = 0;
+      if (gl == 0) sv[q] = __float_as_uint(a.alpha[gs[q]]);
+      else if (gl == 1) sv[q] = (uint64_t)__double_as_longlong(a.num[gs[q]]);
+      else if (gl == 2) sv[q] = (uint64_t)__double_as_longlong(a.den[gs[q]]);
+      else if (gl == 3) sv[q] = (uint32_t)a.pos[gs[q]];
+      else if (gl == 4) sv[q] = __float_as_uint(a.vnorm[gs[q]]);
+      else if (gl == 5 && a.sigma) sv[q] = __float_as_uint(a.sigma[gs[q]]);
     }
-    if (gl == 0) {
-      a.alpha[gd] = a.alpha[gs];
-      a.num[gd] = a.num[gs];
-      a.den[gd] = a.den[gs];
-      a.pos[gd] = a.pos[gs];
-      a.vnorm[gd] = a.vnorm[gs];
-      if (a.sigma) a.sigma[gd] = a.sigma[gs];
-      if (a.kept_out) a.kept_out[(size_t)u * a.ld_kept + dst] = src;
+#pragma unroll
+    for (int q = 0; q < MB; ++q) {
+      if (!ok[q]) continue;
+#pragma unroll
+      for (int cc = 0; cc < CPL; ++cc) {
+        const int c = gl + 16 * cc;
+        if (c < N16) {
+          *reinterpret_cast<uint4*>(kb + gd[q] * D * ELT + c * 16) = kx[q][cc];
+          *reinterpret_cast<uint4*>(vb + gd[q] * D * ELT + c * 16) = vx[q][cc];
+        }
+      }
+      if (gl == 0) a.alpha[gd[q]] = __uint_as_float((uint32_t)sv[q]);
+      else if (gl == 1) a.num[gd[q]] = __longlong_as_double((long long)sv[q]);
+      else if (gl == 2) a.den[gd[q]] = __longlong_as_double((long long)sv[q]);
+      else if (gl == 3) a.pos[gd[q]] = (int32_t)(uint32_t)sv[q];
+      else if (gl == 4) a.vnorm[gd[q]] = __uint_as_float((uint32_t)sv[q]);
+      else if (gl == 5 && a.sigma) a.sigma[gd[q]] = __uint_as_float((uint32_t)sv[q]);
+      else if (gl == 6 && a.kept_out)
+        a.kept_out[(size_t)u * a.ld_kept + (int)(gd[q] - ub)] = (int)(gs[q] - ub);
     }
   }
 }
