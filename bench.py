@@ -124,6 +124,33 @@ def _events(n):
     return [torch.cuda.Event(enable_timing=True) for _ in range(n)]
 
 
+def _load_compression_kernels(wl, cap, pol, dev, sample=None):
+    """A kernel's first launch also loads its code (milliseconds).  Run the
+    compression step once on a one-unit cache of the same length, so that the
+    reported step 0 is the GPU's work on the workload."""
+    import torch
+    from paper_2608_08878_amd.buffers import DecodeBuffers
+    from paper_2608_08878_amd import binding as B
+    G, D = wl.group, wl.head_dim
+    td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    one = DecodeBuffers(1, 1, G, 1, D, cap, wl.dtype, wl.ent_window)
+    one.reserve_workspace(cap)
+    one.feat_init(wl.n0, 0)
+    q = torch.zeros((1, G, D), dtype=td, device=dev)
+    kn = torch.zeros((1, D), dtype=td, device=dev)
+    if sample is None:
+        one.decode_evict(pol, wl.budget, q, kn, kn.clone())
+    else:
+        L = wl.n0 + 1
+        sc = torch.empty((1, L), dtype=torch.float32, device=dev)
+        kp = torch.empty((1, wl.budget), dtype=torch.int32, device=dev)
+        lp = torch.empty(1, dtype=torch.float64, device=dev)
+        one.decode_sample_evict(pol, wl.budget, B.make_gumbel(1.0, sample, 0), q, kn, kn.clone(),
+                                None, sc, kp, lp)
+    torch.cuda.synchronize()
+    del one
+
+
 def bench_single_step(args, wl, dev, log):
     """Workload 1: one step (attention, features, score, top-B, compaction) over a
     512-row fp32 cache, no append.  Each repetition starts from the same state
@@ -193,6 +220,7 @@ def bench_periodic_evict(args, wl, dev, log):
         sg.queries(wl, t, q[t])
         sg.new_rows(wl, t, kn[t], vn[t], U)
     out = torch.empty((U, G, D), dtype=torch.bfloat16, device=dev)
+    _load_compression_kernels(wl, cap, pol, dev)
     torch.cuda.synchronize()
     a, b = _events(2)
     a.record()
@@ -281,6 +309,15 @@ def bench_teacher_student_kl(args, wl, dev, log):
         sc_flat = torch.empty(U * (wl.n0 + 1), dtype=torch.float32, device=dev)
         kept = torch.empty((U, wl.budget), dtype=torch.int32, device=dev)
         logp = torch.empty(U, dtype=torch.float64, device=dev)
+    # load step 0's kernels (student compression, teacher, KL) before timing it
+    _load_compression_kernels(wl, wl.n0 + 1, pol, dev, sample=wl.seed if train else None)
+    nt = 128                   # enough units for the teacher's one-workgroup-per-unit path
+    one_t = DecodeBuffers(nt, 1, G, 1, D, wl.n0 + 2, wl.dtype, wl.ent_window, features=False)
+    one_t.kv.len = wl.n0
+    one_t.decode_step(q[:nt], kn[:nt], vn[:nt], features=False)
+    B.dc_kl_reward(rows, hid, voc, hf[0], hc[0], w, kl, ws, ws.numel(), sh)
+    torch.cuda.synchronize()
+    del one_t
     for t in range(nsteps):
         sg.queries(wl, t, q)
         sg.new_rows(wl, t, kn, vn, U)
@@ -684,6 +721,7 @@ def main():
     log(f"setup {time.time() - t0:.1f}s: {U} units, cache {buf.k.numel() * elt * 2 / 1e9:.1f} GB")
 
     # step 0: compression n0+1 -> budget (reported separately)
+    _load_compression_kernels(wl, cap, pol, dev)
     e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
     e0.record()
     buf.decode_evict(pol, wl.budget, Q[0], KN[0], VN[0], out)
