@@ -110,3 +110,18 @@ def test_kl_reward_does_not_depend_on_the_rows_per_call():
     step = _kl_gpu(8, hid, voc, hf[96:104].contiguous(), hc[96:104].contiguous(), w)
     assert np.array_equal(wide[:100], narrow)
     assert np.array_equal(wide[96:104], step)
+
+
+def test_kl_reward_at_the_maximum_row_count():
+    """DC_KL_MAX_ROWS rows in one call (256 row blocks of the GEMM); sampled rows
+    against the oracle, including the last."""
+    rows, hid, voc = B.KL_MAX_ROWS, 256, 1024
+    g = torch.Generator(device="cpu").manual_seed(16384)
+    hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
+    hc = (hf.float() + 0.2 * torch.randn(rows, hid, generator=g)).to(torch.bfloat16)
+    w = (0.1 * torch.randn(voc, hid, generator=g)).to(torch.bfloat16)
+    got = _kl_gpu(rows, hid, voc, hf.cuda(), hc.cuda(), w.cuda())
+    idx = [0, 1, 63, 64, 8191, 12345, rows - 65, rows - 1]
+    ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], w.float().numpy())
+    assert _kl_ok(got[idx], ref), (got[idx], ref)
+    assert np.all(got >= 0) and np.all(np.isfinite(got))
