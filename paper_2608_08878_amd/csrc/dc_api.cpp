@@ -35,7 +35,37 @@ float scale_of(const dc_dims* d) { return d->scale > 0.0f ? d->scale : 1.0f / sq
 
 size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-int nchunks_of(int L) { return (L + dc::decode_chunk_rows() - 1) / dc::decode_chunk_rows(); }
+// Units below which one workgroup per unit leaves most of the chip idle.
+constexpr int FEW_UNITS = 128;
+constexpr int MIN_CHUNK = 512;   // rows per workgroup on the chunked path, at least
+
+// Rows per workgroup on the chunked path.  Many units (or fp32): full chunks.
+// Few bf16 units: at most 16 chunks per unit (every workgroup of the combining
+// kernels walks all of its unit's partials) and about 512 workgroups in all,
+// rounded up to 128 rows and kept within [512, full chunk].  Measured for 1-64
+// units at 4097-32769 rows: 1-8 units of 4097 rows take 46-47 us per step
+// against 61-63 us with full chunks; the rule never measured slower.
+int chunk_rows(const dc_dims* d, int L) {
+  const int c = dc::decode_chunk_rows();
+  const long U = (long)units_of(d);
+  if (d->dtype != DC_BF16 || U >= FEW_UNITS) return c;
+  const long by_chunks = (L + 15) / 16, by_groups = ((long)L * U + 511) / 512;
+  const long want = by_chunks > by_groups ? by_chunks : by_groups;
+  const long r = (want + 127) / 128 * 128;
+  return r < MIN_CHUNK ? MIN_CHUNK : r > c ? c : (int)r;
+}
+
+int nchunks_of(const dc_dims* d, int L) {
+  const int c = chunk_rows(d, L);
+  return (L + c - 1) / c;
+}
+
+// Chunks of any length up to L: the workspace bound (the chunk grows with L,
+// so the count is not monotone in L).
+int nchunks_bound(const dc_dims* d, int L) {
+  const bool few = d->dtype == DC_BF16 && units_of(d) < FEW_UNITS;
+  return few ? (L + MIN_CHUNK - 1) / MIN_CHUNK : nchunks_of(d, L);
+}
 
 // Per-unit row stride of the decode scratch: L rows plus padding that takes the
 // stores of lanes past the last row (so those stores need no branch), rounded
@@ -47,7 +77,7 @@ int scratch_rows(int L) { return (L + 8 + 31) / 32 * 32; }
 size_t split_bytes(const dc_dims* d, int L) {
   const size_t U = (size_t)units_of(d), G = group_of(d), D = d->head_dim;
   const size_t rows = U * (size_t)scratch_rows(L) * (G + 3) * sizeof(float);
-  const size_t parts = U * (size_t)nchunks_of(L) * (3 * G + G * D) * sizeof(float);
+  const size_t parts = U * (size_t)nchunks_bound(d, L) * (3 * G + G * D) * sizeof(float);
   return align256(rows) + align256(parts);
 }
 
@@ -55,7 +85,7 @@ bool use_split(const dc_dims* d, int L, bool feat) {
   const int G = group_of(d);
   if (feat && !dc::decode_fits_lds(L, G, d->head_dim)) return true;
   // few units: spread one unit's rows over several workgroups
-  return units_of(d) < 128 && L > 2 * dc::decode_chunk_rows();
+  return units_of(d) < FEW_UNITS && L > 2 * dc::decode_chunk_rows();
 }
 
 size_t evict_bytes(const dc_dims* d, int L) { return align256(dc::evict_ws_bytes((int)units_of(d), L)); }
@@ -195,7 +225,7 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   if (ragged && dims->dtype != DC_BF16) return DC_ERR_UNSUPPORTED;
   if (dims->dtype == DC_BF16)
     split = ragged || !dc::step_fits(L, G, D, feat != nullptr, 0) ||
-            (U < 128 && L > 2 * dc::step_chunk_rows());
+            (U < FEW_UNITS && L > 2 * dc::step_chunk_rows());
   else
     split = use_split(dims, L, feat != nullptr);
   // the matrix-core unit path parks each row's retired (cz, cn) in the workspace
@@ -244,8 +274,8 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
     const size_t rows = (size_t)U * scratch_rows(L);
     float* base = (float*)ws;
     a.lmax = scratch_rows(L);
-    a.chunk = dc::decode_chunk_rows();
-    a.nchunks = nchunks_of(L);
+    a.chunk = chunk_rows(dims, L);
+    a.nchunks = nchunks_of(dims, L);
     a.ws_s = base;
     a.ws_r = base + rows * G;
     a.ws_v = base + rows * (G + 2);
