@@ -620,3 +620,79 @@ def test_fused_step_across_head_groups_and_dims(n_q, n_kv, d):
             kmask[kp[u, :nk]] = True
             assert np.array_equal(kp[u, :nk], H.hole_fill_layout(pre_pos, kmask, nk)), (t, u)
     print("ambiguous selections excluded:", amb_total)
+
+
+@pytest.mark.parametrize("dtype,head_dim,mode", [("bf16", 128, "one_launch"),
+                                                 ("bf16", 128, "two_calls"),
+                                                 ("f32", 64, "one_launch")])
+def test_decode_from_an_empty_cache(dtype, head_dim, mode):
+    """The first append onto an empty cache (one row: weight 1, entropy 0), then
+    caches shorter than one 16-row tile while they grow to the budget of 6
+    (no eviction: every row kept), then one eviction per step, past step 64
+    where the entropy window starts to retire.  Device and oracle run their
+    own trajectories and must agree until a selection lands in the near-tie band."""
+    budget = 6
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=2, n_q_heads=8, n0=0, budget=budget, steps=80,
+                               dtype=dtype, head_dim=head_dim)
+    U = wl.units
+    buf = _buffers(wl)
+    buf.reserve_workspace(wl.capacity)
+    buf.feat_init(0, 0)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    sts = [H.oracle_student(wl, u) for u in range(U)]
+    assert all(st.L == 0 for st in sts)
+    q, kn, vn = _step_tensors(wl)
+    slot_pos = [np.zeros(0, np.int64) for _ in range(U)]    # device slot order before the step
+    print(f"empty cache: {dtype} d={head_dim} {mode}", flush=True)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        L = buf.kv.len + 1
+        scores = torch.empty((U, L), dtype=torch.float32, device="cuda")
+        kept = torch.empty((U, min(L, budget)), dtype=torch.int32, device="cuda")
+        if mode == "one_launch":
+            out = buf.decode_evict(pol, budget, q, kn, vn, scores_out=scores, kept_out=kept)
+        else:
+            out = buf.decode_step(q, kn, vn)
+            buf.score_evict(pol, budget, scores, kept)
+        torch.cuda.synchronize()
+        assert buf.kv.len == min(L, budget)
+        outn, sc, kp = H.to_np(out), H.to_np(scores), H.to_np(kept)
+        diverged = False
+        for u in range(U):
+            st = sts[u]
+            att = ounit.decode_step(st, *H.step_inputs_np(wl, t, u))
+            assert H.rel_err_rows(outn[u], att.o) <= H.OUT_TOL, (t, u)
+            if t == 0:
+                assert np.allclose(att.o, st.V[0][None, :].repeat(wl.group, 0))   # one row: its value
+            s_or = ounit.scores(st, pnp, wl.hidden)
+            dev_pos = np.append(slot_pos[u], t)                 # the appended row takes the last slot
+            o_dev, o_or = np.argsort(dev_pos), np.argsort(st.pos)
+            assert np.array_equal(dev_pos[o_dev], st.pos[o_or]), (t, u)
+            ok, worst = H.vec_ok(sc[u][o_dev], s_or[o_or])
+            assert ok, (t, u, "scores", worst)
+            assert np.array_equal(np.sort(dev_pos[kp[u]]), np.sort(
+                H.download_unit(buf, u)["pos"])), (t, u, "kept_out names the kept rows")
+            post = H.download_unit(buf, u)
+            ok, amb, flips = H.selection_check(s_or, st.pos, post["pos"], budget)
+            assert ok, (t, u, amb, flips)
+            diverged |= flips > 0
+            pre_pos = st.pos.copy()
+            ounit.evict(st, s_or, budget)
+            if flips == 0:
+                Z, N = st.hist.sums()
+                pb = H.by_position(post)
+                o = np.argsort(st.pos)
+                assert np.array_equal(pb["pos"], st.pos[o]), (t, u)
+                for name, ref in (("k", st.K), ("v", st.V)):
+                    assert H.rel_err_rows(pb[name], ref[o]) <= H.OUT_TOL, (t, u, name)
+                for name, ref in (("alpha", st.alpha), ("den", Z), ("num", N),
+                                  ("vnorm", np.sqrt((st.V ** 2).sum(1)))):
+                    ok, worst = H.vec_ok(pb[name], ref[o])
+                    assert ok, (t, u, name, worst)
+            assert len(pre_pos) == L
+            slot_pos[u] = post["pos"].astype(np.int64)
+        if diverged:
+            print("trajectories parted at a near-tie at step", t)
+            return
