@@ -149,6 +149,21 @@ def test_workspace_sizes():
     assert B.dc_workspace_bytes(_dims(head_dim=96), 100, 0, 0) == 0
 
 
+@pytest.mark.parametrize("kv_heads,dtype", [(1, "bf16"), (2, "bf16"), (8, "bf16"), (64, "bf16"),
+                                            (127, "bf16"), (128, "bf16"), (2, "f32")])
+def test_workspace_never_shrinks_as_the_length_grows(kv_heads, dtype):
+    """A workspace sized for max_len serves every shorter cache.  Few bf16 units
+    cut their rows into chunks that grow with the length, so the number of
+    chunks alone is not monotone in the length; the bound must be."""
+    d = _dims(batch=1, n_layers=1, n_q_heads=4 * kv_heads, n_kv_heads=kv_heads, capacity=40960,
+              dtype=B.DC_BF16 if dtype == "bf16" else B.DC_F32)
+    lengths = sorted(set(list(range(1, 9000, 97)) + [4096, 4097, 4098, 8192, 8193, 16384, 16385,
+                                                      16513, 32768, 32769, 40960]))
+    sizes = [B.dc_workspace_bytes(d, L, 0, 0) for L in lengths]
+    assert all(a <= b for a, b in zip(sizes, sizes[1:])), [
+        (L, a, b) for L, a, b in zip(lengths[1:], sizes, sizes[1:]) if a > b][:3]
+
+
 def _logprob(units=4, length=100, budget=10, tau=1.0, scores=FAKE, kept=FAKE, logz=FAKE,
              logp=FAKE, ws=None, wsb=0):
     return B.lib().dc_subset_log_prob(units, length, budget, tau, scores, kept, logz, logp, ws,
