@@ -649,9 +649,9 @@ def main():
                     help="size of the plain copy kernel run first (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the decode step shards by independent "
-              "(batch, layer, KV head) units with no exchange, and this build runs on a "
-              "single MI355X; run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU (--gpus 1): the decode step shards by independent "
+              "(batch, layer, KV head) units with no exchange between GPUs, and the "
+              "multi-GPU launcher is not implemented.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
