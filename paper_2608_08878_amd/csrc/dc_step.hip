@@ -16,7 +16,7 @@
 //           a_ji = p_ji / l_j; with eviction fused, the policy score and the
 //           64-bit ranking key of every row are formed here and the unit is
 //           compacted before the workgroup exits.
-// Caches too long for LDS use the chunked form of the same passes (three
+// Caches too long for LDS use the chunked form of the same passes (two
 // kernels, logits in the workspace).
 #include "dc_select.hpp"
 
@@ -715,17 +715,37 @@ __global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArg
 }
 
 // ---------------------------------------------------------------- chunked path
-// ws_part per (unit, chunk): [G] max, [G] l, [G] u, [G*D] o.
+// ws_part per (unit, chunk): [G] chunk max m_c, [G] l_c, [G] u_c, [G*D] o_c, the
+// sums taken relative to the chunk's own maximum (stepc_d rescales them).
+template <int G>
+__device__ __forceinline__ void chunk_max(const DecodeArgs& a, int u, int D, float (&M)[G]) {
+  const float* parts = a.ws_part + (size_t)u * a.nchunks * (3 * G + G * D);
+#pragma unroll
+  for (int j = 0; j < G; ++j) {
+    float m = parts[j];
+    for (int c = 1; c < a.nchunks; ++c) m = fmaxf(m, parts[(size_t)c * (3 * G + G * D) + j]);
+    M[j] = m;
+  }
+}
+
+// Passes A, P and B of one chunk in one workgroup: K streamed once (logits and
+// retired pairs to the workspace), p = exp(s - m_c) against the chunk maximum,
+// then V streamed once.  The chunk's logits come back from the workspace
+// while still in L2 (this workgroup stored them moments before).
 template <int D, int G, bool FEAT>
-__global__ void __launch_bounds__(SNT) stepc_a_kernel(DecodeArgs a) {
+__global__ void __launch_bounds__(SNT) stepc_ab_kernel(DecodeArgs a) {
+  constexpr int LPR = MG<D>::LPR;
+  __shared__ float pbuf[SCHUNK * G];
+  __shared__ float obuf[SNW * G * D];
   __shared__ float stat[SNW * 2 * G + 2 * G];
-  const int c = blockIdx.x, u = a.y0 + blockIdx.y;
+  const int c = blockIdx.x, u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Lu = len_old_of(a, u) + a.append;       // this unit's rows (ragged caches: per unit)
-  const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk);
+  const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk), n = r1 - r0;
   if (c == 0 && a.append) append_rows<D>(a, u);
-  if (r0 >= r1) {
+  float* part = a.ws_part + ((size_t)u * a.nchunks + c) * (3 * G + G * D);
+  if (n <= 0) {
     // a chunk past this unit's rows: neutral partials (max -inf, sums 0, no output)
-    if (threadIdx.x < G) a.ws_part[((size_t)u * a.nchunks + c) * (3 * G + G * D) + threadIdx.x] = NEG_BIG;
+    for (int t = tid; t < 3 * G + G * D; t += SNT) part[t] = t < G ? NEG_BIG : 0.0f;
     return;
   }
   const bool retire = FEAT && a.retire;
@@ -739,42 +759,7 @@ __global__ void __launch_bounds__(SNT) stepc_a_kernel(DecodeArgs a) {
                             FEAT ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr, 0, qa, retire, rs,
                             mrun, zr, nr);
   float M[G];
-  block_max<G>(mrun, stat, M);
-  if (threadIdx.x < G) {
-    float* part = a.ws_part + ((size_t)u * a.nchunks + c) * (3 * G + G * D);
-#pragma unroll
-    for (int j = 0; j < G; ++j)
-      if (j == (int)threadIdx.x) part[j] = M[j];
-  }
-}
-
-template <int G>
-__device__ __forceinline__ void chunk_max(const DecodeArgs& a, int u, int D, float (&M)[G]) {
-  const float* parts = a.ws_part + (size_t)u * a.nchunks * (3 * G + G * D);
-#pragma unroll
-  for (int j = 0; j < G; ++j) {
-    float m = parts[j];
-    for (int c = 1; c < a.nchunks; ++c) m = fmaxf(m, parts[(size_t)c * (3 * G + G * D) + j]);
-    M[j] = m;
-  }
-}
-
-template <int D, int G>
-__global__ void __launch_bounds__(SNT) stepc_b_kernel(DecodeArgs a) {
-  constexpr int LPR = MG<D>::LPR;
-  __shared__ float pbuf[SCHUNK * G];
-  __shared__ float obuf[SNW * G * D];
-  __shared__ float stat[SNW * 2 * G + 2 * G];
-  const int c = blockIdx.x, u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int Lu = len_old_of(a, u) + a.append;
-  const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk), n = r1 - r0;
-  if (n <= 0) {
-    float* part = a.ws_part + ((size_t)u * a.nchunks + c) * (3 * G + G * D);
-    for (int t = tid; t < 2 * G + G * D; t += SNT) part[G + t] = 0.0f;
-    return;
-  }
-  float M[G];
-  chunk_max<G>(a, u, D, M);
+  block_max<G>(mrun, stat, M);    // (its barriers also order the logit stores before the reads)
   const float* src = a.ws_s + ((size_t)u * a.lmax + r0) * G;
   for (int t = tid; t < n * G; t += SNT) pbuf[t] = src[t];
   __syncthreads();
@@ -791,7 +776,6 @@ __global__ void __launch_bounds__(SNT) stepc_b_kernel(DecodeArgs a) {
       for (int x = 0; x < 8; ++x) obuf[(wave * G + j) * D + lane * 8 + x] = o[j][x];
   }
   __syncthreads();
-  float* part = a.ws_part + ((size_t)u * a.nchunks + c) * (3 * G + G * D);
   for (int t = tid; t < G * D; t += SNT) {
     float acc = 0.0f;
     for (int w = 0; w < SNW; ++w) acc = acc + obuf[w * G * D + t];
@@ -801,6 +785,7 @@ __global__ void __launch_bounds__(SNT) stepc_b_kernel(DecodeArgs a) {
 #pragma unroll
     for (int j = 0; j < G; ++j)
       if (j == tid) {
+        part[j] = M[j];
         part[G + j] = ls[j];
         part[2 * G + j] = us[j];
       }
@@ -817,12 +802,17 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
   const float* parts = a.ws_part + (size_t)u * a.nchunks * PART;
   float M[G], ls[G], us[G], invl[G], H[G];
   chunk_max<G>(a, u, D, M);
+  // chunk c's sums move to the common maximum M: with f = e^(m_c - M),
+  // l += f l_c, u += f (u_c + (m_c - M) l_c), o += f o_c (a neutral chunk: f = 0)
 #pragma unroll
   for (int j = 0; j < G; ++j) {
     float l = 0.0f, uu = 0.0f;
     for (int cc = 0; cc < a.nchunks; ++cc) {
-      l = l + parts[(size_t)cc * PART + G + j];
-      uu = uu + parts[(size_t)cc * PART + 2 * G + j];
+      const float* pc = parts + (size_t)cc * PART;
+      const float dm = pc[j] - M[j];
+      const float f = __builtin_amdgcn_exp2f(dm * LOG2E);
+      l = l + f * pc[G + j];
+      uu = uu + f * (pc[2 * G + j] + dm * pc[G + j]);
     }
     ls[j] = l;
     us[j] = uu;
@@ -850,9 +840,15 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
   }
   if (c != 0) return;
   for (int t = tid; t < G * D; t += SNT) {
-    float acc = 0.0f;
-    for (int cc = 0; cc < a.nchunks; ++cc) acc = acc + parts[(size_t)cc * PART + 3 * G + t];
     const int j = t / D;
+    float mj = M[0];
+#pragma unroll
+    for (int jj = 1; jj < G; ++jj) mj = (jj == j) ? M[jj] : mj;
+    float acc = 0.0f;
+    for (int cc = 0; cc < a.nchunks; ++cc) {
+      const float* pc = parts + (size_t)cc * PART;
+      acc = acc + __builtin_amdgcn_exp2f((pc[j] - mj) * LOG2E) * pc[3 * G + t];
+    }
     float il = invl[0];
 #pragma unroll
     for (int jj = 1; jj < G; ++jj) il = (jj == j) ? invl[jj] : il;
@@ -933,13 +929,8 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
     for_grid_y(a.units, [&](int y0, int ny) {
       DecodeArgs b = a;
       b.y0 = y0;
-      if (feat) hipLaunchKernelGGL((stepc_a_kernel<D, G, true>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
-      else hipLaunchKernelGGL((stepc_a_kernel<D, G, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
-    });
-    for_grid_y(a.units, [&](int y0, int ny) {
-      DecodeArgs b = a;
-      b.y0 = y0;
-      hipLaunchKernelGGL((stepc_b_kernel<D, G>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      if (feat) hipLaunchKernelGGL((stepc_ab_kernel<D, G, true>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      else hipLaunchKernelGGL((stepc_ab_kernel<D, G, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
     });
     for_grid_y(a.units, [&](int y0, int ny) {
       DecodeArgs b = a;
