@@ -696,3 +696,45 @@ def test_decode_from_an_empty_cache(dtype, head_dim, mode):
         if diverged:
             print("trajectories parted at a near-tie at step", t)
             return
+
+
+@pytest.mark.parametrize("n_q,n_kv,d", [(2, 2, 128), (4, 2, 128), (8, 2, 128), (16, 2, 128),
+                                        (2, 2, 64), (8, 2, 64), (16, 2, 64)])
+def test_chunked_step_across_head_groups_and_dims(n_q, n_kv, d):
+    """The chunked decode on two units of 5001 rows (ten chunks, the last one
+    ragged; each chunk's K and V passes in one workgroup, the chunks combined at
+    their common maximum) at G = 1, 2, 4, 8 and head_dim 64 and 128, with an
+    entropy window of 2 so that the third step retires; then a compression
+    step through the stand-alone selection, all against the oracle."""
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=n_kv, n_q_heads=n_q, head_dim=d, n0=5000, budget=1200,
+                               steps=3, ent_window=2)
+    U = wl.units
+    buf = _buffers(wl)
+    buf.reserve_workspace(wl.capacity)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(wl.n0, 0)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    sts = [H.oracle_student(wl, u) for u in range(U)]
+    q, kn, vn = _step_tensors(wl)
+    print(f"chunked G={wl.group} d={d}", flush=True)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        out = buf.decode_step(q, kn, vn)
+        torch.cuda.synchronize()
+        outn = H.to_np(out)
+        for u in range(U):
+            att = ounit.decode_step(sts[u], *H.step_inputs_np(wl, t, u))
+            _check_decode(wl, outn[u], H.download_unit(buf, u), sts[u], att, (t, u))
+    L = buf.kv.len
+    assert L == 5003
+    pre = [H.download_unit(buf, u) for u in range(U)]
+    scores = torch.empty((U, L), dtype=torch.float32, device="cuda")
+    kept = torch.empty((U, wl.budget), dtype=torch.int32, device="cuda")
+    buf.score_evict(pol, wl.budget, scores, kept)
+    torch.cuda.synchronize()
+    sc, kp = H.to_np(scores), H.to_np(kept)
+    for u in range(U):
+        s_or = ounit.scores(sts[u], pnp, wl.hidden)
+        _check_evict(wl, wl.budget, pre[u], sc[u], kp[u], H.download_unit(buf, u), s_or, ("c", u))
