@@ -68,6 +68,7 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = unit_rows(a, u);
+  if (!a.scores_out && unit_budget(a, u) >= L) return;   // a unit that keeps every row reads no key
   for (int base = blockIdx.x * 256; base < L; base += gridDim.x * 256) {
     const int r = base + threadIdx.x;
     float x[1][4];
@@ -89,6 +90,7 @@ __global__ void __launch_bounds__(256) score_ext_kernel(EvictArgs a, uint64_t* k
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = unit_rows(a, u);
+  if (!a.scores_out && unit_budget(a, u) >= L) return;   // a unit that keeps every row reads no key
   for (int base = blockIdx.x * 256; base < L; base += gridDim.x * 256) {
     const int r = base + threadIdx.x;
     if (r < L) {

@@ -105,6 +105,8 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
   constexpr int NS = HP / 4;     // MFMA k-steps (4 units each)
   constexpr int NC = HP / 16;    // 16-column blocks of layer 2
   extern __shared__ float sm[];
+  // a unit that keeps every row reads no key (the whole workgroup leaves)
+  if (!a.scores_out && unit_budget(a, a.y0 + blockIdx.y) >= unit_rows(a, a.y0 + blockIdx.y)) return;
   stage<HP>(a, sm);
   __syncthreads();
   const int u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
