@@ -134,3 +134,49 @@ def test_two_layer_policy_on_ragged_caches():
 
 def test_two_layer_policy_sampled_on_ragged_caches():
     assert _ragged_run([120, 700, 90], steps=3, gumbel=77, tau=0.7, hidden=(64, 64)) >= 1
+
+
+@pytest.mark.parametrize("hidden", [None, (64, 64)])
+def test_units_that_keep_every_row_are_not_scored_without_scores_out(hidden):
+    """Without scores_out, a unit whose budget covers its rows is not scored (its
+    selection reads no key).  Two buffers run the same ragged steps, one asking
+    for scores and one not: every state buffer, length and slot map must agree
+    bit for bit, while the covering units keep every row in place."""
+    budgets = [5000, 300, 5000, 120]                    # units 0 and 2 keep their full cache
+    kw = {"hidden": tuple(hidden)} if hidden else {}
+    wl = W.WORKLOADS[2].scaled(n_kv_heads=len(budgets), n_q_heads=4 * len(budgets), n0=700,
+                               budget=max(budgets), steps=4, **kw)
+    U = wl.units
+    bufs = []
+    for _ in range(2):
+        b = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                          wl.capacity, wl.dtype, wl.ent_window, 0.0, True, ragged=True)
+        b.reserve_workspace(wl.capacity)
+        sg.init_cache(wl, b.k, b.v, U, b.cap)
+        b.feat_init(wl.n0, 0)
+        bufs.append(b)
+    _, pol = _policy(wl)
+    bud = torch.tensor(budgets, dtype=torch.int32, device="cuda")
+    q, kn, vn = _step_tensors(wl)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        kept = []
+        for i, b in enumerate(bufs):
+            b.decode_step(q, kn, vn)
+            Lb = b.kv.len
+            k = torch.full((U, min(max(budgets), Lb)), -7, dtype=torch.int32, device="cuda")
+            sc = torch.empty((U, Lb), dtype=torch.float32, device="cuda") if i == 0 else None
+            b.score_evict_units(pol, bud, max(budgets), None, sc, k, None)
+            kept.append(k)
+        torch.cuda.synchronize()
+        assert np.array_equal(H.to_np(kept[0]), H.to_np(kept[1])), t
+        lens = [H.to_np(b.unit_len).astype(int) for b in bufs]
+        assert np.array_equal(lens[0], lens[1]), t
+        for u in range(U):
+            a, c = _download(bufs[0], u, lens[0][u]), _download(bufs[1], u, lens[1][u])
+            for name in a:
+                assert np.array_equal(a[name], c[name]), (t, u, name)
+            if budgets[u] >= wl.n0 + t + 1:              # covering: its rows before the selection
+                assert np.array_equal(a["pos"], np.arange(wl.n0 + t + 1)), (t, u)
+                assert np.array_equal(H.to_np(kept[1][u])[:lens[0][u]], np.arange(lens[0][u]))
