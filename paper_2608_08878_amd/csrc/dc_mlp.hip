@@ -184,10 +184,8 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
       }
       const float rs = 1.0f / __builtin_sqrtf(sum4rows(s2) / fh1 + LN_EPS);
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const int k = 4 * s + kg;
+      for (int s = 0; s < NS; ++s)
         h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + 4 * s], p1[O_B1 + 2 * HP + 4 * s]);
-      }
     }
 #pragma unroll
     for (int s = 0; s < NS; ++s) h[s] = (4 * s + kg) < h1 ? fmaxf(h[s], 0.0f) : 0.0f;
