@@ -15,6 +15,8 @@ Every value is computed in binary64 from the exact stored input values
   (Sec. 3.1.1, with sigma_i left out) and the windowed entropy H_i.
 * ``policy``     – the scoring MLP s_i = f_phi(x_i) (Sec. 3.1.2, App. D).
 * ``select``     – deterministic argtop_B (Sec. 3.3, Algorithm 1).
+* ``compact``    – storage order of the pruned cache (hole filling; the
+  paper fixes none).
 * ``kl``         – the per-step reward R_t = -KL(P_t || P^_t) (Sec. 3.1.4).
 * ``sampling``   – training-mode selection: Gumbel-perturbed top-B, the exact
   log-partition log Z(s, B, tau) and log pi(a | s) (Sec. 3.1.2, App. C).

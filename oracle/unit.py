@@ -9,7 +9,8 @@ the cache; the policy scores every cached token; the top-B tokens are kept and
 the pruned cache serves the *next* step.  Sec. 3.1.3 adds the teacher cache
 (never pruned, same appends) whose distribution defines the reward.
 
-``StudentState`` holds, per cached row (in ascending position order): key and
+``StudentState`` holds, per cached row (in slot order: ascending position until
+the first eviction, then the hole-filling order of ``compact``): key and
 value rows, absolute position p, alpha, the windowed-entropy history, and —
 for the add/retire cross-check — running N/Z sums plus the per-step records
 (q, m, l, H, largest position present) of the last w steps.
@@ -26,7 +27,7 @@ from dataclasses import dataclass, field
 
 import numpy as np
 
-from . import attention, features, policy, select
+from . import attention, compact, features, policy, select
 
 
 @dataclass
@@ -147,14 +148,15 @@ def scores(st: StudentState, params, hidden, n_in: int = 4, layer_norm: bool = F
 
 
 def evict(st: StudentState, scores_, budget: int) -> np.ndarray:
-    """Keep the top-``budget`` rows under ``scores_``; returns the kept row indices
-    (ascending, i.e. the pruned cache keeps position order)."""
-    kept = select.top_budget(scores_, st.pos, budget)
-    st.K, st.V, st.pos = st.K[kept], st.V[kept], st.pos[kept]
-    st.alpha, st.N, st.Z = st.alpha[kept], st.N[kept], st.Z[kept]
-    st.sigma = st.sigma[kept]
-    st.hist.keep_rows(kept)
-    return kept
+    """Keep the top-``budget`` rows under ``scores_`` and store them in the
+    hole-filling order of ``compact.hole_fill``; returns that slot map (old slot
+    of every new slot)."""
+    slot_map = compact.hole_fill(select.top_budget(scores_, st.pos, budget), st.L)
+    st.K, st.V, st.pos = st.K[slot_map], st.V[slot_map], st.pos[slot_map]
+    st.alpha, st.N, st.Z = st.alpha[slot_map], st.N[slot_map], st.Z[slot_map]
+    st.sigma = st.sigma[slot_map]
+    st.hist.keep_rows(slot_map)
+    return slot_map
 
 
 def score_evict(st: StudentState, params, hidden, budget: int):

@@ -10,6 +10,7 @@ import numpy as np
 import torch
 
 from oracle import attention as oatt
+from oracle import compact as ocomp
 from oracle import select as osel
 from oracle import unit as ounit
 from synth import philox as px
@@ -83,12 +84,16 @@ def upload_unit(buf, u: int, st: ounit.StudentState) -> None:
     buf.num[u, :L] = torch.from_numpy(N).to(buf.k.device)
     buf.den[u, :L] = torch.from_numpy(Z).to(buf.k.device)
     buf.vnorm[u, :L] = torch.from_numpy(np.sqrt((st.V ** 2).sum(1)).astype(np.float32)).to(buf.k.device)
-    if buf.window > 0:
+    if buf.window > 0 and st.records:
+        # the ring slots of the last w steps (slots of older steps are never read)
+        ring = np.zeros(tuple(buf.qring.shape[1:]), np.float32)
+        stat = np.zeros(tuple(buf.qstat.shape[1:]), np.float32)
         for step, rec in st.records.items():
             slot = step % buf.window
-            buf.qring[u, slot] = torch.from_numpy(rec.q.astype(np.float32)).to(td).to(buf.k.device)
-            stat = np.stack([rec.m, 1.0 / rec.l, rec.H], axis=1).astype(np.float32)
-            buf.qstat[u, slot] = torch.from_numpy(stat).to(buf.k.device)
+            ring[slot] = rec.q
+            stat[slot] = np.stack([rec.m, 1.0 / rec.l, rec.H], axis=1)
+        buf.qring[u] = torch.from_numpy(ring).to(td).to(buf.k.device)
+        buf.qstat[u] = torch.from_numpy(stat).to(buf.k.device)
 
 
 def set_host_fields(buf, st: ounit.StudentState) -> None:
@@ -141,15 +146,14 @@ def selection_check(scores_oracle, pos, kept_pos_gpu, budget):
     return bool(not np.any(mism & ~amb)), int(amb.sum()), int((mism & amb).sum())
 
 
-def hole_fill_layout(old_pos, kept_mask, budget):
-    """Expected post-eviction slot contents (old slot per new slot) for the
-    documented compaction: kept rows below `budget` stay, holes below `budget`
-    take the kept rows from slots >= budget in ascending order."""
-    L = len(old_pos)
-    holes = [i for i in range(budget) if not kept_mask[i]]
-    movers = [i for i in range(budget, L) if kept_mask[i]]
-    assert len(holes) == len(movers)
-    layout = list(range(budget))
-    for h, m in zip(holes, movers):
-        layout[h] = m
-    return np.array(layout)
+def oracle_slot_map(scores_gpu, pos, budget):
+    """The oracle's selection applied to the GPU's own float32 scores, stored in
+    the oracle's compaction order: the slot map that kept_out must equal."""
+    kept = osel.top_budget(np.asarray(scores_gpu, np.float64), pos, budget)
+    return ocomp.hole_fill(kept, len(pos))
+
+
+def slot_map_of(kept_rows, n_rows):
+    """The oracle's compaction order for a kept set decided elsewhere (sampled
+    selection, whose kept set is checked on its own)."""
+    return ocomp.hole_fill(kept_rows, n_rows)

@@ -124,11 +124,12 @@ def test_extended_policy_steps(n_in, hidden, ln):
             post = H.download_unit(buf, u)
             ok, amb, flips = H.selection_check(s_or, sts[u].pos, post["pos"], wl.budget)
             assert ok, (t, u, amb, flips)
-            kept_rows = ounit.evict(sts[u], s_or, wl.budget)
-            # the kept rows carry their sigma (compare by position)
+            slot_map = ounit.evict(sts[u], s_or, wl.budget)
+            # the kept rows carry their sigma, in the oracle's slot order
             if flips == 0:
-                order = np.argsort(post["pos"])
-                sig_post = H.to_np(buf.sigma[u, :buf.kv.len])[order]
+                assert np.array_equal(H.to_np(kept)[u], slot_map), (t, u)
+                assert np.array_equal(post["pos"], sts[u].pos), (t, u)
+                sig_post = H.to_np(buf.sigma[u, :buf.kv.len])
                 ok, worst = H.vec_ok(sig_post, sts[u].sigma)
                 assert ok, (t, u, "sigma", worst)
 

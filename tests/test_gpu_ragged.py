@@ -68,20 +68,22 @@ def _ragged_run(budgets, steps, n0=700, gumbel=None, tau=1.0, hidden=None):
         for u in range(U):
             att = ounit.decode_step(sts[u], *H.step_inputs_np(wl, t, u))
             assert lens[u] == sts[u].L, (t, u, lens[u], sts[u].L)
-            order = np.argsort(pre[u]["pos"])            # device slots -> oracle (position) order
-            _check_decode(wl, outn[u], {k: v[order] for k, v in pre[u].items()}, sts[u], att, (t, u))
+            # until a near-tie parts them, device and oracle store the rows in the same slots
+            _check_decode(wl, outn[u], pre[u], sts[u], att, (t, u))
             s_or = ounit.scores(sts[u], pnp, wl.hidden)
-            ok, worst = H.vec_ok(sc[u, :lens[u]][order], s_or)
+            ok, worst = H.vec_ok(sc[u, :lens[u]], s_or)
             assert ok, (t, u, worst)
             Bu = budgets[u]
             nk = min(Bu, lens[u])
             assert post_lens[u] == nk, (t, u)
             assert np.all(kp[u, nk:] == -1) and np.all(kp[u, :nk] >= 0), (t, u)
             post = _download(buf, u, nk)
-            # documented compaction for this unit's own budget
-            kmask = np.zeros(lens[u], bool)
-            kmask[kp[u, :nk]] = True
-            layout = H.hole_fill_layout(pre[u]["pos"], kmask, nk)
+            # the oracle's compaction for this unit's own budget (deterministic: its
+            # selection on the GPU's own scores; sampled: the kept set checked below)
+            if gumbel:
+                layout = H.slot_map_of(kp[u, :nk], lens[u])
+            else:
+                layout = H.oracle_slot_map(sc[u, :lens[u]], pre[u]["pos"], nk)
             assert np.array_equal(kp[u, :nk], layout), (t, u)
             for name in ("k", "v", "pos", "alpha", "num", "den", "vnorm"):
                 assert np.array_equal(post[name], pre[u][name][layout]), (t, u, name)

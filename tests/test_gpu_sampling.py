@@ -154,10 +154,8 @@ def _sampled_check(s_or, pos, kept_pos_gpu, budget, tau, seed, unit, draw):
 
 def _check_layout(pre_u, kept_u, post_u, budget):
     L = len(pre_u["pos"])
-    kmask = np.zeros(L, bool)
-    kmask[kept_u] = True
-    assert kmask.sum() == min(budget, L)
-    layout = H.hole_fill_layout(pre_u["pos"], kmask, min(budget, L))
+    assert len(set(kept_u.tolist())) == min(budget, L)
+    layout = H.slot_map_of(kept_u, L)
     assert np.array_equal(kept_u, layout)
     for name in ("k", "v", "pos", "alpha", "num", "den", "vnorm"):
         assert np.array_equal(post_u[name], pre_u[name][layout]), name

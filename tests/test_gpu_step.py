@@ -97,10 +97,7 @@ def test_config1_single_step_matches_oracle():
         ok, worst = H.vec_ok(scores[u], s_or)
         assert ok, (u, "scores", worst)
         # exact: the oracle's selection applied to the GPU's own float32 scores
-        kept_exact = osel.top_budget(scores[u].astype(np.float64), pre[u]["pos"], wl.budget)
-        kmask = np.zeros(wl.n0, bool)
-        kmask[kept_exact] = True
-        layout = H.hole_fill_layout(pre[u]["pos"], kmask, wl.budget)
+        layout = H.oracle_slot_map(scores[u], pre[u]["pos"], wl.budget)
         assert np.array_equal(kept[u], layout)
         for name in ("k", "v", "pos", "alpha", "num", "den", "vnorm"):
             assert np.array_equal(post[u][name], pre[u][name][layout]), name
@@ -131,10 +128,7 @@ def _check_decode(wl, out_u, pre_u, st, att, tag):
 def _check_evict(wl, budget, pre_u, scores_u, kept_u, post_u, s_or, tag):
     ok, worst = H.vec_ok(scores_u, s_or)
     assert ok, (tag, "scores", worst)
-    kept_exact = osel.top_budget(scores_u.astype(np.float64), pre_u["pos"], budget)
-    kmask = np.zeros(len(pre_u["pos"]), bool)
-    kmask[kept_exact] = True
-    layout = H.hole_fill_layout(pre_u["pos"], kmask, min(budget, len(kmask)))
+    layout = H.oracle_slot_map(scores_u, pre_u["pos"], budget)
     assert np.array_equal(kept_u, layout), tag
     for name in ("k", "v", "pos", "alpha", "num", "den", "vnorm"):
         assert np.array_equal(post_u[name], pre_u[name][layout]), (tag, name)
@@ -201,7 +195,7 @@ def test_free_running_trajectory_until_first_near_tie():
         out = buf.decode_step(q, kn, vn)
         torch.cuda.synchronize()
         outn = H.to_np(out)
-        pre = [H.by_position(H.download_unit(buf, u)) for u in range(U)]
+        pre = [H.download_unit(buf, u) for u in range(U)]      # same slot order as the oracle
         buf.score_evict(pol, wl.budget)
         torch.cuda.synchronize()
         diverged = False
@@ -324,10 +318,7 @@ def test_adversarial_selection(case):
     sc, kp = H.to_np(scores), H.to_np(kept)
     for u in range(U):
         post = H.download_unit(buf, u)
-        kept_exact = osel.top_budget(sc[u].astype(np.float64), pre[u]["pos"], budget)
-        kmask = np.zeros(L, bool)
-        kmask[kept_exact] = True
-        layout = H.hole_fill_layout(pre[u]["pos"], kmask, min(budget, L))
+        layout = H.oracle_slot_map(sc[u], pre[u]["pos"], budget)
         assert np.array_equal(kp[u], layout), case
         for name in ("k", "v", "pos", "alpha", "num", "den", "vnorm"):
             assert np.array_equal(post[name], pre[u][name][layout]), (case, name)
@@ -559,6 +550,8 @@ def test_dynamic_budget_trajectory():
             assert ok, (t, u, amb, flips)
             ounit.evict(sts[u], s_or, budget)
             assert buf.kv.len == sts[u].L
+            if flips == 0:      # both trajectories store the kept rows in the same slots
+                assert np.array_equal(post["pos"], sts[u].pos), (t, u)
             diverged |= flips > 0
         if diverged:
             print("trajectories parted at a near-tie at step", t)
@@ -604,21 +597,16 @@ def test_fused_step_across_head_groups_and_dims(n_q, n_kv, d):
             assert ok, (t, u, amb, flips)
             amb_total += amb
             pre_pos = sts[u].pos.copy()
-            Z, N = sts[u].hist.sums()
-            pre = {"alpha": sts[u].alpha.copy(), "den": Z, "num": N}
-            ounit.evict(sts[u], s_or, wl.budget)
+            # exact: the oracle's selection and compaction on the GPU's own scores
+            assert np.array_equal(kp[u], H.oracle_slot_map(sc[u], pre_pos, wl.budget)), (t, u)
+            slot_map = ounit.evict(sts[u], s_or, wl.budget)
             if flips == 0:
-                # the kept rows carry the oracle's post-step features
-                assert np.array_equal(np.sort(post["pos"]), sts[u].pos), (t, u)
-                src = np.searchsorted(pre_pos, post["pos"])
-                for name in ("alpha", "den", "num"):
-                    ok, worst = H.vec_ok(post[name], pre[name][src])
+                # the oracle's own step: same slot map, rows carrying its post-step features
+                assert np.array_equal(kp[u], slot_map) and np.array_equal(post["pos"], sts[u].pos)
+                Z, N = sts[u].hist.sums()
+                for name, ref in (("alpha", sts[u].alpha), ("den", Z), ("num", N)):
+                    ok, worst = H.vec_ok(post[name], ref)
                     assert ok, (t, u, name, worst)
-            # the slot map is the documented hole-filling compaction of the kept set
-            nk = min(wl.budget, len(pre_pos))
-            kmask = np.zeros(len(pre_pos), bool)
-            kmask[kp[u, :nk]] = True
-            assert np.array_equal(kp[u, :nk], H.hole_fill_layout(pre_pos, kmask, nk)), (t, u)
     print("ambiguous selections excluded:", amb_total)
 
 
@@ -668,13 +656,15 @@ def test_decode_from_an_empty_cache(dtype, head_dim, mode):
                 assert np.allclose(att.o, st.V[0][None, :].repeat(wl.group, 0))   # one row: its value
             s_or = ounit.scores(st, pnp, wl.hidden)
             dev_pos = np.append(slot_pos[u], t)                 # the appended row takes the last slot
+            assert np.array_equal(dev_pos, st.pos), (t, u)       # same compaction order so far
             o_dev, o_or = np.argsort(dev_pos), np.argsort(st.pos)
             assert np.array_equal(dev_pos[o_dev], st.pos[o_or]), (t, u)
             ok, worst = H.vec_ok(sc[u][o_dev], s_or[o_or])
             assert ok, (t, u, "scores", worst)
-            assert np.array_equal(np.sort(dev_pos[kp[u]]), np.sort(
-                H.download_unit(buf, u)["pos"])), (t, u, "kept_out names the kept rows")
             post = H.download_unit(buf, u)
+            # exact: the oracle's selection and compaction applied to the device's scores
+            assert np.array_equal(kp[u], H.oracle_slot_map(sc[u], dev_pos, budget)), (t, u)
+            assert np.array_equal(post["pos"], dev_pos[kp[u]]), (t, u)
             ok, amb, flips = H.selection_check(s_or, st.pos, post["pos"], budget)
             assert ok, (t, u, amb, flips)
             diverged |= flips > 0

@@ -328,7 +328,7 @@ def test_eviction_carries_rows_and_state():
     before = (st.K.copy(), st.V.copy(), st.pos.copy(), st.alpha.copy(), st.hist.z.copy())
     s = r.normal(size=st.L)
     kept = unit.evict(st, s, 20)
-    assert st.L == 20 and np.all(np.diff(st.pos) > 0)
+    assert st.L == 20 and len(set(st.pos.tolist())) == 20
     for arr, old in zip((st.K, st.V, st.pos, st.alpha, st.hist.z), before):
         assert np.array_equal(arr, old[kept])
 
