@@ -57,7 +57,8 @@ typedef enum {
   DC_ERR_BUDGET = 5,       /* budget < 1 */
   DC_ERR_WORKSPACE = 6,    /* workspace missing or smaller than dc_workspace_bytes */
   DC_ERR_HIP = 7,          /* a HIP launch failed */
-  DC_ERR_VALUE = 8         /* a scalar argument out of range (temperature not finite and > 0) */
+  DC_ERR_VALUE = 8,        /* a scalar argument out of range (temperature not finite and > 0) */
+  DC_ERR_SCRATCH = 9       /* larger than the fixed scratch of an allocation-free entry point */
 } dc_status;
 
 typedef enum { DC_F32 = 0, DC_BF16 = 1 } dc_dtype;
@@ -352,6 +353,26 @@ size_t dc_global_alpha_workspace_bytes(const dc_dims *dims, int32_t positions);
 dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void *h_full,
                        const void *h_comp, const void *w_lm, float *kl_out, void *ws,
                        size_t ws_bytes, void *hip_stream);
+
+/* Largest rows * (vocab / 64) of one dc_kl_reward_static call. */
+#define DC_KL_STATIC_MAX_PAIRS 524288
+
+/* dc_kl_reward without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, serving loops and harnesses that
+ * forbid allocation).  Same arguments, kernels and result bits as
+ * dc_kl_reward; the per-(row, 64-column tile) statistics go to a scratch array
+ * of 16 * DC_KL_STATIC_MAX_PAIRS bytes (8 MiB) that the library holds on each
+ * device it runs on until the process ends (e.g. 1024 rows of a
+ * 32768-entry vocabulary).  The call allocates nothing.  Calls that overlap on
+ * one device share that array and race: order them on one stream.  Every
+ * entry a call reads is written earlier in the same call, so nothing left by
+ * an earlier call is used.
+ * Errors: those of dc_kl_reward except DC_ERR_WORKSPACE; DC_ERR_SCRATCH when
+ * rows * (vocab / 64) > DC_KL_STATIC_MAX_PAIRS (checked before any device
+ * work); DC_ERR_HIP when the scratch address cannot be obtained. */
+dc_status dc_kl_reward_static(int32_t rows, int32_t hidden, int32_t vocab, const void *h_full,
+                              const void *h_comp, const void *w_lm, float *kl_out,
+                              void *hip_stream);
 
 /* Dynamic budget (App. D, experimental protocol): the budget of a decode step
  * scales with the sequence, B_t = max(floor(ratio * seq_len), b_min).  The

@@ -13,7 +13,7 @@ MAX_WINDOW = 64
 DC_F32, DC_BF16 = 0, 1
 STATUS = {0: "DC_OK", 1: "DC_ERR_NULL", 2: "DC_ERR_SHAPE", 3: "DC_ERR_UNSUPPORTED",
           4: "DC_ERR_CAPACITY", 5: "DC_ERR_BUDGET", 6: "DC_ERR_WORKSPACE", 7: "DC_ERR_HIP",
-          8: "DC_ERR_VALUE"}
+          8: "DC_ERR_VALUE", 9: "DC_ERR_SCRATCH"}
 
 
 class dc_dims(ctypes.Structure):
@@ -58,11 +58,13 @@ class dc_reinforce_cfg(ctypes.Structure):
 
 
 KL_MAX_ROWS = 16384
+KL_STATIC_MAX_PAIRS = 524288     # rows * (vocab / 64) of one dc_kl_reward_static call
 
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
            "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_score_evict_units",
            "dc_subset_log_prob",
-           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_reinforce_terms",
+           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_kl_reward_static",
+           "dc_reinforce_terms",
            "dc_dynamic_budget", "dc_global_alpha", "dc_global_alpha_workspace_bytes",
            "dc_status_str")
 
@@ -113,6 +115,8 @@ def lib() -> ctypes.CDLL:
         L.dc_subset_log_prob_workspace_bytes.restype = sz
         L.dc_kl_reward.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
         L.dc_kl_reward.restype = ctypes.c_int
+        L.dc_kl_reward_static.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp]
+        L.dc_kl_reward_static.restype = ctypes.c_int
         L.dc_reinforce_terms.argtypes = [i32, i32, ctypes.POINTER(dc_reinforce_cfg), vp, vp, vp,
                                          vp, vp, vp, vp, vp, vp]
         L.dc_reinforce_terms.restype = ctypes.c_int
@@ -198,6 +202,12 @@ def dc_kl_reward(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_ou
                  ws_bytes: int = 0, stream=None) -> None:
     _check(lib().dc_kl_reward(rows, hidden, vocab, _ptr(h_full), _ptr(h_comp), _ptr(w_lm),
                               _ptr(kl_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_kl_reward_static(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_out,
+                        stream=None) -> None:
+    _check(lib().dc_kl_reward_static(rows, hidden, vocab, _ptr(h_full), _ptr(h_comp),
+                                     _ptr(w_lm), _ptr(kl_out), stream))
 
 
 def dc_sample_evict(dims, kv, feat, policy, budget: int, gumbel, scores_out=None, kept_out=None,

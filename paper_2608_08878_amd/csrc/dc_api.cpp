@@ -109,6 +109,7 @@ const char* dc_status_str(dc_status s) {
     case DC_ERR_WORKSPACE: return "DC_ERR_WORKSPACE: workspace missing or too small";
     case DC_ERR_HIP: return "DC_ERR_HIP: a HIP launch failed";
     case DC_ERR_VALUE: return "DC_ERR_VALUE: scalar argument out of range";
+    case DC_ERR_SCRATCH: return "DC_ERR_SCRATCH: larger than the fixed scratch of the allocation-free entry point";
   }
   return "unknown dc_status";
 }
@@ -406,6 +407,31 @@ dc_status prep_logz(int32_t units, int32_t L, int32_t B, float tau, const float*
   return DC_OK;
 }
 
+dc_status kl_check(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
+                   const void* h_comp, const void* w_lm, const float* kl_out) {
+  if (!h_full || !h_comp || !w_lm || !kl_out) return DC_ERR_NULL;
+  if (rows < 1 || hidden < 1 || vocab < 1) return DC_ERR_SHAPE;
+  if (rows > DC_KL_MAX_ROWS || hidden % 128 || vocab % dc::kl_tile_cols()) return DC_ERR_UNSUPPORTED;
+  return DC_OK;
+}
+
+// part: rows * (vocab / 64) * 4 floats of per-(row, tile) statistics.
+dc_status kl_launch(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
+                    const void* h_comp, const void* w_lm, float* kl_out, float* part,
+                    void* hip_stream) {
+  dc::KLArgs a;
+  a.h_full = h_full;
+  a.h_comp = h_comp;
+  a.w = w_lm;
+  a.out = kl_out;
+  a.part = part;
+  a.rows = rows;
+  a.hidden = hidden;
+  a.vocab = vocab;
+  a.ntiles = vocab / dc::kl_tile_cols();
+  return dc::launch_kl(a, hip_stream) == 0 ? DC_OK : DC_ERR_HIP;
+}
+
 }  // namespace
 
 extern "C" {
@@ -655,23 +681,22 @@ dc_status dc_global_alpha(const dc_dims* dims, const dc_kv* kv, dc_feat* feat, v
 dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
                        const void* h_comp, const void* w_lm, float* kl_out, void* ws,
                        size_t ws_bytes, void* hip_stream) {
-  if (!h_full || !h_comp || !w_lm || !kl_out) return DC_ERR_NULL;
-  if (rows < 1 || hidden < 1 || vocab < 1) return DC_ERR_SHAPE;
-  if (rows > DC_KL_MAX_ROWS || hidden % 128 || vocab % dc::kl_tile_cols()) return DC_ERR_UNSUPPORTED;
-  const size_t need = kl_bytes(rows, vocab);
-  if (!ws || ws_bytes < need) return DC_ERR_WORKSPACE;
-  dc::KLArgs a;
-  a.h_full = h_full;
-  a.h_comp = h_comp;
-  a.w = w_lm;
-  a.out = kl_out;
-  a.part = (float*)ws;
-  a.rows = rows;
-  a.hidden = hidden;
-  a.vocab = vocab;
-  a.ntiles = vocab / dc::kl_tile_cols();
-  if (dc::launch_kl(a, hip_stream) != 0) return DC_ERR_HIP;
-  return DC_OK;
+  const dc_status st = kl_check(rows, hidden, vocab, h_full, h_comp, w_lm, kl_out);
+  if (st != DC_OK) return st;
+  if (!ws || ws_bytes < kl_bytes(rows, vocab)) return DC_ERR_WORKSPACE;
+  return kl_launch(rows, hidden, vocab, h_full, h_comp, w_lm, kl_out, (float*)ws, hip_stream);
+}
+
+dc_status dc_kl_reward_static(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
+                              const void* h_comp, const void* w_lm, float* kl_out,
+                              void* hip_stream) {
+  const dc_status st = kl_check(rows, hidden, vocab, h_full, h_comp, w_lm, kl_out);
+  if (st != DC_OK) return st;
+  if ((size_t)rows * (size_t)(vocab / dc::kl_tile_cols()) > (size_t)DC_KL_STATIC_MAX_PAIRS)
+    return DC_ERR_SCRATCH;
+  float* part = nullptr;
+  if (dc::kl_static_scratch(&part) != 0 || !part) return DC_ERR_HIP;
+  return kl_launch(rows, hidden, vocab, h_full, h_comp, w_lm, kl_out, part, hip_stream);
 }
 
 }  // extern "C"

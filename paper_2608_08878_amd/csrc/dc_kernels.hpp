@@ -164,6 +164,9 @@ int evict_max_len();
 size_t evict_ws_bytes(int units, int L);
 size_t evict_ext_ws_bytes(int units, int L);
 int launch_kl(const KLArgs& a, void* stream);
+// Device address of the allocation-free KL entry point's scratch on the current
+// device (looked up once per device); 0 on success.
+int kl_static_scratch(float** out);
 int launch_global_alpha(const GlobalAlphaArgs& a, void* stream);
 int global_alpha_groups(int per_seq);    // unit groups of one sequence (workspace sizing)
 // bf16 matrix-core step (dc_step.hip); e != nullptr fuses scoring and eviction.

@@ -18,8 +18,11 @@
 // where P_t is P restricted to the tile.  Kernel 2 merges the tiles exactly:
 //     w_t = s_t e^{m_t - M} / S,  mu = sum w_t mu_t,  x_t = mu - mu_t,
 //     KL = log1p( sum_t w_t (g(x_t) + e^{x_t} A_t) ).
+#include <mutex>
+
 #include "dc_device.hpp"
 #include "dc_kernels.hpp"
+#include "distillcache.h"
 
 #pragma clang fp contract(off)
 
@@ -457,6 +460,37 @@ int launch_kl(const KLArgs& a, void* stream) {
   }
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();
+}
+
+}  // namespace dc
+
+// Scratch of dc_kl_reward_static: the per-(row, tile) statistics (4 floats per
+// pair) in a fixed device array instead of a caller workspace.  Each device
+// holds its own copy at its own address.  Host code never passes the array's
+// name to a kernel (on the host it is only a stand-in for the symbol): the
+// device address is looked up once per device with that device current and
+// kept, and the kernels receive it as their `part` argument.
+static __device__ __align__(256) float scratch[(size_t)DC_KL_STATIC_MAX_PAIRS * 4];
+
+namespace {
+constexpr int SCRATCH_MAX_DEVICES = 64;
+std::mutex scratch_mu;
+void* scratch_addr[SCRATCH_MAX_DEVICES] = {};
+}  // namespace
+
+namespace dc {
+
+int kl_static_scratch(float** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= SCRATCH_MAX_DEVICES) return -1;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return -1;
+    scratch_addr[dev] = p;
+  }
+  *out = static_cast<float*>(scratch_addr[dev]);
+  return 0;
 }
 
 }  // namespace dc

@@ -139,6 +139,20 @@ def test_kl_reward_rejects_bad_arguments():
     assert L.dc_kl_reward(8, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == 6
 
 
+def test_kl_reward_static_rejects_bad_arguments_before_any_device_work():
+    L = B.lib()
+    assert L.dc_kl_reward_static(8, 4096, 32768, None, FAKE, FAKE, FAKE, None) == 1
+    assert L.dc_kl_reward_static(8, 4096, 32768, FAKE, FAKE, FAKE, None, None) == 1
+    assert L.dc_kl_reward_static(0, 4096, 32768, FAKE, FAKE, FAKE, FAKE, None) == 2
+    assert L.dc_kl_reward_static(8, 4000, 32768, FAKE, FAKE, FAKE, FAKE, None) == 3
+    assert L.dc_kl_reward_static(B.KL_MAX_ROWS + 1, 4096, 64, FAKE, FAKE, FAKE, FAKE, None) == 3
+    # one pair past the fixed scratch (rows * vocab / 64 > 524288): DC_ERR_SCRATCH
+    assert L.dc_kl_reward_static(1025, 4096, 32768, FAKE, FAKE, FAKE, FAKE, None) == 9
+    assert L.dc_kl_reward_static(1, 128, 64 * (B.KL_STATIC_MAX_PAIRS + 1), FAKE, FAKE, FAKE,
+                                 FAKE, None) == 9
+    assert "scratch" in B.dc_status_str(9)
+
+
 def test_workspace_sizes():
     d = _dims(batch=16, n_layers=32, n_q_heads=32, n_kv_heads=8, capacity=16385)
     assert B.dc_workspace_bytes(d, 0, 0, 0) == 0
