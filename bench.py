@@ -6,9 +6,12 @@ budget 4096 (25 %), per-KV-head top-k.  One *step* is the whole hot path over
 every (batch, layer, KV head) unit: append the new K/V row, GQA decode
 attention, feature accumulation (alpha, windowed entropy, ||v||, position),
 policy-MLP scoring of every cached token, top-4096 keep and in-place
-compaction.  The first (compression) step 16385 -> 4096 runs before the warm-up
-and is reported separately; the timed steps are steady decode steps
-(4097 -> 4096 per unit).
+compaction.  The workload's 128 steps run first, each timed on its own: the
+compression step 16385 -> 4096, steps 1..63 while the entropy window fills,
+steps 64..127 with the window full; their average and the two kinds of steady
+step are reported separately.  The headline value times further steady steps
+(4097 -> 4096 per unit), all with the window full, so each also retires the
+queries of step t - 64.
 
 Prints one JSON line.  Inputs are resident in HBM before timing starts.
 """
@@ -87,36 +90,67 @@ def measured_traffic():
     return int(tb.group(1))
 
 
-def run_oracle_baseline(wl, units, steps, seed_units=0):
-    """Time the CPU oracle on a bounded sample: `units` units, each brought to the
-    steady state (untimed compression step) and then stepped `steps` times."""
-    import numpy as np
+def _oracle_units_worker(task):
+    """Worker process of the CPU baseline: bring each unit to a full entropy
+    window (steps 0..w-1, untimed) and time `steps` further steps of the oracle
+    (append, attention, features, score, top-B, compaction), one BLAS thread."""
+    cid, units, steps = task
+    from threadpoolctl import threadpool_limits
 
-    from oracle import unit as ounit
     from oracle import attention as oatt
+    from oracle import unit as ounit
     from synth import workloads as W
 
+    wl = W.WORKLOADS[cid]
     params = W.policy_params(wl)
     scale = oatt.default_scale(wl.head_dim)
-    total = 0.0
-    for k in range(units):
-        u = (k * 2654435761 + seed_units) % wl.units
-        pos = np.arange(wl.n0)
-        st = ounit.new_student(W.key_rows(wl, u, pos), W.value_rows(wl, u, pos), pos,
-                               G=wl.group, scale=scale, window=wl.ent_window, next_pos=wl.n0)
-        inputs = []
-        for t in range(steps + 1):
-            p = [wl.n0 + t]
-            inputs.append((W.queries(wl, t, u), W.key_rows(wl, u, p)[0], W.value_rows(wl, u, p)[0]))
-        ounit.decode_step(st, *inputs[0])
-        ounit.score_evict(st, params, wl.hidden, wl.budget)
-        t0 = time.perf_counter()
-        for t in range(1, steps + 1):
-            ounit.decode_step(st, *inputs[t])
-            ounit.score_evict(st, params, wl.hidden, wl.budget)
-        total += time.perf_counter() - t0
-    per_unit_step = total / (units * steps)
-    return per_unit_step, total
+    fill = max(wl.ent_window, 1)
+    timed = 0.0
+    with threadpool_limits(1):
+        for u in units:
+            pos = np.arange(wl.n0)
+            st = ounit.new_student(W.key_rows(wl, u, pos), W.value_rows(wl, u, pos), pos,
+                                   G=wl.group, scale=scale, window=wl.ent_window, next_pos=wl.n0)
+            inputs = []
+            for t in range(fill + steps):
+                p = [wl.n0 + t]
+                inputs.append((W.queries(wl, t, u), W.key_rows(wl, u, p)[0],
+                               W.value_rows(wl, u, p)[0]))
+            for t in range(fill):
+                ounit.decode_step(st, *inputs[t])
+                ounit.score_evict(st, params, wl.hidden, wl.budget)
+            t0 = time.perf_counter()
+            for t in range(fill, fill + steps):
+                ounit.decode_step(st, *inputs[t])
+                ounit.score_evict(st, params, wl.hidden, wl.budget)
+            timed += time.perf_counter() - t0
+    return timed, len(units) * steps
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def run_oracle_baseline(wl, n_units, steps, workers):
+    """Time the CPU oracle on a bounded sample of units in `workers` processes
+    (one thread each); returns (unit-steps per second of the whole pool, total
+    timed CPU seconds).  Units are independent, so the pool's rate scales to
+    the workload by its unit count."""
+    import multiprocessing
+
+    units = [(k * 2654435761) % wl.units for k in range(n_units)]
+    chunks = [units[w::workers] for w in range(workers) if units[w::workers]]
+    ctx = multiprocessing.get_context("spawn")      # fresh interpreters, no GPU state
+    with ctx.Pool(len(chunks)) as pool:
+        res = pool.map(_oracle_units_worker, [(wl.cid, c, steps) for c in chunks])
+    wall = max(r[0] for r in res)                   # the pool finishes with its slowest worker
+    return sum(r[1] for r in res) / wall, sum(r[0] for r in res)
 
 
 def _events(n):
@@ -643,8 +677,8 @@ def main():
     ap.add_argument("--train-select", action="store_true",
                     help="workload 5: the student keeps a Gumbel-sampled top-B and computes "
                          "log pi (training mode) instead of the deterministic selection")
-    ap.add_argument("--cpu-units", type=int, default=64)
-    ap.add_argument("--cpu-steps", type=int, default=96)
+    ap.add_argument("--cpu-units", type=int, default=128)
+    ap.add_argument("--cpu-steps", type=int, default=64)
     ap.add_argument("--calib-copy-mib", type=int, default=1024,
                     help="size of the plain copy kernel run first (counter calibration)")
     args = ap.parse_args()
@@ -667,12 +701,22 @@ def main():
     U, G, D, elt = wl.units, wl.group, wl.head_dim, 2 if wl.dtype == "bf16" else 4
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
 
-    # plain copy kernel of known size (HBM counter calibration under rocprofv3 --pmc)
+    # plain copy kernel of known size (HBM counter calibration under rocprofv3 --pmc),
+    # then timed: the measured copy bandwidth (bytes read + written per second)
+    copy_gbps = None
     if args.calib_copy_mib > 0:
         a = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
         b.copy_(a)
         torch.cuda.synchronize()
+        c0, c1 = _events(2)
+        c0.record()
+        for _ in range(5):
+            b.copy_(a)
+        c1.record()
+        torch.cuda.synchronize()
+        copy_gbps = 5 * 2 * a.numel() / (c0.elapsed_time(c1) * 1e-3) / 1e9
+        log(f"device copy: {copy_gbps:.0f} GB/s (read + write)")
         del a, b
 
     if args.config in (1, 4, 5) or args.policy == "paper" or args.hybrid > 0 or args.global_alpha:
@@ -708,7 +752,13 @@ def main():
     params = torch.empty(wl.n_params, dtype=torch.float32, device=dev)
     sg.fill_normal(params, wl, W.S_POLICY, 0, 0.1)
     pol = make_policy(params, wl.hidden)
-    nsteps = 1 + args.warmup + args.steps
+    # The workload's own steps run first (step 0 compresses, steps 1..w-1 fill the
+    # entropy window, from step w on every step also retires step t - w), then
+    # `warmup` untimed and `steps` timed steps: every timed step is a window-full
+    # steady step, whatever --steps and --warmup are.
+    fill = max(wl.ent_window, 1)
+    n_wl = max(wl.steps, fill)
+    nsteps = n_wl + args.warmup + args.steps + 1         # + one untimed step with the slot map
     td = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
     Q = torch.empty((nsteps, U, G, D), dtype=td, device=dev)
     KN = torch.empty((nsteps, U, D), dtype=td, device=dev)
@@ -720,33 +770,47 @@ def main():
     torch.cuda.synchronize()
     log(f"setup {time.time() - t0:.1f}s: {U} units, cache {buf.k.numel() * elt * 2 / 1e9:.1f} GB")
 
-    # step 0: compression n0+1 -> budget (reported separately)
+    # step 0: compression n0+1 -> budget
     _load_compression_kernels(wl, cap, pol, dev)
-    e0, e1 = (torch.cuda.Event(enable_timing=True) for _ in range(2))
+    e0, e1 = _events(2)
     e0.record()
     buf.decode_evict(pol, wl.budget, Q[0], KN[0], VN[0], out)
     e1.record()
     torch.cuda.synchronize()
     first_ms = e0.elapsed_time(e1)
     log(f"step 0 (L={wl.n0 + 1} -> {wl.budget}): {first_ms:.3f} ms")
-
     if not args.no_shrink:
         # after compression only budget + 1 rows per unit are live: move them into
-        # budget-sized buffers (one-time, untimed, like step 0)
+        # budget-sized buffers (one-time, between steps 0 and 1)
         buf.shrink(wl.budget + 1)
         log(f"caches moved to capacity {buf.cap}")
 
-    for t in range(1, 1 + args.warmup):
+    # the rest of the workload's steps, each between its own events
+    ev = [_events(2) for _ in range(n_wl)]
+    for t in range(1, n_wl):
+        ev[t][0].record()
+        buf.decode_evict(pol, wl.budget, Q[t], KN[t], VN[t], out)
+        ev[t][1].record()
+    torch.cuda.synchronize()
+    wl_ms = [first_ms] + [ev[t][0].elapsed_time(ev[t][1]) for t in range(1, n_wl)]
+    pre_ms = float(np.mean(wl_ms[1:fill])) if fill > 1 else float("nan")
+    full_ms = float(np.mean(wl_ms[fill:])) if n_wl > fill else float("nan")
+    wl_avg_ms = float(np.sum(wl_ms[:wl.steps])) / wl.steps
+    log(f"workload steps 1..{fill - 1} (window filling): {pre_ms:.4f} ms/step; steps "
+        f"{fill}..{n_wl - 1} (window full): {full_ms:.4f} ms/step; {wl.steps}-step average "
+        f"incl. step 0: {wl_avg_ms:.4f} ms")
+
+    for t in range(n_wl, n_wl + args.warmup):
         buf.decode_evict(pol, wl.budget, Q[t], KN[t], VN[t], out)
     torch.cuda.synchronize()
+    assert buf.feat.step >= fill, "timed steps must all retire a window step"
 
     L_steady = buf.kv.len + 1
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(args.steps)]
+    ev = [_events(2) for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for i in range(args.steps):
-        t = 1 + args.warmup + i
+        t = n_wl + args.warmup + i
         a, b = ev[i]
         a.record()
         buf.decode_evict(pol, wl.budget, Q[t], KN[t], VN[t], out)
@@ -755,7 +819,8 @@ def main():
     wall = time.perf_counter() - t_start
     step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     ms_per_step = wall * 1e3 / args.steps
-    log(f"steady: {ms_per_step:.3f} ms/step wall; fused step kernel {step_ms:.3f} ms (events)")
+    log(f"steady (window full): {ms_per_step:.3f} ms/step wall; fused step kernel "
+        f"{step_ms:.3f} ms (events)")
 
     # moved rows per steady step (one untimed extra step with the slot map)
     kept = torch.empty((U, wl.budget), dtype=torch.int32, device=dev)
@@ -764,11 +829,11 @@ def main():
     torch.cuda.synchronize()
     moved = int((kept != torch.arange(wl.budget, device=dev, dtype=torch.int32)[None, :]).sum())
 
-    retire = True
-    step_bytes = step_alg_bytes(U, L_steady, G, D, elt, retire, moved)
+    step_bytes = step_alg_bytes(U, L_steady, G, D, elt, True, moved)
     kvb = kv_bytes(U, L_steady, D, elt, moved)
     steps_per_s = 1e3 / ms_per_step
     step_gbps = step_bytes / (step_ms * 1e-3) / 1e9
+    kv_gbps = kvb / (ms_per_step * 1e-3) / 1e9
     result = {
         "metric": METRIC,
         "value": round(steps_per_s, 3),
@@ -786,29 +851,44 @@ def main():
                    "q_heads": wl.n_q_heads, "kv_heads": wl.n_kv_heads, "head_dim": D,
                    "context": wl.n0, "budget": wl.budget, "units": U,
                    "steady_len": L_steady, "steady_capacity": buf.cap,
+                   "timed_steps": f"{n_wl + args.warmup}..{n_wl + args.warmup + args.steps - 1} "
+                                  f"(entropy window full: every step retires step t - {fill})",
                    "policy": "4->%s->1 ReLU MLP" % "->".join(map(str, wl.hidden))},
-        "kv_gbps": round(kvb / (ms_per_step * 1e-3) / 1e9, 1),
-        "kv_frac_of_8TBps": round(kvb / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBPS, 4),
+        "kv_gbps": round(kv_gbps, 1),
+        "kv_frac_of_8TBps": round(kv_gbps / HBM_PEAK_GBPS, 4),
         "kv_bytes_per_step": kvb,
         "moved_rows_per_step": moved,
         "step_kernel_ms": round(step_ms, 4),
         "first_step_ms": round(first_ms, 3),
+        "prewindow_step_ms": round(pre_ms, 4),
+        "workload_window_full_step_ms": round(full_ms, 4),
+        f"workload_{wl.steps}_step_avg_ms": round(wl_avg_ms, 4),
+        f"workload_{wl.steps}_step_avg_steps_per_s": round(1e3 / wl_avg_ms, 3),
         "roofline": {"bound": "hbm", "kernel": "step_unit_kernel (attention + features + score + select + compact)",
                      "achieved": round(step_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(step_gbps / HBM_PEAK_GBPS, 4),
                      "traffic": measured_traffic() if wl.name == W.WORKLOADS[3].name else None,
                      "alg_bytes_per_launch": step_bytes},
     }
+    if copy_gbps:
+        result["copy_gbps"] = round(copy_gbps, 1)
+        result["kv_frac_of_copy"] = round(kv_gbps / copy_gbps, 4)
+        result["roofline"]["frac_of_measured_copy"] = round(step_gbps / copy_gbps, 4)
     if not args.no_cpu_baseline:
         del buf, Q, KN, VN
         torch.cuda.empty_cache()
-        per_unit_step, total = run_oracle_baseline(wl, args.cpu_units, args.cpu_steps)
-        cpu_sps = 1.0 / (per_unit_step * U)
-        threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+        workers = min(16, len(os.sched_getaffinity(0)))
+        t_cpu = time.time()
+        rate, cpu_s = run_oracle_baseline(wl, args.cpu_units, args.cpu_steps, workers)
+        log(f"cpu oracle: {args.cpu_units} units x {args.cpu_steps} steps on {workers} workers, "
+            f"{time.time() - t_cpu:.1f}s wall")
         result["cpu_baseline"] = {
-            "value": cpu_sps, "unit": "decode steps/s", "cores": threads, "kind": "oracle",
-            "sample": f"{args.cpu_units} units x {args.cpu_steps} steady steps "
-                      f"({total:.1f} s), scaled by {U} units per step; numpy float64"}
+            "value": rate / U, "unit": "decode steps/s", "cores": workers, "kind": "oracle",
+            "cpu": cpu_model(),
+            "sample": f"{args.cpu_units} of {U} units x {args.cpu_steps} window-full steady "
+                      f"steps each ({cpu_s:.1f} CPU-s timed), {workers} worker processes x 1 "
+                      f"BLAS thread; extrapolated from {args.cpu_units} units by the unit count; "
+                      f"numpy float64"}
     print(json.dumps(result), flush=True)
 
 
