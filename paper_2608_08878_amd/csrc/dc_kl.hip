@@ -31,9 +31,11 @@ namespace dc {
 constexpr int KL_WAVES = 4;
 constexpr int KL_TILE = 16 * KL_WAVES;   // vocabulary columns per workgroup
 constexpr int KL_KSTEP = 128;            // hidden elements per main-loop iteration
-constexpr int KL_PH = 2048;              // hidden elements of the 16 A rows staged in LDS at a time
+constexpr int KL_PH = 1024;              // hidden elements of the 16 A rows staged per phase
 constexpr int KL_AROW = KL_PH * 2 + 16;  // LDS bytes per staged row (16-byte pad: the 16 rows of one
                                          // 16-lane read group fall in different banks)
+constexpr int KL_ABUF = 16 * KL_AROW;    // one staging buffer; two alternate (double buffering)
+constexpr int KL_SPT = 16 * (KL_PH / 8) / (64 * KL_WAVES);   // 16-byte chunks staged per thread
 
 // g(y) = e^y - 1 - y without cancellation.
 __device__ __forceinline__ float gfun(float y) {
@@ -89,49 +91,79 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   // 4t + kg (both operands use the same map, which the dot product does not
   // see), so each lm-head load instruction reads 64 contiguous bytes of 16
   // rows.  The 16 A rows (8 full, 8 compressed hidden states of this row block)
-  // are shared by the 4 waves: they are staged in LDS 2048 elements at a time
-  // (one read from L2 per workgroup instead of one per wave) and each wave
-  // reads its fragments there.  Two lm-head blocks are in flight per wave;
-  // every load is unconditional (a block past the phase re-reads its last one),
-  // so a wait covers only the block it consumes.
+  // are shared by the 4 waves: they are staged in LDS KL_PH elements (a phase)
+  // at a time, read once per workgroup instead of once per wave, in two
+  // alternating buffers: the next phase's chunks are requested into registers
+  // when a phase starts and written to the other buffer when it ends, so one
+  // barrier per phase suffices and no wave waits for a staging load.  Two
+  // lm-head blocks are in flight per wave, across phase boundaries.  Every load
+  // is unconditional (past the end a load re-reads the last block or chunk),
+  // so a wait covers only the data it consumes.  The blocks feed the matrix
+  // cores in hidden order, 0 .. hidden/128 - 1.
   extern __shared__ __attribute__((aligned(16))) char alds[];
-  const char* arow_lds = alds + i * KL_AROW;
-  auto mma = [&](int lblk, const uint4 (&bv)[4]) {
+  const int nbt = a.hidden / KL_KSTEP;               // lm-head blocks in total
+  constexpr int BPP = KL_PH / KL_KSTEP;               // blocks per phase
+  const int nph = (nbt + BPP - 1) / BPP;
+  auto wload = [&](int gb, uint4 (&bv)[4]) {
+    const int off = (gb < nbt ? gb : nbt - 1) * KL_KSTEP * 2;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) bv[t] = ldg16(brow + off + 16 * (4 * t + kg));
+  };
+  // chunk c of phase ph: row r = c / cpr (0..7 full, 8..15 compressed), chunk c % cpr
+  auto stage_load = [&](int ph, uint4 (&xs)[KL_SPT]) {
+    const int k0 = ph * KL_PH, kn = a.hidden - k0 < KL_PH ? a.hidden - k0 : KL_PH;
+    const int cpr = kn / 8, nch = 16 * cpr;
+#pragma unroll
+    for (int j = 0; j < KL_SPT; ++j) {
+      const int c = threadIdx.x + j * 64 * KL_WAVES;
+      const int cc = c < nch ? c : nch - 1;
+      const int r = cc / cpr, ch = cc - r * cpr;
+      const int kr = rb * 8 + (r & 7);
+      const int krc = kr < a.rows ? kr : a.rows - 1;
+      xs[j] = ldg16((const char*)(r < 8 ? a.h_full : a.h_comp) + ((size_t)krc * a.hidden + k0 + ch * 8) * 2);
+    }
+  };
+  auto stage_store = [&](int ph, char* buf, const uint4 (&xs)[KL_SPT]) {   // rows past `rows`: zeros
+    const int k0 = ph * KL_PH, kn = a.hidden - k0 < KL_PH ? a.hidden - k0 : KL_PH;
+    const int cpr = kn / 8, nch = 16 * cpr;
+#pragma unroll
+    for (int j = 0; j < KL_SPT; ++j) {
+      const int c = threadIdx.x + j * 64 * KL_WAVES;
+      if (c < nch) {
+        const int r = c / cpr, ch = c - r * cpr;
+        const int kr = rb * 8 + (r & 7);
+        *reinterpret_cast<uint4*>(buf + r * KL_AROW + ch * 16) = kr < a.rows ? xs[j] : make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto mma = [&](const char* arow, int lblk, const uint4 (&bv)[4]) {
 #pragma unroll
     for (int t = 0; t < 4; ++t) {
-      const uint4 av = *reinterpret_cast<const uint4*>(arow_lds + (lblk * 16 + 4 * t + kg) * 16);
+      const uint4 av = *reinterpret_cast<const uint4*>(arow + (lblk * 16 + 4 * t + kg) * 16);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
                                                     __builtin_bit_cast(bf16x8_t, bv[t]), acc, 0, 0, 0);
     }
   };
-  for (int k0 = 0; k0 < a.hidden; k0 += KL_PH) {
-    const int kn = a.hidden - k0 < KL_PH ? a.hidden - k0 : KL_PH;
-    const int nb = kn / KL_KSTEP;
-    auto load = [&](int lb, uint4 (&bv)[4]) {
-      const int off = (k0 + (lb < nb ? lb : nb - 1) * KL_KSTEP) * 2;
-#pragma unroll
-      for (int t = 0; t < 4; ++t) bv[t] = ldg16(brow + off + 16 * (4 * t + kg));
-    };
-    uint4 b0[4], b1[4];
-    load(0, b0);
-    load(1, b1);
-    // stage A[16][k0 .. k0 + kn) (rows past `rows` as zeros)
-    __syncthreads();                      // the previous phase's readers are done
-    const int cpr = kn / 8;               // 16-byte chunks per row
-    for (int c = threadIdx.x; c < 16 * cpr; c += 64 * KL_WAVES) {
-      const int r = c / cpr, ch = c - r * cpr;
-      const int kr = rb * 8 + (r & 7);
-      uint4 x = make_uint4(0, 0, 0, 0);
-      if (kr < a.rows)
-        x = ldg16((const char*)(r < 8 ? a.h_full : a.h_comp) + ((size_t)kr * a.hidden + k0 + ch * 8) * 2);
-      *reinterpret_cast<uint4*>(alds + r * KL_AROW + ch * 16) = x;
-    }
+  {
+    uint4 b0[4], b1[4], xs[KL_SPT];
+    wload(0, b0);
+    wload(1, b1);
+    stage_load(0, xs);
+    stage_store(0, alds, xs);
     __syncthreads();
-    for (int lb = 0; lb < nb; lb += 2) {
-      mma(lb, b0);
-      load(lb + 2, b0);
-      if (lb + 1 < nb) mma(lb + 1, b1);
-      load(lb + 3, b1);
+    for (int ph = 0; ph < nph; ++ph) {
+      stage_load(ph + 1 < nph ? ph + 1 : ph, xs);
+      const char* arow = alds + (ph & 1) * KL_ABUF + i * KL_AROW;
+      const int gb0 = ph * BPP, gb1 = gb0 + BPP < nbt ? gb0 + BPP : nbt;
+      for (int gb = gb0; gb < gb1; gb += 2) {
+        mma(arow, gb - gb0, b0);
+        wload(gb + 2, b0);
+        if (gb + 1 < gb1) mma(arow, gb + 1 - gb0, b1);
+        wload(gb + 3, b1);
+      }
+      // the other buffer was last read in phase ph - 1, before the previous barrier
+      if (ph + 1 < nph) stage_store(ph + 1, alds + ((ph + 1) & 1) * KL_ABUF, xs);
+      __syncthreads();
     }
   }
   // lane holds C[4*kg + r][i] for r < 4: kg 0,1 full rows 0..7, kg 2,3 compressed rows 0..7
@@ -454,7 +486,7 @@ int launch_kl(const KLArgs& a, void* stream) {
   } else {
     const int nrb = (a.rows + 7) / 8;
     const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
-    const int lds = 16 * KL_AROW;
+    const int lds = 2 * KL_ABUF;
     hipFuncSetAttribute((const void*)kl_tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
     hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), lds, s, a);
   }
