@@ -113,7 +113,11 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
   const int ri = lane & 15, kg = lane >> 4;
   const int h1 = a.h1, h2 = a.h2, ln = a.ln;
   const int L = unit_rows(a, u);   // this unit's rows (scores_out keeps stride a.L)
-  const float fh1 = (float)h1, fh2 = (float)h2;
+  // LayerNorm: the moments multiply by 1 / width (one rounding more than a
+  // division, far inside the score tolerance) and the scale uses the
+  // hardware reciprocal square root: the IEEE division sequences cost about a
+  // tenth of the kernel's VALU work, which adds to the matrix-core time here
+  const float ih1 = 1.0f / (float)h1, ih2 = 1.0f / (float)h2;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const float bout = const_params(a.params)[h1 * a.n_in + h1 + (ln ? 2 * h1 : 0) + h2 * h1 + h2 +
@@ -175,14 +179,14 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
       s1 += k < h1 ? z : 0.0f;
     }
     if (ln) {
-      const float mean = sum4rows(s1) / fh1;
+      const float mean = sum4rows(s1) * ih1;
       float s2 = 0.0f;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
         const float d = h[s] - mean;
         s2 += (4 * s + kg) < h1 ? d * d : 0.0f;
       }
-      const float rs = 1.0f / __builtin_sqrtf(sum4rows(s2) / fh1 + LN_EPS);
+      const float rs = __builtin_amdgcn_rsqf(__builtin_fmaf(sum4rows(s2), ih1, LN_EPS));
 #pragma unroll
       for (int s = 0; s < NS; ++s)
         h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + 4 * s], p1[O_B1 + 2 * HP + 4 * s]);
@@ -228,14 +232,14 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
       }
       float mean = 0.0f, rs = 1.0f;
       if (ln) {
-        mean = sum16(t1) / fh2;
+        mean = sum16(t1) * ih2;
         float t2 = 0.0f;
 #pragma unroll
         for (int cb = 0; cb < NC; ++cb) {
           const float d = z[cb] - mean;
           t2 += (16 * cb + ri) < h2 ? d * d : 0.0f;
         }
-        rs = 1.0f / __builtin_sqrtf(sum16(t2) / fh2 + LN_EPS);
+        rs = __builtin_amdgcn_rsqf(__builtin_fmaf(sum16(t2), ih2, LN_EPS));
       }
       float o = 0.0f;
 #pragma unroll
