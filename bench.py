@@ -616,6 +616,7 @@ def bench_hybrid(args, wl, dev, log):
 
 LOGZ_OPS_PER_UPDATE = 7     # VALU instructions of one recursion update (see the design notes)
 VALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12   # lane-instructions/s without packed math
+FP32_VECTOR_PEAK_TFLOPS = 157.3                 # MI355X fp32 vector peak (an FMA counts 2)
 
 
 def time_log_partition(wl, U, dev, log, reps=5):
@@ -649,8 +650,14 @@ def time_log_partition(wl, U, dev, log, reps=5):
         out[f"logz_{tag}_ms"] = round(ms, 4)
         out[f"logz_{tag}_shape"] = f"units={U} L={L} B={Bk} K={K}"
         if K > 8:
+            # the method's work: L K updates E_j += x_i E_(j-1) of the subset recursion
+            # (App. C, over K = min(B, L - B) entries), one fused multiply-add each
+            tflops = 2.0 * upd / (ms * 1e-3) / 1e12
+            out[f"logz_{tag}_tflops"] = round(tflops, 2)
+            out[f"logz_{tag}_fma_frac"] = round(tflops / FP32_VECTOR_PEAK_TFLOPS, 4)
+            # issue efficiency of the implementation (7 VALU instructions per update)
             tops = upd * LOGZ_OPS_PER_UPDATE / (ms * 1e-3) / 1e12
-            out[f"logz_{tag}_alu_frac"] = round(tops / VALU_PEAK_TOPS, 4)
+            out[f"logz_{tag}_issue_frac"] = round(tops / VALU_PEAK_TOPS, 4)
         log(f"log-partition {tag}: {ms:.4f} ms ({U} units, L={L}, K={K})")
     return out
 
