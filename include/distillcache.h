@@ -271,6 +271,30 @@ dc_status dc_score_evict_units(const dc_dims *dims, dc_kv *kv, dc_feat *feat, co
                                float *scores_out, int32_t *kept_out, double *logp_out, void *ws,
                                size_t ws_bytes, void *hip_stream);
 
+/* One whole decode step of a ragged cache with per-unit budgets (the
+ * appendix's head-level hybrid: a subset of KV heads keeps its full cache, the
+ * others the policy's budget; Algorithm 1 per unit): dc_decode_step followed by
+ * the deterministic dc_score_evict_units, with the same arguments and outputs
+ * (scores_out [units][kv->len + 1], kept_out [units][min(max_budget,
+ * kv->len + 1)], unit_len and host bookkeeping as after the two calls).  k_new
+ * and v_new are required.  With the four-input one-hidden-layer policy
+ * without LayerNorm, no sigma, bf16 and G >= 4, every unit whose rows after
+ * the append fit on chip (at most a few thousand, two workgroups per CU) runs
+ * the whole step in one launch (K/V read once, per-unit top-B and compaction
+ * before the workgroup exits); longer units (the full-cache heads) take the
+ * chunked decode and then their own scoring and selection.  Otherwise the call
+ * is the two calls in sequence.  Results agree with the two calls to the
+ * tolerances of the kernels (attention and features sum in a different order
+ * on the two paths); the slot map follows the same rule.
+ * Workspace: dc_workspace_bytes(dims, kv->len + 1, 0, 0).
+ * Errors: those of dc_decode_step and dc_score_evict_units; DC_ERR_NULL also
+ * for a missing append; nothing is enqueued unless both validate. */
+dc_status dc_decode_evict_units(const dc_dims *dims, dc_kv *kv, dc_feat *feat,
+                                const dc_policy *policy, const int32_t *budgets, int32_t max_budget,
+                                const void *q, const void *k_new, const void *v_new, void *out,
+                                float *scores_out, int32_t *kept_out, void *ws, size_t ws_bytes,
+                                void *hip_stream);
+
 /* One whole training-mode decode step: dc_decode_step followed by
  * dc_sample_evict with the same policy, budget, noise and outputs, with results
  * and host bookkeeping bit-identical to the two calls in sequence.  Where the

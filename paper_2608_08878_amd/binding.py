@@ -62,6 +62,7 @@ KL_STATIC_MAX_PAIRS = 524288     # rows * (vocab / 64) of one dc_kl_reward_stati
 
 EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evict",
            "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_score_evict_units",
+           "dc_decode_evict_units",
            "dc_subset_log_prob",
            "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_kl_reward_static",
            "dc_reinforce_terms",
@@ -109,6 +110,10 @@ def lib() -> ctypes.CDLL:
                                            ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy), vp,
                                            i32, ctypes.POINTER(dc_gumbel), vp, vp, vp, vp, sz, vp]
         L.dc_score_evict_units.restype = ctypes.c_int
+        L.dc_decode_evict_units.argtypes = [ctypes.POINTER(dc_dims), ctypes.POINTER(dc_kv),
+                                            ctypes.POINTER(dc_feat), ctypes.POINTER(dc_policy),
+                                            vp, i32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.dc_decode_evict_units.restype = ctypes.c_int
         L.dc_subset_log_prob.argtypes = [i32, i32, i32, ctypes.c_float, vp, vp, vp, vp, vp, sz, vp]
         L.dc_subset_log_prob.restype = ctypes.c_int
         L.dc_subset_log_prob_workspace_bytes.argtypes = [i32, i32, i32]
@@ -247,6 +252,15 @@ def dc_decode_sample_evict(dims, kv, feat, policy, budget: int, gumbel, q, k_new
                                         _ref(policy), budget, _ref(gumbel), _ptr(q), _ptr(k_new),
                                         _ptr(v_new), _ptr(out), _ptr(scores_out), _ptr(kept_out),
                                         _ptr(logp_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_decode_evict_units(dims, kv, feat, policy, budgets, max_budget: int, q, k_new, v_new, out,
+                          scores_out=None, kept_out=None, ws=None, ws_bytes: int = 0,
+                          stream=None) -> None:
+    _check(lib().dc_decode_evict_units(ctypes.byref(dims), ctypes.byref(kv), ctypes.byref(feat),
+                                       ctypes.byref(policy), _ptr(budgets), max_budget, _ptr(q),
+                                       _ptr(k_new), _ptr(v_new), _ptr(out), _ptr(scores_out),
+                                       _ptr(kept_out), _ptr(ws), ws_bytes, stream))
 
 
 def dc_score_evict_units(dims, kv, feat, policy, budgets, max_budget: int, gumbel=None,

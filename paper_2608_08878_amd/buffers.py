@@ -153,6 +153,17 @@ class DecodeBuffers:
                                  stream_handle(stream))
         return out
 
+    def decode_evict_units(self, policy, budgets, max_budget, q, k_new, v_new, out=None,
+                           scores_out=None, kept_out=None, stream=None):
+        """One decode step of a ragged cache with per-unit budgets (decode, then the
+        deterministic per-unit selection); units that fit on chip run it in one launch."""
+        if out is None:
+            out = torch.empty_like(q)
+        B.dc_decode_evict_units(self.dims, self.kv, self.feat, policy, budgets, max_budget, q,
+                                k_new, v_new, out, scores_out, kept_out, self.ws, self.ws_bytes,
+                                stream_handle(stream))
+        return out
+
     def score_evict_units(self, policy, budgets, max_budget, gumbel=None, scores_out=None,
                           kept_out=None, logp_out=None, stream=None):
         B.dc_score_evict_units(self.dims, self.kv, self.feat, policy, budgets, max_budget, gumbel,

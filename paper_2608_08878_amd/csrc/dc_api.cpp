@@ -595,6 +595,61 @@ dc_status dc_score_evict_units(const dc_dims* dims, dc_kv* kv, dc_feat* feat, co
   return DC_OK;
 }
 
+dc_status dc_decode_evict_units(const dc_dims* dims, dc_kv* kv, dc_feat* feat,
+                                const dc_policy* policy, const int32_t* budgets, int32_t max_budget,
+                                const void* q, const void* k_new, const void* v_new, void* out,
+                                float* scores_out, int32_t* kept_out, void* ws, size_t ws_bytes,
+                                void* hip_stream) {
+  if (!kv || !feat || !budgets || !kv->unit_len || !k_new || !v_new) return DC_ERR_NULL;
+  dc::DecodeArgs a;
+  bool split = false;
+  size_t need_d = 0, need_e = 0;
+  dc_status st = prep_decode(dims, kv, feat, q, k_new, v_new, out, ws, ws_bytes, a, split, need_d);
+  if (st != DC_OK) return st;
+  dc::EvictArgs e;
+  st = prep_evict(dims, kv, feat, policy, max_budget, scores_out, kept_out, ws, ws_bytes, a.L, a.T,
+                  e, need_e);
+  if (st != DC_OK) return st;
+  e.budgets = budgets;              // per unit, clamped to [1, e.budget] by the kernels
+  const int G = group_of(dims), D = dims->head_dim;
+  // units of up to Lf rows after the append: the single-launch step (decode,
+  // features, the fused one-hidden-layer policy, per-unit top-B, compaction).
+  // Few units take the chunked decode whatever their rows: one workgroup per
+  // unit leaves most of the chip idle (as for uniform caches)
+  const int Lf = dc::step_ragged_rows(G, D);
+  if (e.ext || feat->sigma || Lf < 1 || (int)units_of(dims) < FEW_UNITS) {
+    // the two-call route: chunked decode, then the per-unit selection
+    st = launch_decode_any(dims, a, true, split, hip_stream);
+    if (st != DC_OK) return st;
+    if (ragged_after_decode(kv, a, hip_stream) != DC_OK) return DC_ERR_HIP;
+    if (dc::launch_evict(e, dims->dtype, D, hip_stream) != 0) return DC_ERR_HIP;
+  } else {
+    dc::DecodeArgs af = a;
+    af.L = a.L < Lf ? a.L : Lf;     // the rows one workgroup serves (LDS); longer units leave
+    dc::EvictArgs ef = e;
+    ef.L = a.L;                     // row stride of scores_out
+    if (dc::launch_step(af, &ef, D, G, true, false, hip_stream) != 0) return DC_ERR_HIP;
+    if (a.L > af.L) {
+      // the longer units: chunked decode, then their scoring and selection
+      dc::DecodeArgs ac = a;
+      ac.fused_rows = af.L;
+      st = launch_decode_any(dims, ac, true, true, hip_stream);
+      if (st != DC_OK) return st;
+    }
+    // every kernel of the decode has read the old lengths
+    if (ragged_after_decode(kv, a, hip_stream) != DC_OK) return DC_ERR_HIP;
+    if (a.L > af.L) {
+      dc::EvictArgs el = e;
+      el.fused_rows = af.L;
+      if (dc::launch_evict(el, dims->dtype, D, hip_stream) != 0) return DC_ERR_HIP;
+    }
+  }
+  if (ragged_after_evict(kv, e, budgets, e.budget, hip_stream) != DC_OK) return DC_ERR_HIP;
+  commit_decode(kv, feat, a, dims->ent_window);
+  kv->len = e.budget;
+  return DC_OK;
+}
+
 dc_status dc_subset_log_prob(int32_t units, int32_t len, int32_t budget, float tau,
                              const float* scores, const int32_t* kept, double* logz_out,
                              double* logp_out, void* ws, size_t ws_bytes, void* hip_stream) {

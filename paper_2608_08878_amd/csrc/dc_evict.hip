@@ -68,6 +68,7 @@ __global__ void __launch_bounds__(256) score_kernel(EvictArgs a, uint64_t* keys,
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = unit_rows(a, u);
+  if (L <= a.fused_rows) return;                         // served by the single-launch step
   if (!a.scores_out && unit_budget(a, u) >= L) return;   // a unit that keeps every row reads no key
   for (int base = blockIdx.x * 256; base < L; base += gridDim.x * 256) {
     const int r = base + threadIdx.x;
@@ -90,6 +91,7 @@ __global__ void __launch_bounds__(256) score_ext_kernel(EvictArgs a, uint64_t* k
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = unit_rows(a, u);
+  if (L <= a.fused_rows) return;                         // served by the single-launch step
   if (!a.scores_out && unit_budget(a, u) >= L) return;   // a unit that keeps every row reads no key
   for (int base = blockIdx.x * 256; base < L; base += gridDim.x * 256) {
     const int r = base + threadIdx.x;
@@ -109,6 +111,7 @@ __global__ void __launch_bounds__(ENT) select_kernel(EvictArgs a, const uint64_t
   __shared__ SelShared sh;
   const int u = blockIdx.x;
   const int L = unit_rows(a, u);
+  if (L <= a.fused_rows) return;        // served by the single-launch step
   const int Bu = unit_budget(a, u);
   if (Bu >= L) {                        // (per-unit budgets) this unit keeps every row
     if (a.kept_out)

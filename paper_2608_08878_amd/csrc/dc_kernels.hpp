@@ -45,6 +45,8 @@ struct DecodeArgs {
                         // past L are padding that absorbs the stores of lanes without a row)
   int chunk;
   int nchunks;
+  int fused_rows;       // ragged caches: units of at most this many rows after the append were
+                        // served by the single-launch kernel; the chunked kernels skip them (0: none)
 };
 
 struct EvictArgs {
@@ -80,6 +82,8 @@ struct EvictArgs {
   int sample;           // 1: rank by the Gumbel-perturbed score s / tau + g (training mode)
   float tau;            // sampling temperature
   uint32_t seed0, seed1, draw;  // Philox key and draw number of the Gumbel noise
+  int fused_rows;       // ragged caches: units of at most this many rows were scored, selected
+                        // and compacted by the single-launch step; these kernels skip them (0: none)
 };
 
 // Log-partition / log-probability of size-B subsets (one call covers every unit).
@@ -173,6 +177,9 @@ int global_alpha_groups(int per_seq);    // unit groups of one sequence (workspa
 int launch_step(const DecodeArgs& a, const EvictArgs* e, int D, int G, bool feat, bool chunked,
                 void* stream);
 bool step_fits(int L, int G, int D, bool feat, int nmoves);
+// Ragged caches: the most rows per unit (after the append) the single-launch
+// step serves at two workgroups per CU, or 0 when it serves no unit of this shape.
+int step_ragged_rows(int G, int D);
 int step_chunk_rows();
 int kl_tile_cols();
 

@@ -106,6 +106,7 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
   constexpr int NC = HP / 16;    // 16-column blocks of layer 2
   extern __shared__ float sm[];
   // a unit that keeps every row reads no key (the whole workgroup leaves)
+  if (unit_rows(a, a.y0 + blockIdx.y) <= a.fused_rows) return;    // served by the single-launch step
   if (!a.scores_out && unit_budget(a, a.y0 + blockIdx.y) >= unit_rows(a, a.y0 + blockIdx.y)) return;
   stage<HP>(a, sm);
   __syncthreads();

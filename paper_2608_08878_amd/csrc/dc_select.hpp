@@ -310,8 +310,10 @@ __device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, 
 // rows k*NT + tid for k < kpt (invalid rows beyond L are ignored); NT is the
 // workgroup size.
 // Keep the top B of unit u's L rows (B < L) and compact; kept_out rows have
-// stride a.ld_kept.
-template <typename Keys, int DTYPE, int D, int NT = ENT>
+// stride a.ld_kept.  Move j of the plan is the pair (hole, mover) at
+// mv[MS j], mv[MS j + 1] (MS = 2: a dense list; a larger stride lets the list
+// share row slots with the keys, move j beside row j's key).
+template <typename Keys, int DTYPE, int D, int NT = ENT, int MS = 2>
 __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Keys& keys, int kpt,
                                SelShared& sh, int* mv) {
   constexpr int ELT = DTYPE == 0 ? 4 : 2;
@@ -451,8 +453,8 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
     const bool mover = r >= B && r < L && !ev;
     int rk0, rk1, t0, t1;
     block_scan2<NT>(hole, mover, rk0, rk1, t0, t1, sh);
-    if (hole) mv[2 * (run0 + rk0)] = r;
-    if (mover) mv[2 * (run1 + rk1) + 1] = r;
+    if (hole) mv[MS * (run0 + rk0)] = r;
+    if (mover) mv[MS * (run1 + rk1) + 1] = r;
     if (a.kept_out && r < B && !ev) a.kept_out[(size_t)u * a.ld_kept + r] = r;
     run0 += t0;
     run1 += t1;
@@ -500,8 +502,8 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
       const int j = j0 + q * ngrp;
       ok[q] = j < nm;
       const int jj = ok[q] ? j : j0;         // past the list: re-read a listed move, no store
-      gd[q] = ub + mv[2 * jj];
-      gs[q] = ub + mv[2 * jj + 1];
+      gd[q] = ub + mv[MS * jj];
+      gs[q] = ub + mv[MS * jj + 1];
 #pragma unroll
       for (int cc = 0; cc < CPL; ++cc) {
         const int c = gl + 16 * cc < N16 ? gl + 16 * cc : N16 - 1;

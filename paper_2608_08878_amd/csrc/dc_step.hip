@@ -518,10 +518,18 @@ struct RowStride {
 
 // SMP: training-mode ranking by the Gumbel-perturbed score; the unperturbed
 // score is kept in the row's LDS slot beside its key (needs RS >= 4, G >= 4).
-template <int D, int G, bool FEAT, bool EVICT, bool SIG = false, bool SMP = false>
+// RAG: ragged cache with per-unit budgets (e.budgets).  Unit u has its own rows
+// (unit_len[u] + the append) and budget; a.L bounds the rows a workgroup serves
+// (it sizes the LDS), and a unit with more rows leaves at once (the chunked
+// kernels serve it).  The compaction plan sits in the free half of the rows'
+// LDS slots beside the keys (move j beside row j's key: at most L / 2 moves,
+// however many rows the unit evicts), so it needs RS >= 4 (G >= 4).
+template <int D, int G, bool FEAT, bool EVICT, bool SIG = false, bool SMP = false, bool RAG = false>
 __global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArgs a, EvictArgs e) {
   static_assert(!SIG || (FEAT && !EVICT), "sigma is stored by the decode-only variant");
   static_assert(!SMP || (EVICT && RowStride<G>::RS >= 4), "sampling keeps the score beside the key");
+  static_assert(!RAG || (FEAT && EVICT && !SIG && !SMP && RowStride<G>::RS >= 4),
+                "the ragged variant plans its moves beside the keys");
   constexpr int LPR = MG<D>::LPR;
   constexpr int RS = RowStride<G>::RS, KS = RowStride<G>::KS;
   extern __shared__ float lds[];
@@ -529,7 +537,10 @@ __global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArg
   __shared__ float stat[SNW * 2 * G + 2 * G];
   __shared__ float newnorm_slot;
   const int u = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int L = a.L;
+  const int L = RAG ? len_old_of(a, u) + a.append : a.L;
+  if constexpr (RAG) {
+    if (L > a.L || L < 1) return;                     // whole workgroup: the chunked kernels' unit
+  }
   float* sbuf = lds;                                  // row stride RS
   float* obuf = lds + (size_t)L * RS;                 // (SNW / 2) * G * D
   int* mv = (int*)(obuf + (SNW / 2) * G * D);
@@ -690,22 +701,34 @@ __global__ void __launch_bounds__(SNT, G > 4 ? 2 : 4) step_unit_kernel(DecodeArg
     if (a.window > 0) write_ring2<D, G>(a, u, M, invl, H);
     if constexpr (EVICT) {
       __syncthreads();
+      // row stride of scores_out: the unit's rows, or the bound of a ragged cache
+      const size_t lso = RAG ? (size_t)e.L : (size_t)L;
       if (e.scores_out) {
         // the scores: beside the keys when sampling, else recovered from the
         // ranking keys (-0 reads back as +0)
         for (int r = tid; r < L; r += SNT) {
           if constexpr (SMP) {
-            e.scores_out[(size_t)u * L + r] = sbuf[(size_t)r * RS + 2];
+            e.scores_out[(size_t)u * lso + r] = sbuf[(size_t)r * RS + 2];
           } else {
             const uint32_t k = (uint32_t)(keys[(size_t)r * KS] >> 32);
             const uint32_t bits = (k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k;
-            e.scores_out[(size_t)u * L + r] = __uint_as_float(bits);
+            e.scores_out[(size_t)u * lso + r] = __uint_as_float(bits);
           }
         }
       }
-      if (e.evict) {
-        const int nslots = (L + SNT - 1) / SNT;
-        LdsKeys<S_KMAX, SNT> lk{keys, KS};
+      const int nslots = (L + SNT - 1) / SNT;
+      LdsKeys<S_KMAX, SNT> lk{keys, KS};
+      if constexpr (RAG) {
+        const int Bu = unit_budget(e, u);
+        if (Bu < L) {
+          select_compact<LdsKeys<S_KMAX, SNT>, 1, D, SNT, RS>(e, u, L, Bu, lk, nslots, sh,
+                                                             reinterpret_cast<int*>(sbuf) + 2);
+          if (e.kept_out)     // slots past this unit's budget
+            for (int r = Bu + tid; r < e.ld_kept; r += SNT) e.kept_out[(size_t)u * e.ld_kept + r] = -1;
+        } else if (e.kept_out) {
+          for (int r = tid; r < e.ld_kept; r += SNT) e.kept_out[(size_t)u * e.ld_kept + r] = r < L ? r : -1;
+        }
+      } else if (e.evict) {
         select_compact<LdsKeys<S_KMAX, SNT>, 1, D, SNT>(e, u, L, e.budget, lk, nslots, sh, mv);
       } else if (e.kept_out) {
         for (int r = tid; r < L; r += SNT) e.kept_out[(size_t)u * L + r] = r;
@@ -740,6 +763,7 @@ __global__ void __launch_bounds__(SNT) stepc_ab_kernel(DecodeArgs a) {
   __shared__ float stat[SNW * 2 * G + 2 * G];
   const int c = blockIdx.x, u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int Lu = len_old_of(a, u) + a.append;       // this unit's rows (ragged caches: per unit)
+  if (Lu <= a.fused_rows) return;                   // served by the single-launch kernel
   const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk), n = r1 - r0;
   if (c == 0 && a.append) append_rows<D>(a, u);
   float* part = a.ws_part + ((size_t)u * a.nchunks + c) * (3 * G + G * D);
@@ -797,6 +821,7 @@ __global__ void __launch_bounds__(SNT) stepc_d_kernel(DecodeArgs a) {
   __shared__ float newnorm_slot;
   const int c = blockIdx.x, u = a.y0 + blockIdx.y, tid = threadIdx.x;
   const int Lu = len_old_of(a, u) + a.append;
+  if (Lu <= a.fused_rows) return;                   // served by the single-launch kernel
   const int r0 = c * a.chunk, r1 = min(Lu, r0 + a.chunk);
   const int PART = 3 * G + G * D;
   const float* parts = a.ws_part + (size_t)u * a.nchunks * PART;
@@ -901,11 +926,20 @@ bool step_fits(int L, int G, int D, bool feat, int nmoves) {
 
 int step_chunk_rows() { return SCHUNK; }
 
+int step_ragged_rows(int G, int D) {
+  if (G < 4) return 0;                            // keys fill the row slots: no room for the plan
+  // two workgroups per CU: half the dynamic LDS budget; rows in registers: S_KMAX per thread
+  int L = S_KMAX * SNT;
+  while (L > 0 && step_lds_bytes(L, G, D, true, 0) > (size_t)S_LDS / 2) --L;
+  return L;
+}
+
 template <int D, int G>
 static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, bool chunked,
                          hipStream_t s) {
   if (!chunked) {
-    const int nm = e && e->evict ? (a.L - e->budget < e->budget ? a.L - e->budget : e->budget) : 0;
+    // (the ragged variant plans its moves beside the keys: no separate list)
+    const int nm = e && e->evict && !a.unit_len ? (a.L - e->budget < e->budget ? a.L - e->budget : e->budget) : 0;
     EvictArgs ee;
     if (e) ee = *e;
     else __builtin_memset(&ee, 0, sizeof(ee));
@@ -919,6 +953,10 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
     if (!feat) pick(step_unit_kernel<D, G, false, false>);
     else if (e && e->sample) {
       if constexpr (RowStride<G>::RS >= 4) pick(step_unit_kernel<D, G, true, true, false, true>);
+      else return (int)hipErrorInvalidValue;     // the caller takes the separate path
+    }
+    else if (e && a.unit_len) {
+      if constexpr (RowStride<G>::RS >= 4) pick(step_unit_kernel<D, G, true, true, false, false, true>);
       else return (int)hipErrorInvalidValue;     // the caller takes the separate path
     }
     else if (e) pick(step_unit_kernel<D, G, true, true>);

@@ -282,6 +282,27 @@ def test_score_evict_units_rejects_bad_arguments():
     assert kv.len == 50
 
 
+def test_decode_evict_units_rejects_bad_arguments_and_leaves_host_fields():
+    L = B.lib()
+    pol = B.dc_policy(4, 1, (ctypes.c_int32 * 2)(32, 0), FAKE)
+
+    def call(kv, feat=None, budgets=FAKE, maxb=64, kn=FAKE, vn=FAKE, ws=None, wsb=0, dims=None):
+        return L.dc_decode_evict_units(ctypes.byref(dims or _dims()), ctypes.byref(kv),
+                                       ctypes.byref(feat or _feat()), ctypes.byref(pol), budgets,
+                                       maxb, FAKE, kn, vn, FAKE, FAKE, FAKE, ws, wsb, None)
+
+    kv = B.dc_kv(FAKE, FAKE, 50, FAKE)
+    feat = _feat()
+    assert call(kv, feat, budgets=None) == 1
+    assert call(B.dc_kv(FAKE, FAKE, 50, None), feat) == 1      # per-unit lengths are required
+    assert call(kv, feat, kn=None, vn=None) == 1                # a step appends
+    assert call(kv, feat, maxb=0, ws=FAKE, wsb=1 << 40) == 5
+    assert call(kv, feat) == 6                                  # the chunked decode needs the workspace
+    assert call(kv, feat, dims=_dims(dtype=B.DC_F32)) == 3      # ragged caches are bf16
+    assert call(B.dc_kv(FAKE, FAKE, 100, FAKE), feat, ws=FAKE, wsb=1 << 40) == 4   # capacity
+    assert kv.len == 50 and feat.step == 5 and feat.next_pos == 50
+
+
 def test_ragged_decode_needs_bf16_and_moves_fit_on_chip():
     L = B.lib()
     kv = B.dc_kv(FAKE, FAKE, 10, FAKE)

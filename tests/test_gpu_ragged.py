@@ -182,3 +182,125 @@ def test_units_that_keep_every_row_are_not_scored_without_scores_out(hidden):
             if budgets[u] >= wl.n0 + t + 1:              # covering: its rows before the selection
                 assert np.array_equal(a["pos"], np.arange(wl.n0 + t + 1)), (t, u)
                 assert np.array_equal(H.to_np(kept[1][u])[:lens[0][u]], np.arange(lens[0][u]))
+
+
+def _fused_ragged_run(pattern, steps, n0, batch=32):
+    """dc_decode_evict_units (one call per step) on free-running device and oracle
+    trajectories, on enough units for the single-launch route (unit u keeps the
+    budget of KV head u mod len(pattern)); the oracle follows unit 0, the last
+    unit and six seeded random units: attention output, scores, the slot map
+    (exactly, under the oracle's selection and compaction of the GPU's scores),
+    lengths and the post-step state, until a selection lands in the near-tie band."""
+    wl = W.WORKLOADS[2].scaled(batch=batch, n_kv_heads=len(pattern), n_q_heads=4 * len(pattern),
+                               n0=n0, budget=max(pattern), steps=steps)
+    U = wl.units
+    assert U >= 128
+    budgets = [pattern[u % len(pattern)] for u in range(U)]
+    buf = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                        wl.capacity, wl.dtype, wl.ent_window, 0.0, True, ragged=True)
+    buf.reserve_workspace(wl.capacity)
+    sg.init_cache(wl, buf.k, buf.v, U, buf.cap)
+    buf.feat_init(n0, 0)
+    params, pol = _policy(wl)
+    pnp = H.to_np(params)
+    bud = torch.tensor(budgets, dtype=torch.int32, device="cuda")
+    maxb = max(budgets)
+    rng = np.random.default_rng(wl.seed)
+    sample = sorted({0, U - 1, *rng.choice(np.arange(1, U - 1), 6, replace=False).tolist()})
+    sts = {u: H.oracle_student(wl, u) for u in sample}
+    q, kn, vn = _step_tensors(wl)
+    for t in range(steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        Lb = buf.kv.len + 1
+        scores = torch.full((U, Lb), float("nan"), dtype=torch.float32, device="cuda")
+        kept = torch.full((U, min(maxb, Lb)), -7, dtype=torch.int32, device="cuda")
+        if t % 16 == 0:
+            print(f"one-call ragged step {t}: bound {Lb} rows", flush=True)
+        out = buf.decode_evict_units(pol, bud, maxb, q, kn, vn, scores_out=scores, kept_out=kept)
+        torch.cuda.synchronize()
+        outn, sc, kp = H.to_np(out), H.to_np(scores), H.to_np(kept)
+        lens = H.to_np(buf.unit_len).astype(int)
+        diverged = False
+        for u in sample:
+            st = sts[u]
+            att = ounit.decode_step(st, *H.step_inputs_np(wl, t, u))
+            Lu = st.L
+            assert H.rel_err_rows(outn[u], att.o) <= H.OUT_TOL, (t, u)
+            s_or = ounit.scores(st, pnp, wl.hidden)
+            ok, worst = H.vec_ok(sc[u, :Lu], s_or)       # same slots as the oracle so far
+            assert ok, (t, u, "scores", worst)
+            Bu = budgets[u]
+            nk = min(Bu, Lu)
+            assert lens[u] == nk, (t, u, lens[u], nk)
+            # exact: the oracle's selection and compaction on the GPU's own scores
+            assert np.array_equal(kp[u, :nk], H.oracle_slot_map(sc[u, :Lu], st.pos, Bu)), (t, u)
+            assert np.all(kp[u, nk:] == -1), (t, u)
+            post = _download(buf, u, nk)
+            ok, amb, flips = H.selection_check(s_or, st.pos, post["pos"], Bu)
+            assert ok, (t, u, amb, flips)
+            ounit.evict(st, s_or, Bu)
+            if flips == 0:
+                assert np.array_equal(post["pos"], st.pos), (t, u)
+                Z, N = st.hist.sums()
+                for name, ref in (("alpha", st.alpha), ("den", Z), ("num", N)):
+                    ok, worst = H.vec_ok(post[name], ref)
+                    assert ok, (t, u, name, worst)
+            diverged |= flips > 0
+        assert buf.kv.len == min(maxb, Lb)
+        assert np.all(lens == np.minimum(budgets, n0 + t + 1)), t
+        if diverged:
+            print("trajectories parted at a near-tie at step", t)
+            return t
+    return steps
+
+
+def test_one_call_ragged_step_all_units_on_chip():
+    # the full-cache units grow from 701 rows and stay within the single-launch bound
+    assert _fused_ragged_run([200, 10 ** 6, 150, 320], steps=70, n0=700) >= 1
+
+
+def test_one_call_ragged_step_with_long_full_cache_units():
+    # 4601 rows exceed the single-launch bound (4479 rows at head_dim 128, G = 4): step 0
+    # compresses every unit through the chunked decode and the stand-alone selection;
+    # then the budgeted units run in one launch and the full-cache units on the chunked path
+    assert _fused_ragged_run([200, 10 ** 6, 150, 10 ** 6], steps=70, n0=4600) >= 1
+
+
+def test_one_call_ragged_step_equals_the_uniform_single_launch_step():
+    """Equal lengths and budgets: the ragged single-launch variant does exactly
+    what the uniform one does, bit for bit (outputs, scores, slot maps, every
+    state buffer), through the window's retire."""
+    wl = W.WORKLOADS[2].scaled(batch=64, n_kv_heads=2, n_q_heads=8, n0=700, budget=256, steps=70)
+    U, budget = wl.units, wl.budget
+    assert U >= 128
+    uni = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                        wl.capacity, wl.dtype, wl.ent_window, 0.0, True)
+    rag = DecodeBuffers(wl.batch, wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim,
+                        wl.capacity, wl.dtype, wl.ent_window, 0.0, True, ragged=True)
+    for b in (uni, rag):
+        b.reserve_workspace(wl.capacity)
+        sg.init_cache(wl, b.k, b.v, U, b.cap)
+        b.feat_init(wl.n0, 0)
+    _, pol = _policy(wl)
+    bud = torch.full((U,), budget, dtype=torch.int32, device="cuda")
+    q, kn, vn = _step_tensors(wl)
+    for t in range(wl.steps):
+        sg.queries(wl, t, q)
+        sg.new_rows(wl, t, kn, vn, U)
+        L = uni.kv.len + 1
+        sc = [torch.empty((U, L), dtype=torch.float32, device="cuda") for _ in range(2)]
+        kp = [torch.empty((U, min(L, budget)), dtype=torch.int32, device="cuda") for _ in range(2)]
+        o0 = uni.decode_evict(pol, budget, q, kn, vn, scores_out=sc[0], kept_out=kp[0])
+        o1 = rag.decode_evict_units(pol, bud, budget, q, kn, vn, scores_out=sc[1], kept_out=kp[1])
+        torch.cuda.synchronize()
+        assert torch.equal(o0, o1), t
+        assert torch.equal(sc[0], sc[1]) and torch.equal(kp[0], kp[1]), t
+        n = uni.kv.len
+        assert rag.kv.len == n and torch.all(rag.unit_len == n), t
+        for name in ("k", "v", "alpha", "num", "den", "pos", "vnorm", "qring", "qstat"):
+            a0, a1 = getattr(uni, name), getattr(rag, name)
+            if name in ("qring", "qstat"):
+                assert torch.equal(a0, a1), (t, name)
+            else:
+                assert torch.equal(a0[:, :n], a1[:, :n]), (t, name)
