@@ -416,6 +416,198 @@ static void launch_kl_gemm(const KLArgs& a, hipStream_t s) {
   hipLaunchKernelGGL((kl_gemm_kernel<TW, PF>), dim3(8 * nM * ((nN + 7) / 8)), dim3(256), kg_lds<TW>(), s, a);
 }
 
+// Many rows, the larger shape: a 256 x 256 block of logits per workgroup (128
+// kl rows, full and compressed interleaved per 8 as above, against 256
+// vocabulary columns), eight waves of 128 x 64 (32 MFMA 16x16x32 bf16
+// accumulators each, two waves per SIMD).  The hidden dimension goes in
+// windows of 64 elements, so every row is read 128 bytes (one cache line) at a
+// time: the lm-head rows by direct-to-LDS loads (global_load_lds_dwordx4: no
+// registers, no LDS stores) one window ahead, the hidden-state rows by
+// ordinary loads into registers two windows ahead, stored to LDS one window
+// ahead (32 KB each per window; two LDS buffers per operand, 128 KB).  Each
+// load instruction covers 8 rows x 128 bytes; a row's 16-byte chunk c sits at
+// position c ^ (row mod 8) of its 128 LDS bytes (lane j of the instruction
+// loads the chunk that lands at byte 16 j), so the loads and stores are linear
+// in LDS and the MFMA operand reads (lane (i, kg): row i, chunk 4 t + kg) hit
+// eight different bank groups per eight lanes.  Each logit sees the per-step
+// kernel's MFMA sequence (32-element blocks of the hidden dimension in
+// ascending order) and the epilogue keeps kl_gemm_kernel's arithmetic, so the
+// statistics, and the KL, are bit-identical to the other kernels'.  The waits
+// for loads are explicit and count in issue order: at window w each wave waits
+// until only its newest hidden-state loads (window w + 2) may be in flight,
+// then the workgroup meets at a barrier (LDS stores complete before it); the
+// LDS buffers are distinct objects, so the compiler sees which buffer a read
+// touches and adds no wait for loads into the others.  A buffer is refilled
+// only after the barrier that follows every wave's last read of it.
+constexpr int KM_M = 256;                       // logit rows per workgroup (128 kl rows)
+constexpr int KM_N = 256;                       // vocabulary columns per workgroup
+constexpr int KM_BK = 64;                       // hidden elements per window
+constexpr int KM_OP = 256 * KM_BK * 2;          // LDS bytes of one operand's window
+constexpr int KM_WAVES = 8;
+constexpr int KM_LPW = 256 / 8 / KM_WAVES;      // 8-row load instructions per wave and operand
+constexpr int KM_MIN_ROWS = 256;                // from here on this kernel
+
+typedef __attribute__((address_space(3))) void* lds_vptr_t;
+
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+__global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
+  __shared__ __attribute__((aligned(1024))) char ha0[KM_OP];   // hidden-state rows, even windows
+  __shared__ __attribute__((aligned(1024))) char ha1[KM_OP];   // odd windows
+  __shared__ __attribute__((aligned(1024))) char wb0[KM_OP];   // lm-head rows, even windows
+  __shared__ __attribute__((aligned(1024))) char wb1[KM_OP];   // odd windows
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int nM = (a.rows + 127) / 128, nN = (a.vocab + KM_N - 1) / KM_N;
+  const int slot = blockIdx.x >> 3;
+  const int nt = (blockIdx.x & 7) + 8 * (slot / nM), mt = slot % nM;
+  if (nt >= nN) return;                 // whole workgroup: no barrier is skipped
+  const int i = lane & 15, kg = lane >> 4;
+  // load instruction q of this wave: rows 8 (KM_LPW wave + q) + lane / 8 of
+  // each operand, source chunk (lane mod 8) ^ (lane / 8), LDS byte 16 lane of
+  // the instruction's 1 KB
+  const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
+  const char* hsrc[KM_LPW];
+  const char* wsrc[KM_LPW];
+#pragma unroll
+  for (int q = 0; q < KM_LPW; ++q) {
+    const int R = 8 * (KM_LPW * wave + q) + lrow;     // row of the 256 in the tile
+    int r = mt * 128 + 8 * (R >> 4) + (R & 7);        // kl row of logit row R
+    r = r < a.rows ? r : a.rows - 1;                   // past the end: re-read, unused
+    hsrc[q] = (const char*)((R & 15) < 8 ? a.h_full : a.h_comp) + ((size_t)r * a.hidden + 8 * lchunk) * 2;
+    int v = nt * KM_N + R;
+    v = v < a.vocab ? v : a.vocab - 1;
+    wsrc[q] = (const char*)a.w + ((size_t)v * a.hidden + 8 * lchunk) * 2;
+  }
+  const int NW = a.hidden / KM_BK;      // even (hidden % 128 == 0)
+  auto kof = [&](int w) { return 2 * KM_BK * (w < NW ? w : NW - 1); };   // byte offset of window w
+  auto issue_w = [&](char* B, int w) {
+#pragma unroll
+    for (int q = 0; q < KM_LPW; ++q)
+      __builtin_amdgcn_global_load_lds((const void*)(wsrc[q] + kof(w)),
+                                       (lds_vptr_t)(B + (KM_LPW * wave + q) * 1024), 16, 0, 0);
+  };
+  auto load_h = [&](uint4 (&x)[KM_LPW], int w) {
+#pragma unroll
+    for (int q = 0; q < KM_LPW; ++q) x[q] = ldg16(hsrc[q] + kof(w));
+  };
+  auto store_h = [&](char* A, const uint4 (&x)[KM_LPW]) {
+#pragma unroll
+    for (int q = 0; q < KM_LPW; ++q)
+      *reinterpret_cast<uint4*>(A + (KM_LPW * wave + q) * 1024 + 16 * lane) = x[q];
+  };
+  const int wm = wave >> 2, wn = wave & 3;       // rows 128 wm .., columns 64 wn ..
+  f32x4_t acc[8][4];
+#pragma unroll
+  for (int b = 0; b < 8; ++b)
+#pragma unroll
+    for (int c = 0; c < 4; ++c) acc[b][c] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
+  // operand of lane (i, kg) for the 16-row block starting at row R0, k-step t
+  auto frag = [&](const char* X, int R0, int t) {
+    const int r = R0 + i;
+    return *reinterpret_cast<const uint4*>(X + r * 128 + (((4 * t + kg) ^ (r & 7)) << 4));
+  };
+  auto compute = [&](const char* A, const char* B) {
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      uint4 af[8], bf[4];
+#pragma unroll
+      for (int b = 0; b < 8; ++b) af[b] = frag(A, 128 * wm + 16 * b, t);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) bf[c] = frag(B, 64 * wn + 16 * c, t);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+#pragma unroll
+        for (int b = 0; b < 8; ++b)
+          acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[b]),
+                                                              __builtin_bit_cast(bf16x8_t, bf[c]),
+                                                              acc[b][c], 0, 0, 0);
+    }
+  };
+  // Window w: its lm-head rows (direct loads) and the next window's
+  // hidden-state rows (in registers) have landed once only the newest batch
+  // of hidden-state loads (window w + 2) is in flight; meet; refill the
+  // buffers of window w - 1: lm head of window w + 1 by direct loads, hidden
+  // states of window w + 1 from registers; load window w + 3's hidden states
+  // into those registers; compute window w.
+  uint4 h0[KM_LPW], h1[KM_LPW];
+  auto window = [&](const char* A, const char* B, char* An, char* Bn, uint4 (&hn)[KM_LPW], int w) {
+    __builtin_amdgcn_s_waitcnt(0x0070 | KM_LPW);   // vmcnt(KM_LPW), lgkmcnt(0)
+    compiler_fence();
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue_w(Bn, w + 1);
+    compiler_fence();
+    store_h(An, hn);
+    load_h(hn, w + 3);
+    compiler_fence();
+    compute(A, B);
+  };
+  load_h(h0, 0);
+  issue_w(wb0, 0);
+  load_h(h1, 1);
+  __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * KM_LPW));   // vmcnt(2 KM_LPW): window 0's hidden states
+  compiler_fence();
+  store_h(ha0, h0);
+  compiler_fence();
+  load_h(h0, 2);
+  for (int w = 0; w < NW; w += 2) {
+    window(ha0, wb0, ha1, wb1, h1, w);
+    window(ha1, wb1, ha0, wb0, h0, w + 1);
+  }
+  __builtin_amdgcn_s_waitcnt(0x0070);           // vmcnt(0), lgkmcnt(0): nothing outlives the loop
+  compiler_fence();
+  // acc[b][c][r]: logit row 16 b + 4 kg + r of the wave's 128, column 16 c + i;
+  // lanes kg = 0, 1 hold full rows, kg = 2, 3 the same rows compressed.  One
+  // lane swap per pair of row blocks (b, b + 1) gives lanes 0..31 block b and
+  // lanes 32..63 block b + 1, full logit in one register and compressed in the
+  // other, so all 64 lanes form statistics (same arithmetic per row as above).
+  auto epilogue2 = [&](const f32x4_t (&x0)[4], const f32x4_t (&x1)[4], int b) {
+    float lf[4][4], dl[4][4];
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(x0[c][r]),
+                                                         __float_as_uint(x1[c][r]), false, false);
+        const float full = __uint_as_float(sw[0]), comp = __uint_as_float(sw[1]);
+        lf[c][r] = full;
+        dl[c][r] = full - comp;                 // delta = full - compressed logit
+      }
+    const int bb = b + (kg >> 1);               // row block of this half-wave
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      float m = fmaxf(fmaxf(lf[0][r], lf[1][r]), fmaxf(lf[2][r], lf[3][r]));
+      m = max16(m);
+      float p[4], S = 0.0f, T = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        p[c] = __expf(lf[c][r] - m);
+        S = S + sum16(p[c]);
+        T = T + sum16(p[c] * dl[c][r]);
+      }
+      const float mu = T / S;
+      float A = 0.0f;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) A = A + sum16(p[c] * gfun(mu - dl[c][r]));
+      const int row = mt * 128 + 64 * wm + 8 * bb + 4 * (kg & 1) + r;
+      const int tile = (nt * KM_N + 64 * wn) / 64;
+      if (i == 0 && row < a.rows && tile < a.ntiles)
+        *reinterpret_cast<float4*>(a.part + ((size_t)row * a.ntiles + tile) * 4) =
+            make_float4(m, S, mu, A / S);
+    }
+  };
+  epilogue2(acc[0], acc[1], 0);
+  epilogue2(acc[2], acc[3], 2);
+  epilogue2(acc[4], acc[5], 4);
+  epilogue2(acc[6], acc[7], 6);
+}
+
+static void launch_kl_mm(const KLArgs& a, hipStream_t s) {
+  const int nM = (a.rows + 127) / 128, nN = (a.vocab + KM_N - 1) / KM_N;
+  hipLaunchKernelGGL(kl_mm_kernel, dim3(8 * nM * ((nN + 7) / 8)), dim3(64 * KM_WAVES), 0, s, a);
+}
+
 // One workgroup per row: merge the tile statistics (fixed reduction order).
 __global__ void __launch_bounds__(256) kl_merge_kernel(KLArgs a) {
   __shared__ float red[256];
@@ -479,7 +671,9 @@ int kl_tile_cols() { return KL_TILE; }
 
 int launch_kl(const KLArgs& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
-  if (a.rows >= KG_WIDE_ROWS) {
+  if (a.rows >= KM_MIN_ROWS) {
+    launch_kl_mm(a, s);
+  } else if (a.rows >= KG_WIDE_ROWS) {
     launch_kl_gemm<128, 1>(a, s);
   } else if (a.rows >= KG_MIN_ROWS) {
     launch_kl_gemm<64, 2>(a, s);
