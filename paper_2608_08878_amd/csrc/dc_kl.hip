@@ -421,41 +421,44 @@ static void launch_kl_gemm(const KLArgs& a, hipStream_t s) {
 // vocabulary columns), eight waves of 128 x 64 (32 MFMA 16x16x32 bf16
 // accumulators each, two waves per SIMD).  The hidden dimension goes in
 // windows of 64 elements, so every row is read 128 bytes (one cache line) at a
-// time: the lm-head rows by direct-to-LDS loads (global_load_lds_dwordx4: no
-// registers, no LDS stores) one window ahead, the hidden-state rows by
-// ordinary loads into registers two windows ahead, stored to LDS one window
-// ahead (32 KB each per window; two LDS buffers per operand, 128 KB).  Each
-// load instruction covers 8 rows x 128 bytes; a row's 16-byte chunk c sits at
-// position c ^ (row mod 8) of its 128 LDS bytes (lane j of the instruction
-// loads the chunk that lands at byte 16 j), so the loads and stores are linear
-// in LDS and the MFMA operand reads (lane (i, kg): row i, chunk 4 t + kg) hit
-// eight different bank groups per eight lanes.  Each logit sees the per-step
-// kernel's MFMA sequence (32-element blocks of the hidden dimension in
-// ascending order) and the epilogue keeps kl_gemm_kernel's arithmetic, so the
-// statistics, and the KL, are bit-identical to the other kernels'.  The waits
-// for loads are explicit and count in issue order: at window w each wave waits
-// until only its newest hidden-state loads (window w + 2) may be in flight,
-// then the workgroup meets at a barrier (LDS stores complete before it); the
-// LDS buffers are distinct objects, so the compiler sees which buffer a read
-// touches and adds no wait for loads into the others.  A buffer is refilled
-// only after the barrier that follows every wave's last read of it.
+// time.  A window is two stages of 32 KB, its 256 hidden-state rows and its
+// 256 lm-head rows, loaded straight into LDS (global_load_lds_dwordx4: no
+// registers, no LDS stores) through a ring of five stage buffers (160 KB):
+// while a window's two stages feed the matrix cores, the next three stages
+// are in flight.  Each load instruction covers 8 rows x 128 bytes; a row's
+// 16-byte chunk c sits at position c ^ (row mod 8) of its 128 LDS bytes (lane
+// j of the instruction loads the chunk that lands at byte 16 j), so the MFMA
+// operand reads (lane (i, kg): row i, chunk 4 t + kg) hit eight different
+// bank groups per eight lanes.  Each logit sees the per-step kernel's MFMA
+// sequence (32-element blocks of the hidden dimension in ascending order) and
+// the epilogue keeps kl_gemm_kernel's arithmetic, so the statistics, and the
+// KL, are bit-identical to the other kernels'.  The loads into LDS are issued
+// from inline assembly, out of the compiler's sight, and their waits are
+// explicit: they complete in issue order, so at window w each wave waits until
+// only its loads of the stage after the window may be in flight, and then the
+// workgroup meets at a barrier.  A stage buffer is refilled only after the
+// barrier that follows every wave's last read of it (the MFMAs of the
+// previous window have consumed their operands).
 constexpr int KM_M = 256;                       // logit rows per workgroup (128 kl rows)
 constexpr int KM_N = 256;                       // vocabulary columns per workgroup
 constexpr int KM_BK = 64;                       // hidden elements per window
-constexpr int KM_OP = 256 * KM_BK * 2;          // LDS bytes of one operand's window
+constexpr int KM_STG = 256 * KM_BK * 2;         // LDS bytes of one stage (one operand, one window)
+constexpr int KM_SLOTS = 5;                     // stage buffers
 constexpr int KM_WAVES = 8;
-constexpr int KM_LPW = 256 / 8 / KM_WAVES;      // 8-row load instructions per wave and operand
+constexpr int KM_LPW = 256 / 8 / KM_WAVES;      // 8-row load instructions per wave and stage
 constexpr int KM_MIN_ROWS = 256;                // from here on this kernel
 
-typedef __attribute__((address_space(3))) void* lds_vptr_t;
+typedef __attribute__((address_space(3))) char lds_char_t;
 
 __device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
 
+// 16 bytes per lane from global memory to LDS byte lds + 16 lane (lds uniform)
+__device__ __forceinline__ void load_to_lds16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(lds) : "memory", "m0");
+}
+
 __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
-  __shared__ __attribute__((aligned(1024))) char ha0[KM_OP];   // hidden-state rows, even windows
-  __shared__ __attribute__((aligned(1024))) char ha1[KM_OP];   // odd windows
-  __shared__ __attribute__((aligned(1024))) char wb0[KM_OP];   // lm-head rows, even windows
-  __shared__ __attribute__((aligned(1024))) char wb1[KM_OP];   // odd windows
+  __shared__ __attribute__((aligned(1024))) char ring[KM_SLOTS * KM_STG];
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int nM = (a.rows + 127) / 128, nN = (a.vocab + KM_N - 1) / KM_N;
@@ -464,8 +467,8 @@ __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
   if (nt >= nN) return;                 // whole workgroup: no barrier is skipped
   const int i = lane & 15, kg = lane >> 4;
   // load instruction q of this wave: rows 8 (KM_LPW wave + q) + lane / 8 of
-  // each operand, source chunk (lane mod 8) ^ (lane / 8), LDS byte 16 lane of
-  // the instruction's 1 KB
+  // the stage's operand, source chunk (lane mod 8) ^ (lane / 8), LDS byte
+  // 16 lane of the instruction's 1 KB
   const int lrow = lane >> 3, lchunk = (lane & 7) ^ lrow;
   const char* hsrc[KM_LPW];
   const char* wsrc[KM_LPW];
@@ -479,22 +482,20 @@ __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
     v = v < a.vocab ? v : a.vocab - 1;
     wsrc[q] = (const char*)a.w + ((size_t)v * a.hidden + 8 * lchunk) * 2;
   }
-  const int NW = a.hidden / KM_BK;      // even (hidden % 128 == 0)
-  auto kof = [&](int w) { return 2 * KM_BK * (w < NW ? w : NW - 1); };   // byte offset of window w
-  auto issue_w = [&](char* B, int w) {
+  const int NW = a.hidden / KM_BK;
+  const uint32_t ring_lds = (uint32_t)(size_t)(lds_char_t*)ring;
+  // stage t: window t / 2 (past the last window: the last one again), its
+  // hidden-state rows for even t and its lm-head rows for odd t, into buffer t mod 5
+  auto issue = [&](int t) {
+    const int w = (t >> 1) < NW ? (t >> 1) : NW - 1;
+    const uint32_t dst = ring_lds + (t % KM_SLOTS) * KM_STG + KM_LPW * wave * 1024;
+    if (t & 1) {
 #pragma unroll
-    for (int q = 0; q < KM_LPW; ++q)
-      __builtin_amdgcn_global_load_lds((const void*)(wsrc[q] + kof(w)),
-                                       (lds_vptr_t)(B + (KM_LPW * wave + q) * 1024), 16, 0, 0);
-  };
-  auto load_h = [&](uint4 (&x)[KM_LPW], int w) {
+      for (int q = 0; q < KM_LPW; ++q) load_to_lds16(wsrc[q] + 2 * KM_BK * w, dst + q * 1024);
+    } else {
 #pragma unroll
-    for (int q = 0; q < KM_LPW; ++q) x[q] = ldg16(hsrc[q] + kof(w));
-  };
-  auto store_h = [&](char* A, const uint4 (&x)[KM_LPW]) {
-#pragma unroll
-    for (int q = 0; q < KM_LPW; ++q)
-      *reinterpret_cast<uint4*>(A + (KM_LPW * wave + q) * 1024 + 16 * lane) = x[q];
+      for (int q = 0; q < KM_LPW; ++q) load_to_lds16(hsrc[q] + 2 * KM_BK * w, dst + q * 1024);
+    }
   };
   const int wm = wave >> 2, wn = wave & 3;       // rows 128 wm .., columns 64 wn ..
   f32x4_t acc[8][4];
@@ -507,55 +508,55 @@ __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
     const int r = R0 + i;
     return *reinterpret_cast<const uint4*>(X + r * 128 + (((4 * t + kg) ^ (r & 7)) << 4));
   };
+  // k-step 0's operands are read first, then k-step 1's lm-head operands;
+  // k-step 1's hidden-state operands are read one block at a time as k-step 0
+  // releases the registers of that block (blocks in row order)
   auto compute = [&](const char* A, const char* B) {
+    uint4 af[8], bf0[4], bf1[4];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      uint4 af[8], bf[4];
+    for (int b = 0; b < 8; ++b) af[b] = frag(A, 128 * wm + 16 * b, 0);
 #pragma unroll
-      for (int b = 0; b < 8; ++b) af[b] = frag(A, 128 * wm + 16 * b, t);
+    for (int c = 0; c < 4; ++c) bf0[c] = frag(B, 64 * wn + 16 * c, 0);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) bf[c] = frag(B, 64 * wn + 16 * c, t);
+    for (int c = 0; c < 4; ++c) bf1[c] = frag(B, 64 * wn + 16 * c, 1);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
 #pragma unroll
       for (int c = 0; c < 4; ++c)
-#pragma unroll
-        for (int b = 0; b < 8; ++b)
-          acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[b]),
-                                                              __builtin_bit_cast(bf16x8_t, bf[c]),
-                                                              acc[b][c], 0, 0, 0);
+        acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[b]),
+                                                            __builtin_bit_cast(bf16x8_t, bf0[c]),
+                                                            acc[b][c], 0, 0, 0);
+      af[b] = frag(A, 128 * wm + 16 * b, 1);
     }
+#pragma unroll
+    for (int b = 0; b < 8; ++b)
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        acc[b][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[b]),
+                                                            __builtin_bit_cast(bf16x8_t, bf1[c]),
+                                                            acc[b][c], 0, 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 16, 0);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 32, 0);
   };
-  // Window w: its lm-head rows (direct loads) and the next window's
-  // hidden-state rows (in registers) have landed once only the newest batch
-  // of hidden-state loads (window w + 2) is in flight; meet; refill the
-  // buffers of window w - 1: lm head of window w + 1 by direct loads, hidden
-  // states of window w + 1 from registers; load window w + 3's hidden states
-  // into those registers; compute window w.
-  uint4 h0[KM_LPW], h1[KM_LPW];
-  auto window = [&](const char* A, const char* B, char* An, char* Bn, uint4 (&hn)[KM_LPW], int w) {
-    __builtin_amdgcn_s_waitcnt(0x0070 | KM_LPW);   // vmcnt(KM_LPW), lgkmcnt(0)
-    compiler_fence();
+  issue(0);
+  issue(1);
+  issue(2);
+  for (int w = 0; w < NW; ++w) {
+    // this wave's loads of window w have landed (those of stage 2 w + 2 may
+    // still be in flight); after the barrier every wave's have
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(KM_LPW) : "memory");
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    issue_w(Bn, w + 1);
-    compiler_fence();
-    store_h(An, hn);
-    load_h(hn, w + 3);
-    compiler_fence();
-    compute(A, B);
-  };
-  load_h(h0, 0);
-  issue_w(wb0, 0);
-  load_h(h1, 1);
-  __builtin_amdgcn_s_waitcnt(0x0F70 | (2 * KM_LPW));   // vmcnt(2 KM_LPW): window 0's hidden states
-  compiler_fence();
-  store_h(ha0, h0);
-  compiler_fence();
-  load_h(h0, 2);
-  for (int w = 0; w < NW; w += 2) {
-    window(ha0, wb0, ha1, wb1, h1, w);
-    window(ha1, wb1, ha0, wb0, h0, w + 1);
+    issue(2 * w + 3);
+    issue(2 * w + 4);
+    compute(ring + ((2 * w) % KM_SLOTS) * KM_STG, ring + ((2 * w + 1) % KM_SLOTS) * KM_STG);
   }
-  __builtin_amdgcn_s_waitcnt(0x0070);           // vmcnt(0), lgkmcnt(0): nothing outlives the loop
+  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // no load into LDS outlives the loop
   compiler_fence();
   // acc[b][c][r]: logit row 16 b + 4 kg + r of the wave's 128, column 16 c + i;
   // lanes kg = 0, 1 hold full rows, kg = 2, 3 the same rows compressed.  One
