@@ -30,12 +30,22 @@ namespace dc {
 
 constexpr int KL_WAVES = 4;
 constexpr int KL_TILE = 16 * KL_WAVES;   // vocabulary columns per workgroup
-constexpr int KL_KSTEP = 128;            // hidden elements per main-loop iteration
-constexpr int KL_PH = 1024;              // hidden elements of the 16 A rows staged per phase
-constexpr int KL_AROW = KL_PH * 2 + 16;  // LDS bytes per staged row (16-byte pad: the 16 rows of one
-                                         // 16-lane read group fall in different banks)
-constexpr int KL_ABUF = 16 * KL_AROW;    // one staging buffer; two alternate (double buffering)
-constexpr int KL_SPT = 16 * (KL_PH / 8) / (64 * KL_WAVES);   // 16-byte chunks staged per thread
+constexpr int KL_BK = 64;                // hidden elements per stage (128 bytes of a row)
+constexpr int KL_STG = (16 + KL_TILE) * KL_BK * 2;   // one stage: 16 hidden-state rows, then the lm-head rows
+constexpr int KL_NS = 5;                 // stage buffers (50 KB: two workgroups per CU)
+
+typedef __attribute__((address_space(3))) char lds_char_t;
+
+__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
+
+// 16 bytes per lane from global memory to LDS byte lds + 16 lane (lds uniform).
+// Issued from inline assembly, out of the compiler's sight: the caller waits
+// for it explicitly (vmcnt; loads complete in issue order).  A load into LDS
+// needs one wait state after a scalar write of M0 (the s_nop).
+__device__ __forceinline__ void load_to_lds16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               : : "v"(g), "s"(lds) : "memory", "m0");
+}
 
 // g(y) = e^y - 1 - y without cancellation.
 __device__ __forceinline__ float gfun(float y) {
@@ -77,95 +87,71 @@ __device__ __forceinline__ float max16(float x) {
 // blocks (many rows: the deferred reward of a whole rollout in one call).
 __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   __shared__ float red[KL_WAVES][8][4];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __shared__ __attribute__((aligned(1024))) char ring[KL_NS * KL_STG];
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nrb = (a.rows + 7) / 8;
   const int slot = blockIdx.x >> 3;
   const int tile = (blockIdx.x & 7) + 8 * (slot / nrb), rb = slot % nrb;
   if (tile >= a.ntiles) return;      // whole workgroup: no barrier is skipped
-  const int n0 = tile * KL_TILE + wave * 16;      // this wave's 16 columns
   const int i = lane & 15, kg = lane >> 4;        // MFMA row/col index, k group
-  // A row i: rows 0..7 full, 8..15 compressed, of kl rows rb*8 + (i & 7)
-  const char* brow = (const char*)a.w + (size_t)(n0 + i) * a.hidden * 2;
+  // The hidden dimension goes in stages of 64 elements, every row read as one
+  // 128-byte line: a stage holds the 16 A rows (rows 0..7 the full, 8..15 the
+  // compressed hidden states of kl rows rb*8 + 0..7) and the workgroup's 64
+  // lm-head rows, loaded straight into LDS (global_load_lds_dwordx4) through a
+  // ring of KL_NS stage buffers, KL_NS - 2 stages in flight while one feeds
+  // the matrix cores.  A load instruction covers 8 rows x 128 bytes (the A
+  // rows: 4 rows, half a wave); row r's 16-byte chunk c sits at position
+  // c ^ (r mod 8) of its 128 LDS bytes (lane j loads the chunk that lands at
+  // byte 16 j), so the operand reads hit eight bank groups per eight lanes.
+  // MFMA t of a stage takes chunk 4t + kg of both operands: the blocks feed
+  // the matrix cores in hidden order, as in the GEMM kernels.  Every load is
+  // unconditional (past the end a stage re-reads the last one), so each wave
+  // issues three loads per stage and a wait counts stages exactly.
+  const int lrow = lane >> 3;
+  const int ar = 4 * wave + lrow;                  // A row of this lane's load (lanes 0..31)
+  int kr = rb * 8 + (ar & 7);
+  kr = kr < a.rows ? kr : a.rows - 1;              // past the end: re-read, unused
+  const char* asrc = (const char*)(ar < 8 ? a.h_full : a.h_comp) +
+                     ((size_t)kr * a.hidden + 8 * ((lane & 7) ^ (ar & 7))) * 2;
+  const char* wsrc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+    wsrc[j] = (const char*)a.w + ((size_t)(tile * KL_TILE + 8 * (2 * wave + j) + lrow) * a.hidden +
+                                  8 * ((lane & 7) ^ lrow)) * 2;
+  const int S = a.hidden / KL_BK;
+  const uint32_t ring_lds = (uint32_t)(size_t)(lds_char_t*)ring;
+  auto issue = [&](int st) {
+    const int off = 2 * KL_BK * (st < S ? st : S - 1);
+    const uint32_t base = ring_lds + (st % KL_NS) * KL_STG;
+    if (lane < 32) load_to_lds16(asrc + off, base + wave * 512);
+    load_to_lds16(wsrc[0] + off, base + 2048 + (2 * wave) * 1024);
+    load_to_lds16(wsrc[1] + off, base + 2048 + (2 * wave + 1) * 1024);
+  };
   f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
-  // Hidden elements go in blocks of 128; MFMA t of a block takes 16-byte chunk
-  // 4t + kg (both operands use the same map, which the dot product does not
-  // see), so each lm-head load instruction reads 64 contiguous bytes of 16
-  // rows.  The 16 A rows (8 full, 8 compressed hidden states of this row block)
-  // are shared by the 4 waves: they are staged in LDS KL_PH elements (a phase)
-  // at a time, read once per workgroup instead of once per wave, in two
-  // alternating buffers: the next phase's chunks are requested into registers
-  // when a phase starts and written to the other buffer when it ends, so one
-  // barrier per phase suffices and no wave waits for a staging load.  Two
-  // lm-head blocks are in flight per wave, across phase boundaries.  Every load
-  // is unconditional (past the end a load re-reads the last block or chunk),
-  // so a wait covers only the data it consumes.  The blocks feed the matrix
-  // cores in hidden order, 0 .. hidden/128 - 1.
-  extern __shared__ __attribute__((aligned(16))) char alds[];
-  const int nbt = a.hidden / KL_KSTEP;               // lm-head blocks in total
-  constexpr int BPP = KL_PH / KL_KSTEP;               // blocks per phase
-  const int nph = (nbt + BPP - 1) / BPP;
-  auto wload = [&](int gb, uint4 (&bv)[4]) {
-    const int off = (gb < nbt ? gb : nbt - 1) * KL_KSTEP * 2;
+  auto mma = [&](const char* X) {
 #pragma unroll
-    for (int t = 0; t < 4; ++t) bv[t] = ldg16(brow + off + 16 * (4 * t + kg));
-  };
-  // chunk c of phase ph: row r = c / cpr (0..7 full, 8..15 compressed), chunk c % cpr
-  auto stage_load = [&](int ph, uint4 (&xs)[KL_SPT]) {
-    const int k0 = ph * KL_PH, kn = a.hidden - k0 < KL_PH ? a.hidden - k0 : KL_PH;
-    const int cpr = kn / 8, nch = 16 * cpr;
-#pragma unroll
-    for (int j = 0; j < KL_SPT; ++j) {
-      const int c = threadIdx.x + j * 64 * KL_WAVES;
-      const int cc = c < nch ? c : nch - 1;
-      const int r = cc / cpr, ch = cc - r * cpr;
-      const int kr = rb * 8 + (r & 7);
-      const int krc = kr < a.rows ? kr : a.rows - 1;
-      xs[j] = ldg16((const char*)(r < 8 ? a.h_full : a.h_comp) + ((size_t)krc * a.hidden + k0 + ch * 8) * 2);
-    }
-  };
-  auto stage_store = [&](int ph, char* buf, const uint4 (&xs)[KL_SPT]) {   // rows past `rows`: zeros
-    const int k0 = ph * KL_PH, kn = a.hidden - k0 < KL_PH ? a.hidden - k0 : KL_PH;
-    const int cpr = kn / 8, nch = 16 * cpr;
-#pragma unroll
-    for (int j = 0; j < KL_SPT; ++j) {
-      const int c = threadIdx.x + j * 64 * KL_WAVES;
-      if (c < nch) {
-        const int r = c / cpr, ch = c - r * cpr;
-        const int kr = rb * 8 + (r & 7);
-        *reinterpret_cast<uint4*>(buf + r * KL_AROW + ch * 16) = kr < a.rows ? xs[j] : make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto mma = [&](const char* arow, int lblk, const uint4 (&bv)[4]) {
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      const uint4 av = *reinterpret_cast<const uint4*>(arow + (lblk * 16 + 4 * t + kg) * 16);
+    for (int t = 0; t < 2; ++t) {
+      const int pos = ((4 * t + kg) ^ (i & 7)) << 4;
+      const uint4 av = *reinterpret_cast<const uint4*>(X + i * 128 + pos);
+      const uint4 bv = *reinterpret_cast<const uint4*>(X + 2048 + (16 * wave + i) * 128 + pos);
       acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                    __builtin_bit_cast(bf16x8_t, bv[t]), acc, 0, 0, 0);
+                                                    __builtin_bit_cast(bf16x8_t, bv), acc, 0, 0, 0);
     }
   };
-  {
-    uint4 b0[4], b1[4], xs[KL_SPT];
-    wload(0, b0);
-    wload(1, b1);
-    stage_load(0, xs);
-    stage_store(0, alds, xs);
-    __syncthreads();
-    for (int ph = 0; ph < nph; ++ph) {
-      stage_load(ph + 1 < nph ? ph + 1 : ph, xs);
-      const char* arow = alds + (ph & 1) * KL_ABUF + i * KL_AROW;
-      const int gb0 = ph * BPP, gb1 = gb0 + BPP < nbt ? gb0 + BPP : nbt;
-      for (int gb = gb0; gb < gb1; gb += 2) {
-        mma(arow, gb - gb0, b0);
-        wload(gb + 2, b0);
-        if (gb + 1 < gb1) mma(arow, gb + 1 - gb0, b1);
-        wload(gb + 3, b1);
-      }
-      // the other buffer was last read in phase ph - 1, before the previous barrier
-      if (ph + 1 < nph) stage_store(ph + 1, alds + ((ph + 1) & 1) * KL_ABUF, xs);
-      __syncthreads();
-    }
+  for (int st = 0; st < KL_NS - 1; ++st) issue(st);
+  for (int st = 0; st < S; ++st) {
+    // this wave's loads of stage st have landed (KL_NS - 2 later stages may be
+    // in flight); after the barrier every wave's have, and every wave is done
+    // with stage st - 1, whose buffer the next issue refills
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(3 * (KL_NS - 2)) : "memory");
+    __builtin_amdgcn_s_barrier();
+    compiler_fence();
+    issue(st + KL_NS - 1);
+    mma(ring + (st % KL_NS) * KL_STG);
   }
+  asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // no load into LDS outlives the loop
+  compiler_fence();
   // lane holds C[4*kg + r][i] for r < 4: kg 0,1 full rows 0..7, kg 2,3 compressed rows 0..7
   float lf[4], lc[4];
 #pragma unroll
@@ -448,15 +434,6 @@ constexpr int KM_WAVES = 8;
 constexpr int KM_LPW = 256 / 8 / KM_WAVES;      // 8-row load instructions per wave and stage
 constexpr int KM_MIN_ROWS = 256;                // from here on this kernel
 
-typedef __attribute__((address_space(3))) char lds_char_t;
-
-__device__ __forceinline__ void compiler_fence() { asm volatile("" ::: "memory"); }
-
-// 16 bytes per lane from global memory to LDS byte lds + 16 lane (lds uniform)
-__device__ __forceinline__ void load_to_lds16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(g), "s"(lds) : "memory", "m0");
-}
-
 __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
   __shared__ __attribute__((aligned(1024))) char ring[KM_SLOTS * KM_STG];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -681,9 +658,7 @@ int launch_kl(const KLArgs& a, void* stream) {
   } else {
     const int nrb = (a.rows + 7) / 8;
     const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
-    const int lds = 2 * KL_ABUF;
-    hipFuncSetAttribute((const void*)kl_tile_kernel, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
-    hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), lds, s, a);
+    hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), 0, s, a);
   }
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();
