@@ -236,14 +236,12 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
 // whichever kernel and row count served it.  Workgroup g runs on
 // XCD g mod 8; the row blocks of one vocabulary block are consecutive on one
 // XCD, so its lm-head slab comes from HBM once and then from that XCD's L2.
-// Two shapes: TW = 64 with two stages in flight (twice the workgroups: the
-// better one up to a few hundred rows, where parallelism and latency decide)
-// and TW = 128 with one (more work per staged byte, for many rows).
+// Used from 16 to 255 rows with TW = 64 and two stages in flight; from 256
+// rows on kl_mm_kernel below serves the call.
 constexpr int KG_M = 128;                       // logit rows per workgroup (64 kl rows)
 constexpr int KG_BK = 64;                       // hidden elements per stage
 constexpr int KG_RS = KG_BK * 2 + 16;           // LDS row stride (bytes)
 constexpr int KG_MIN_ROWS = 16;                 // fewer rows: kl_tile_kernel
-constexpr int KG_WIDE_ROWS = 256;               // from here on the TW = 128 shape
 
 template <int TW>
 constexpr int kg_lds() { return (KG_M + 2 * TW) * KG_RS; }
@@ -318,17 +316,8 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
   };
   // every load is unconditional: past the last stage a load re-reads the last one
   const int last = a.hidden - KG_BK;
-  if constexpr (PF == 1) {
-    gload(0, ra[0], rb[0]);
-    for (int k0 = 0; k0 < a.hidden; k0 += KG_BK) {
-      __syncthreads();                  // the previous stage's readers are done
-      sstore(ra[0], rb[0]);
-      __syncthreads();
-      gload(k0 + KG_BK <= last ? k0 + KG_BK : last, ra[0], rb[0]);
-      compute();
-    }
-  } else {
-    static_assert(PF == 2, "one or two stages in flight");
+  {
+    static_assert(PF == 2, "two stages in flight");
     // (the stage count hidden / 64 is even: hidden is a multiple of 128)
     gload(0, ra[0], rb[0]);
     gload(KG_BK, ra[1], rb[1]);
@@ -651,8 +640,6 @@ int launch_kl(const KLArgs& a, void* stream) {
   hipStream_t s = (hipStream_t)stream;
   if (a.rows >= KM_MIN_ROWS) {
     launch_kl_mm(a, s);
-  } else if (a.rows >= KG_WIDE_ROWS) {
-    launch_kl_gemm<128, 1>(a, s);
   } else if (a.rows >= KG_MIN_ROWS) {
     launch_kl_gemm<64, 2>(a, s);
   } else {
