@@ -2,23 +2,30 @@
 // network: n_in -> h1 -> h2 -> 1, optional LayerNorm, widths up to 128), gfx950.
 //
 // Scoring every cached row with a wide second hidden layer is a dense
-// contraction, [rows x h1] x [h1 x h2], so it runs on v_mfma_f32_16x16x4_f32
-// (float32 operands and accumulation: the same precision as the scalar path).
-// The hidden widths are padded to HP = 64 (both at most 64) or 128.  One wave
-// takes 16 rows at a time:
-//   layer 1 (VALU): lane l computes, for row l % 16, the units k = 4 s + l / 16
-//     (s < HP / 4) -- exactly the A operand MFMA step s needs from that lane --
-//     with LayerNorm moments reduced over the four lanes that share the row;
-//   layer 2 (MFMA): HP / 16 column blocks x HP / 4 k-steps; B comes from W2
-//     staged in LDS as [k][n] with a row stride of HP + 16 floats (the four k
-//     rows one instruction reads fall in different bank quarters);
+// contraction, [rows x h1] x [h1 x h2].  On this part the float32 matrix
+// instructions run at the float32 vector rate and do not overlap the vector
+// work around them, so the contraction runs on the bf16 matrix cores instead,
+// at float32 accuracy: every float32 operand x is split exactly into three
+// bf16 parts x = xh + xm + xl (8 significand bits each: 24 in all), and the
+// product of an activation h and a weight w keeps the six part products down
+// to 2^-24 relative, hl wh + hm wm + hh wl + hm wh + hh wm + hh wh (each exact
+// in float32, accumulated in float32 by v_mfma_f32_16x16x32_bf16); the three
+// dropped ones are below 2^-31 relative.  The hidden widths are padded to
+// HP = 64 (both at most 64) or 128.  One wave takes 16 rows at a time:
+//   layer 1 (VALU): lane (i, g) computes, for row i, the units
+//     k = 32 t + 8 g + j (j < 8) -- the eight operand values MFMA k-step t
+//     needs from that lane -- with LayerNorm moments reduced over the four
+//     lanes that share the row;
+//   layer 2 (MFMA): HP / 16 column blocks x HP / 32 k-steps x 6 part products;
+//     the weight parts sit in LDS as three [n][k] bf16 arrays with a row
+//     stride of 2 HP + 16 bytes (the 16 rows one read touches start 16 bytes
+//     apart in the banks), split once per workgroup;
 //   the accumulators hold row 4 (l / 16) + i, column 16 cb + l % 16: LayerNorm
 //     moments, ReLU and the output dot product reduce over the 16 lanes of a
 //     DPP row.
-// 512-thread workgroups: at HP = 128 the 78 KB of staged weights allow two per
-// CU, so eight waves share each copy (four per SIMD); at HP = 64 (23 KB) three.
-// Padded units (k >= h1, n >= h2) are exact zeros and are left out of the
-// LayerNorm moments.
+// HP = 128: 1024-thread workgroups (108 KB of LDS, one per CU, four waves per
+// SIMD); HP = 64: 512 threads (30 KB, two per CU).  Padded units (k >= h1,
+// n >= h2) are exact zeros and are left out of the LayerNorm moments.
 #include <hip/hip_runtime.h>
 
 #include "dc_mlp.hpp"
@@ -30,22 +37,29 @@ namespace dc {
 
 namespace {
 
-constexpr int MT = 512;              // 8 waves share one staged copy of the weights
-constexpr int MW = MT / 64;
 constexpr int NX = 5;                // padded input width
 typedef float f32x4_v __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) const char lchar;
 
-// LDS layout (floats) for hidden widths padded to HP (64 or 128); the small
-// arrays first, so that every per-lane read of them is a constant offset within
-// the 64 KB reach of an LDS instruction
+template <int HP>
+struct Cfg {
+  static constexpr int MT = HP == 128 ? 1024 : 512;    // threads per workgroup
+  static constexpr int MINB = HP == 128 ? 1 : 2;       // workgroups per CU
+  static constexpr int MW = MT / 64;                   // waves
+};
+
+// LDS layout for hidden widths padded to HP (64 or 128): the float arrays
+// first, so that every per-lane read of them is a constant offset within the
+// 64 KB reach of an LDS instruction, then the three bf16 parts of W2
 template <int HP>
 struct Lay {
-  static constexpr int W2S = HP + 16;                 // row stride of W2
-  static constexpr int O_W1 = 0;                      // [NX][HP]  W1 transposed (unit-contiguous)
+  static constexpr int RS = 2 * HP + 16;              // bytes per W2 row (unit n, k contiguous)
+  static constexpr int O_W1 = 0;                      // floats: [NX][HP] W1 transposed
   static constexpr int O_B1 = O_W1 + HP * NX;         // b1, g1, be1       [HP] each
   static constexpr int O_B2 = O_B1 + 3 * HP;          // b2, g2, be2, wo   [HP] each
-  static constexpr int O_W2 = O_B2 + 4 * HP;          // [HP][W2S]  W2 as [k][n]
-  static constexpr int FLOATS = O_W2 + HP * W2S;
+  static constexpr int FLOATS = O_B2 + 4 * HP;
+  static constexpr int O_W2 = FLOATS * 4;             // bytes: parts h, m, l, [3][HP][RS]
+  static constexpr int BYTES = O_W2 + 3 * HP * RS;
 };
 
 template <int CTRL>
@@ -65,10 +79,20 @@ __device__ __forceinline__ float sum4rows(float x) {  // over lanes l, l^16, l^3
   return x;
 }
 
+// x = h + m + l exactly (three round-to-nearest bf16 parts; each residual is
+// exact in float32: it holds at most the 16, then 8, bits below the part taken)
+__device__ __forceinline__ void split3(float x, __bf16& h, __bf16& m, __bf16& l) {
+  h = (__bf16)x;
+  const float r1 = x - (float)h;
+  m = (__bf16)r1;
+  const float r2 = r1 - (float)m;
+  l = (__bf16)r2;
+}
+
 template <int HP>
 __device__ void stage(const EvictArgs& a, float* sm) {
   using Y = Lay<HP>;
-  constexpr int W2S = Y::W2S, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2, O_W2 = Y::O_W2;
+  constexpr int MT = Cfg<HP>::MT, RS = Y::RS, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2;
   const cfloat* P = const_params(a.params);
   const int h1 = a.h1, h2 = a.h2, nin = a.n_in, ln = a.ln;
   const cfloat* W1 = P;
@@ -80,9 +104,14 @@ __device__ void stage(const EvictArgs& a, float* sm) {
   const cfloat* g2 = b2 + h2;
   const cfloat* be2 = g2 + h2;
   const cfloat* wo = b2 + h2 + (ln ? 2 * h2 : 0);
-  for (int i = threadIdx.x; i < HP * W2S; i += MT) {
-    const int k = i / W2S, n = i % W2S;
-    sm[O_W2 + i] = (k < h1 && n < h2) ? W2[n * h1 + k] : 0.0f;
+  char* w2 = reinterpret_cast<char*>(sm) + Y::O_W2;
+  for (int e = threadIdx.x; e < HP * HP; e += MT) {
+    const int n = e / HP, k = e % HP;
+    __bf16 wh, wm, wl;
+    split3((k < h1 && n < h2) ? W2[n * h1 + k] : 0.0f, wh, wm, wl);
+    *reinterpret_cast<__bf16*>(w2 + n * RS + 2 * k) = wh;
+    *reinterpret_cast<__bf16*>(w2 + (HP + n) * RS + 2 * k) = wm;
+    *reinterpret_cast<__bf16*>(w2 + (2 * HP + n) * RS + 2 * k) = wl;
   }
   for (int i = threadIdx.x; i < HP; i += MT) {
     const bool v2 = i < h2, v1 = i < h1;
@@ -98,11 +127,12 @@ __device__ void stage(const EvictArgs& a, float* sm) {
   }
 }
 
-template <int HP, int MINB>
-__global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
+template <int HP, bool LN>
+__global__ void __launch_bounds__(Cfg<HP>::MT, Cfg<HP>::MINB)
+score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
   using Y = Lay<HP>;
-  constexpr int W2S = Y::W2S, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2, O_W2 = Y::O_W2;
-  constexpr int NS = HP / 4;     // MFMA k-steps (4 units each)
+  constexpr int MW = Cfg<HP>::MW, RS = Y::RS, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2;
+  constexpr int NT = HP / 32;    // MFMA k-steps (32 units each)
   constexpr int NC = HP / 16;    // 16-column blocks of layer 2
   extern __shared__ float sm[];
   // a unit that keeps every row reads no key (the whole workgroup leaves)
@@ -112,17 +142,16 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
   __syncthreads();
   const int u = a.y0 + blockIdx.y, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int ri = lane & 15, kg = lane >> 4;
-  const int h1 = a.h1, h2 = a.h2, ln = a.ln;
+  const int h1 = a.h1, h2 = a.h2;
   const int L = unit_rows(a, u);   // this unit's rows (scores_out keeps stride a.L)
   // LayerNorm: the moments multiply by 1 / width (one rounding more than a
   // division, far inside the score tolerance) and the scale uses the
-  // hardware reciprocal square root: the IEEE division sequences cost about a
-  // tenth of the kernel's VALU work, which adds to the matrix-core time here
+  // hardware reciprocal square root
   const float ih1 = 1.0f / (float)h1, ih2 = 1.0f / (float)h2;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
-  const float bout = const_params(a.params)[h1 * a.n_in + h1 + (ln ? 2 * h1 : 0) + h2 * h1 + h2 +
-                                            (ln ? 2 * h2 : 0) + h2];
+  const float bout = const_params(a.params)[h1 * a.n_in + h1 + (LN ? 2 * h1 : 0) + h2 * h1 + h2 +
+                                            (LN ? 2 * h2 : 0) + h2];
   // features of this lane's A row (the four lanes of a row load the same row);
   // the next row block's are requested while the current one is computed
   struct Feat {
@@ -164,62 +193,102 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
         x[4] = 0.0f;
       }
     }
-    // layer 1: units k = 4 s + kg (the weights are re-read from LDS per row
-    // block: held across blocks they would take 256 registers)
-    const lfloat* p1 = (const lfloat*)sm + kg;  // LDS, this lane's unit offset; all reads below
-    asm volatile("" : "+v"(p1));                // are constant offsets from it
-    float h[NS];
+    // layer 1: units k = 32 t + 8 kg + j, eight consecutive units per k-step,
+    // so every weight read is a 16-byte LDS load at a constant offset (the
+    // weights are re-read per row block: held across blocks they would take
+    // 256 registers).  Padded units (k >= h1) have zero weights, bias, gain
+    // and shift, so they come out exactly 0 here, after the LayerNorm and
+    // after the ReLU: only the variance sum needs a mask.
+    typedef __attribute__((address_space(3))) const f32x4_v lfloat4;
+    const lfloat* p1 = (const lfloat*)sm + 8 * kg;   // LDS, this lane's unit offset
+    asm volatile("" : "+v"(p1));
+    auto w8 = [&](int off, float (&o)[8]) {         // floats off .. off + 7 from p1
+      const f32x4_v lo = *reinterpret_cast<lfloat4*>(p1 + off);
+      const f32x4_v hi = *reinterpret_cast<lfloat4*>(p1 + off + 4);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        o[j] = lo[j];
+        o[4 + j] = hi[j];
+      }
+    };
+    float h[NT][8];
     float s1 = 0.0f;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const int k = 4 * s + kg;
-      float z = p1[O_B1 + 4 * s];
+    for (int t = 0; t < NT; ++t) {
+      float z[8], w[8];
+      w8(O_B1 + 32 * t, z);
 #pragma unroll
-      for (int i = 0; i < NX; ++i) z = __builtin_fmaf(p1[O_W1 + i * HP + 4 * s], x[i], z);
-      h[s] = z;
-      s1 += k < h1 ? z : 0.0f;
+      for (int i = 0; i < NX; ++i) {
+        w8(O_W1 + i * HP + 32 * t, w);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) z[j] = __builtin_fmaf(w[j], x[i], z[j]);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        h[t][j] = z[j];
+        s1 += z[j];
+      }
     }
-    if (ln) {
+    if (LN) {
       const float mean = sum4rows(s1) * ih1;
       float s2 = 0.0f;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const float d = h[s] - mean;
-        s2 += (4 * s + kg) < h1 ? d * d : 0.0f;
-      }
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float d = h[t][j] - mean;
+          s2 += (32 * t + 8 * kg + j) < h1 ? d * d : 0.0f;
+        }
       const float rs = __builtin_amdgcn_rsqf(__builtin_fmaf(sum4rows(s2), ih1, LN_EPS));
 #pragma unroll
-      for (int s = 0; s < NS; ++s)
-        h[s] = __builtin_fmaf((h[s] - mean) * rs, p1[O_B1 + HP + 4 * s], p1[O_B1 + 2 * HP + 4 * s]);
-    }
+      for (int t = 0; t < NT; ++t) {
+        float g[8], be[8];
+        w8(O_B1 + HP + 32 * t, g);
+        w8(O_B1 + 2 * HP + 32 * t, be);
 #pragma unroll
-    for (int s = 0; s < NS; ++s) h[s] = (4 * s + kg) < h1 ? fmaxf(h[s], 0.0f) : 0.0f;
-    // layer 2 on MFMA
+        for (int j = 0; j < 8; ++j) h[t][j] = __builtin_fmaf((h[t][j] - mean) * rs, g[j], be[j]);
+      }
+    }
+    // layer 2 on the bf16 matrix cores, six part products per k-step and block
     f32x4_v acc[NC];
 #pragma unroll
     for (int cb = 0; cb < NC; ++cb) acc[cb] = (f32x4_v){0.0f, 0.0f, 0.0f, 0.0f};
-    // B of step s + 1 is read while step s's MFMAs run (an opaque pointer per step
-    // keeps the reads from being hoisted further ahead: the whole of W2 would not fit)
-    float bq[2][NC];
-    {
-      const lfloat* br = (const lfloat*)sm + O_W2 + kg * W2S + ri;
-      asm volatile("" : "+v"(br));
 #pragma unroll
-      for (int cb = 0; cb < NC; ++cb) bq[0][cb] = br[16 * cb];
-    }
+    for (int t = 0; t < NT; ++t) {
+      bf16x8_t ah, am, al;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      if (s + 1 < NS) {
-        const lfloat* br = (const lfloat*)sm + O_W2 + (4 * (s + 1) + kg) * W2S + ri;
-        asm volatile("" : "+v"(br));
-#pragma unroll
-        for (int cb = 0; cb < NC; ++cb) bq[(s + 1) & 1][cb] = br[16 * cb];
+      for (int j = 0; j < 8; ++j) {
+        const float v = fmaxf(h[t][j], 0.0f);   // ReLU
+        __bf16 vh, vm, vl;
+        split3(v, vh, vm, vl);
+        ah[j] = vh;
+        am[j] = vm;
+        al[j] = vl;
       }
+      // the weight rows of column block cb, this lane's 8 units of k-step t (an
+      // opaque pointer per k-step keeps the reads from being hoisted out of the
+      // row loop: all of W2's parts would not fit in registers)
+      const lchar* w2 = (const lchar*)sm + Y::O_W2 + ri * RS + (32 * t + 8 * kg) * 2;
+      asm volatile("" : "+v"(w2));
 #pragma unroll
-      for (int cb = 0; cb < NC; ++cb)
-        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x4f32(h[s], bq[s & 1][cb], acc[cb], 0, 0, 0);
+      for (int cb = 0; cb < NC; ++cb) {
+        const bf16x8_t bh = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            w2 + 16 * cb * RS);
+        const bf16x8_t bm = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            w2 + (HP + 16 * cb) * RS);
+        const bf16x8_t bl = *reinterpret_cast<const __attribute__((address_space(3))) bf16x8_t*>(
+            w2 + (2 * HP + 16 * cb) * RS);
+        f32x4_v c = acc[cb];
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bm, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bh, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bm, c, 0, 0, 0);
+        acc[cb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, c, 0, 0, 0);
+      }
     }
-    // rows 4 kg + i of the block, columns 16 cb + ri
+    // rows 4 kg + i of the block, columns 16 cb + ri (padded columns: weights,
+    // bias, gain and shift 0, so exactly 0 but in the variance sum)
     float score[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -229,10 +298,10 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
       for (int cb = 0; cb < NC; ++cb) {
         const int n = 16 * cb + ri;
         z[cb] = acc[cb][i] + sm[O_B2 + n];
-        t1 += n < h2 ? z[cb] : 0.0f;
+        t1 += z[cb];
       }
       float mean = 0.0f, rs = 1.0f;
-      if (ln) {
+      if (LN) {
         mean = sum16(t1) * ih2;
         float t2 = 0.0f;
 #pragma unroll
@@ -246,7 +315,7 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
 #pragma unroll
       for (int cb = 0; cb < NC; ++cb) {
         const int n = 16 * cb + ri;
-        float y = ln ? __builtin_fmaf((z[cb] - mean) * rs, sm[O_B2 + HP + n], sm[O_B2 + 2 * HP + n])
+        float y = LN ? __builtin_fmaf((z[cb] - mean) * rs, sm[O_B2 + HP + n], sm[O_B2 + 2 * HP + n])
                      : z[cb];
         o = __builtin_fmaf(sm[O_B2 + 3 * HP + n], fmaxf(y, 0.0f), o);   // padded units: wo = 0
       }
@@ -271,22 +340,33 @@ __global__ void __launch_bounds__(MT, MINB) score_mlp2_kernel(EvictArgs a, uint6
 }  // namespace
 
 int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* stream) {
-  const int nblk = (a.L + MW * 16 - 1) / (MW * 16);
-  const int gx = nblk < 8 ? nblk : 8;
   // hidden widths up to 64 pad to 64: a quarter of the layer-2 work of 128
   const bool narrow = a.h1 <= 64 && a.h2 <= 64;
-  const void* k = narrow ? (const void*)score_mlp2_kernel<64, 3> : (const void*)score_mlp2_kernel<128, 2>;
-  const size_t lds = (size_t)(narrow ? Lay<64>::FLOATS : Lay<128>::FLOATS) * sizeof(float);
+  const int mw = narrow ? Cfg<64>::MW : Cfg<128>::MW;
+  const int nblk = (a.L + mw * 16 - 1) / (mw * 16);
+  // workgroups per unit: enough for about 2048 in all, each staging the weight
+  // parts once for as many rows as possible
+  int gx = (2048 + a.units - 1) / a.units;
+  gx = gx < nblk ? gx : nblk;
+  gx = gx > 0 ? gx : 1;
+  const bool ln = a.ln != 0;
+  const void* k = narrow ? (ln ? (const void*)score_mlp2_kernel<64, true> : (const void*)score_mlp2_kernel<64, false>)
+                         : (ln ? (const void*)score_mlp2_kernel<128, true> : (const void*)score_mlp2_kernel<128, false>);
+  const size_t lds = (size_t)(narrow ? Lay<64>::BYTES : Lay<128>::BYTES);
   hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   for_grid_y(a.units, [&](int y0, int ny) {
     EvictArgs b = a;
     b.y0 = y0;
-    if (narrow)
-      hipLaunchKernelGGL((score_mlp2_kernel<64, 3>), dim3(gx, ny), dim3(MT), lds, (hipStream_t)stream,
-                         b, keys, kstride);
+    const dim3 grid(gx, ny);
+    const hipStream_t st = (hipStream_t)stream;
+    if (narrow && ln)
+      hipLaunchKernelGGL((score_mlp2_kernel<64, true>), grid, dim3(Cfg<64>::MT), lds, st, b, keys, kstride);
+    else if (narrow)
+      hipLaunchKernelGGL((score_mlp2_kernel<64, false>), grid, dim3(Cfg<64>::MT), lds, st, b, keys, kstride);
+    else if (ln)
+      hipLaunchKernelGGL((score_mlp2_kernel<128, true>), grid, dim3(Cfg<128>::MT), lds, st, b, keys, kstride);
     else
-      hipLaunchKernelGGL((score_mlp2_kernel<128, 2>), dim3(gx, ny), dim3(MT), lds, (hipStream_t)stream,
-                         b, keys, kstride);
+      hipLaunchKernelGGL((score_mlp2_kernel<128, false>), grid, dim3(Cfg<128>::MT), lds, st, b, keys, kstride);
   });
   return (int)hipGetLastError();
 }
