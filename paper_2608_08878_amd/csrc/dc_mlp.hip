@@ -12,19 +12,22 @@
 // in float32, accumulated in float32 by v_mfma_f32_16x16x32_bf16); the three
 // dropped ones are below 2^-31 relative.  The hidden widths are padded to
 // HP = 64 (both at most 64) or 128.  One wave takes 16 rows at a time:
-//   layer 1 (VALU): lane (i, g) computes, for row i, the units
-//     k = 32 t + 8 g + j (j < 8) -- the eight operand values MFMA k-step t
-//     needs from that lane -- with LayerNorm moments reduced over the four
-//     lanes that share the row;
+//   layer 1 (MFMA, the same split, inputs padded to 32): per 16-unit block b,
+//     W1 (16 units x 32 inputs) times the rows' features (32 x 16 rows), so
+//     lane (i, g) receives units 16 b + 4 g + r (r < 4) of row i, with
+//     LayerNorm moments reduced over the four lanes that share the row;
 //   layer 2 (MFMA): HP / 16 column blocks x HP / 32 k-steps x 6 part products;
-//     the weight parts sit in LDS as three [n][k] bf16 arrays with a row
-//     stride of 2 HP + 16 bytes (the 16 rows one read touches start 16 bytes
-//     apart in the banks), split once per workgroup;
+//     k-step t takes from lane (i, g) the units 32 t + 4 g + r and
+//     32 t + 16 + 4 g + r (r < 4) that layer 1 left in it, and the weight
+//     parts sit in LDS as three [n][k] bf16 arrays in that unit order, with
+//     a row stride of 2 HP + 16 bytes (the 16 rows one read touches start 16
+//     bytes apart in the banks); all weight parts are split once per
+//     workgroup;
 //   the accumulators hold row 4 (l / 16) + i, column 16 cb + l % 16: LayerNorm
 //     moments, ReLU and the output dot product reduce over the 16 lanes of a
 //     DPP row.
-// HP = 128: 1024-thread workgroups (108 KB of LDS, one per CU, four waves per
-// SIMD); HP = 64: 512 threads (30 KB, two per CU).  Padded units (k >= h1,
+// HP = 128: 1024-thread workgroups (138 KB of LDS, one per CU, four waves per
+// SIMD); HP = 64: 512 threads (44 KB, two per CU).  Padded units (k >= h1,
 // n >= h2) are exact zeros and are left out of the LayerNorm moments.
 #include <hip/hip_runtime.h>
 
@@ -53,14 +56,22 @@ struct Cfg {
 // 64 KB reach of an LDS instruction, then the three bf16 parts of W2
 template <int HP>
 struct Lay {
-  static constexpr int RS = 2 * HP + 16;              // bytes per W2 row (unit n, k contiguous)
-  static constexpr int O_W1 = 0;                      // floats: [NX][HP] W1 transposed
-  static constexpr int O_B1 = O_W1 + HP * NX;         // b1, g1, be1       [HP] each
+  static constexpr int RS = 2 * HP + 16;              // bytes per W2 row (unit n, k in k-step order)
+  static constexpr int RS1 = 64 + 16;                 // bytes per W1 row (unit, 32 padded inputs)
+  static constexpr int O_B1 = 0;                      // floats: b1, g1, be1       [HP] each
   static constexpr int O_B2 = O_B1 + 3 * HP;          // b2, g2, be2, wo   [HP] each
   static constexpr int FLOATS = O_B2 + 4 * HP;
   static constexpr int O_W2 = FLOATS * 4;             // bytes: parts h, m, l, [3][HP][RS]
-  static constexpr int BYTES = O_W2 + 3 * HP * RS;
+  static constexpr int O_W1 = O_W2 + 3 * HP * RS;     // bytes: parts h, m, l, [3][HP][RS1]
+  static constexpr int BYTES = O_W1 + 3 * HP * RS1;
 };
+
+// position, within its row of W2's parts, of unit k: k-step t = k / 32 holds
+// lane group g's units 32 t + 4 g + r and 32 t + 16 + 4 g + r (r < 4) at
+// bytes 2 (32 t + 8 g) .. + 16
+__host__ __device__ constexpr int w2_pos(int k) {
+  return (k & ~31) + ((k & 31) < 16 ? 8 * ((k & 15) >> 2) + (k & 3) : 8 * ((k & 15) >> 2) + 4 + (k & 3));
+}
 
 template <int CTRL>
 __device__ __forceinline__ float dpp_f(float x) {
@@ -89,10 +100,31 @@ __device__ __forceinline__ void split3(float x, __bf16& h, __bf16& m, __bf16& l)
   l = (__bf16)r2;
 }
 
+// the same for eight values, two at a time (one packed conversion per part
+// and pair)
+typedef float f32x2_v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ void split3x8(const float (&v)[8], bf16x8_t& h, bf16x8_t& m, bf16x8_t& l) {
+#pragma unroll
+  for (int p = 0; p < 4; ++p) {
+    const f32x2_v x = {v[2 * p], v[2 * p + 1]};
+    const bf16x2_t xh = __builtin_convertvector(x, bf16x2_t);
+    const f32x2_v r1 = x - __builtin_convertvector(xh, f32x2_v);
+    const bf16x2_t xm = __builtin_convertvector(r1, bf16x2_t);
+    const f32x2_v r2 = r1 - __builtin_convertvector(xm, f32x2_v);
+    const bf16x2_t xl = __builtin_convertvector(r2, bf16x2_t);
+    h[2 * p] = xh[0];
+    h[2 * p + 1] = xh[1];
+    m[2 * p] = xm[0];
+    m[2 * p + 1] = xm[1];
+    l[2 * p] = xl[0];
+    l[2 * p + 1] = xl[1];
+  }
+}
+
 template <int HP>
 __device__ void stage(const EvictArgs& a, float* sm) {
   using Y = Lay<HP>;
-  constexpr int MT = Cfg<HP>::MT, RS = Y::RS, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2;
+  constexpr int MT = Cfg<HP>::MT, RS = Y::RS, RS1 = Y::RS1, O_B1 = Y::O_B1, O_B2 = Y::O_B2;
   const cfloat* P = const_params(a.params);
   const int h1 = a.h1, h2 = a.h2, nin = a.n_in, ln = a.ln;
   const cfloat* W1 = P;
@@ -109,9 +141,19 @@ __device__ void stage(const EvictArgs& a, float* sm) {
     const int n = e / HP, k = e % HP;
     __bf16 wh, wm, wl;
     split3((k < h1 && n < h2) ? W2[n * h1 + k] : 0.0f, wh, wm, wl);
-    *reinterpret_cast<__bf16*>(w2 + n * RS + 2 * k) = wh;
-    *reinterpret_cast<__bf16*>(w2 + (HP + n) * RS + 2 * k) = wm;
-    *reinterpret_cast<__bf16*>(w2 + (2 * HP + n) * RS + 2 * k) = wl;
+    const int q = 2 * w2_pos(k);
+    *reinterpret_cast<__bf16*>(w2 + n * RS + q) = wh;
+    *reinterpret_cast<__bf16*>(w2 + (HP + n) * RS + q) = wm;
+    *reinterpret_cast<__bf16*>(w2 + (2 * HP + n) * RS + q) = wl;
+  }
+  char* w1 = reinterpret_cast<char*>(sm) + Y::O_W1;
+  for (int e = threadIdx.x; e < HP * 32; e += MT) {
+    const int k = e / 32, x = e % 32;
+    __bf16 wh, wm, wl;
+    split3((k < h1 && x < nin) ? W1[k * nin + x] : 0.0f, wh, wm, wl);
+    *reinterpret_cast<__bf16*>(w1 + k * RS1 + 2 * x) = wh;
+    *reinterpret_cast<__bf16*>(w1 + (HP + k) * RS1 + 2 * x) = wm;
+    *reinterpret_cast<__bf16*>(w1 + (2 * HP + k) * RS1 + 2 * x) = wl;
   }
   for (int i = threadIdx.x; i < HP; i += MT) {
     const bool v2 = i < h2, v1 = i < h1;
@@ -122,17 +164,17 @@ __device__ void stage(const EvictArgs& a, float* sm) {
     sm[O_B1 + i] = v1 ? b1[i] : 0.0f;
     sm[O_B1 + HP + i] = v1 ? (ln ? g1[i] : 1.0f) : 0.0f;
     sm[O_B1 + 2 * HP + i] = v1 && ln ? be1[i] : 0.0f;
-#pragma unroll
-    for (int x = 0; x < NX; ++x) sm[O_W1 + x * HP + i] = (v1 && x < nin) ? W1[i * nin + x] : 0.0f;
   }
 }
 
-template <int HP, bool LN>
+// FULL: both hidden widths equal HP (no padded units, no masks)
+template <int HP, bool LN, bool FULL>
 __global__ void __launch_bounds__(Cfg<HP>::MT, Cfg<HP>::MINB)
 score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
   using Y = Lay<HP>;
-  constexpr int MW = Cfg<HP>::MW, RS = Y::RS, O_W1 = Y::O_W1, O_B1 = Y::O_B1, O_B2 = Y::O_B2;
+  constexpr int MW = Cfg<HP>::MW, RS = Y::RS, RS1 = Y::RS1, O_B1 = Y::O_B1, O_B2 = Y::O_B2;
   constexpr int NT = HP / 32;    // MFMA k-steps (32 units each)
+  constexpr int NB = HP / 16;    // 16-unit blocks of layer 1
   constexpr int NC = HP / 16;    // 16-column blocks of layer 2
   extern __shared__ float sm[];
   // a unit that keeps every row reads no key (the whole workgroup leaves)
@@ -193,79 +235,87 @@ score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
         x[4] = 0.0f;
       }
     }
-    // layer 1: units k = 32 t + 8 kg + j, eight consecutive units per k-step,
-    // so every weight read is a 16-byte LDS load at a constant offset (the
-    // weights are re-read per row block: held across blocks they would take
-    // 256 registers).  Padded units (k >= h1) have zero weights, bias, gain
-    // and shift, so they come out exactly 0 here, after the LayerNorm and
-    // after the ReLU: only the variance sum needs a mask.
+    // layer 1 on the matrix cores: per 16-unit block b, D = W1 x X^T with the
+    // inputs padded to 32 (lanes kg > 0 supply zeros), so lane (ri, kg) gets
+    // units 16 b + 4 kg + r of its row ri, accumulated onto their biases.
+    // Padded units (k >= h1) have zero weights, bias, gain and shift, so they
+    // come out exactly 0 here, after the LayerNorm and after the ReLU: only
+    // the variance sum needs a mask (none when FULL).
     typedef __attribute__((address_space(3))) const f32x4_v lfloat4;
-    const lfloat* p1 = (const lfloat*)sm + 8 * kg;   // LDS, this lane's unit offset
-    asm volatile("" : "+v"(p1));
-    auto w8 = [&](int off, float (&o)[8]) {         // floats off .. off + 7 from p1
-      const f32x4_v lo = *reinterpret_cast<lfloat4*>(p1 + off);
-      const f32x4_v hi = *reinterpret_cast<lfloat4*>(p1 + off + 4);
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        o[j] = lo[j];
-        o[4 + j] = hi[j];
+    typedef __attribute__((address_space(3))) const bf16x8_t lbf16x8;
+    bf16x8_t xh, xm, xl;
+    {
+      float v[8] = {x[0], x[1], x[2], x[3], x[4], 0.0f, 0.0f, 0.0f};
+      split3x8(v, xh, xm, xl);
+      if (kg != 0) {
+        const bf16x8_t zero = {};
+        xh = zero;
+        xm = zero;
+        xl = zero;
       }
-    };
-    float h[NT][8];
+    }
+    const lfloat* p1 = (const lfloat*)sm + 4 * kg;   // LDS, this lane's unit offset in a block
+    const lchar* w1 = (const lchar*)sm + Y::O_W1 + ri * RS1 + 16 * kg;
+    asm volatile("" : "+v"(p1), "+v"(w1));
+    f32x4_v hv[NB];
     float s1 = 0.0f;
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      float z[8], w[8];
-      w8(O_B1 + 32 * t, z);
+    for (int b = 0; b < NB; ++b) {
+      const lchar* wb = w1 + 16 * b * RS1;
+      const bf16x8_t wh = *reinterpret_cast<lbf16x8*>(wb);
+      const bf16x8_t wm = *reinterpret_cast<lbf16x8*>(wb + HP * RS1);
+      const bf16x8_t wl = *reinterpret_cast<lbf16x8*>(wb + 2 * HP * RS1);
+      f32x4_v c = *reinterpret_cast<lfloat4*>(p1 + O_B1 + 16 * b);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wl, xh, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wm, xm, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wh, xl, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wm, xh, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wh, xm, c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wh, xh, c, 0, 0, 0);
+      hv[b] = c;
 #pragma unroll
-      for (int i = 0; i < NX; ++i) {
-        w8(O_W1 + i * HP + 32 * t, w);
-#pragma unroll
-        for (int j = 0; j < 8; ++j) z[j] = __builtin_fmaf(w[j], x[i], z[j]);
-      }
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        h[t][j] = z[j];
-        s1 += z[j];
-      }
+      for (int r = 0; r < 4; ++r) s1 += c[r];
     }
     if (LN) {
       const float mean = sum4rows(s1) * ih1;
       float s2 = 0.0f;
 #pragma unroll
-      for (int t = 0; t < NT; ++t)
+      for (int b = 0; b < NB; ++b)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float d = h[t][j] - mean;
-          s2 += (32 * t + 8 * kg + j) < h1 ? d * d : 0.0f;
+        for (int r = 0; r < 4; ++r) {
+          const float d = hv[b][r] - mean;
+          hv[b][r] = d;
+          if (FULL || (16 * b + 4 * kg + r) < h1) s2 = __builtin_fmaf(d, d, s2);
         }
       const float rs = __builtin_amdgcn_rsqf(__builtin_fmaf(sum4rows(s2), ih1, LN_EPS));
 #pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        float g[8], be[8];
-        w8(O_B1 + HP + 32 * t, g);
-        w8(O_B1 + 2 * HP + 32 * t, be);
+      for (int b = 0; b < NB; ++b) {
+        const f32x4_v g = *reinterpret_cast<lfloat4*>(p1 + O_B1 + HP + 16 * b);
+        const f32x4_v be = *reinterpret_cast<lfloat4*>(p1 + O_B1 + 2 * HP + 16 * b);
 #pragma unroll
-        for (int j = 0; j < 8; ++j) h[t][j] = __builtin_fmaf((h[t][j] - mean) * rs, g[j], be[j]);
+        for (int r = 0; r < 4; ++r) hv[b][r] = __builtin_fmaf(hv[b][r] * rs, g[r], be[r]);
       }
     }
-    // layer 2 on the bf16 matrix cores, six part products per k-step and block
+    // layer 2 on the bf16 matrix cores, six part products per k-step and
+    // block, accumulated onto the bias of the lane's column
     f32x4_v acc[NC];
 #pragma unroll
-    for (int cb = 0; cb < NC; ++cb) acc[cb] = (f32x4_v){0.0f, 0.0f, 0.0f, 0.0f};
+    for (int cb = 0; cb < NC; ++cb) {
+      const float bn = sm[O_B2 + 16 * cb + ri];
+      acc[cb] = (f32x4_v){bn, bn, bn, bn};
+    }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       bf16x8_t ah, am, al;
+      float v[8];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float v = fmaxf(h[t][j], 0.0f);   // ReLU
-        __bf16 vh, vm, vl;
-        split3(v, vh, vm, vl);
-        ah[j] = vh;
-        am[j] = vm;
-        al[j] = vl;
+      for (int r = 0; r < 4; ++r) {            // ReLU; units 32 t + 4 kg + r, then + 16
+        v[r] = fmaxf(hv[2 * t][r], 0.0f);
+        v[4 + r] = fmaxf(hv[2 * t + 1][r], 0.0f);
       }
-      // the weight rows of column block cb, this lane's 8 units of k-step t (an
+      split3x8(v, ah, am, al);
+      // the weight rows of column block cb, this lane's 8 units of k-step t, at
+      // bytes 2 (32 t + 8 kg) .. + 16 of each row in that order (an
       // opaque pointer per k-step keeps the reads from being hoisted out of the
       // row loop: all of W2's parts would not fit in registers)
       const lchar* w2 = (const lchar*)sm + Y::O_W2 + ri * RS + (32 * t + 8 * kg) * 2;
@@ -296,18 +346,18 @@ score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
       float t1 = 0.0f;
 #pragma unroll
       for (int cb = 0; cb < NC; ++cb) {
-        const int n = 16 * cb + ri;
-        z[cb] = acc[cb][i] + sm[O_B2 + n];
+        z[cb] = acc[cb][i];
         t1 += z[cb];
       }
-      float mean = 0.0f, rs = 1.0f;
+      float rs = 1.0f;
       if (LN) {
-        mean = sum16(t1) * ih2;
+        const float mean = sum16(t1) * ih2;
         float t2 = 0.0f;
 #pragma unroll
         for (int cb = 0; cb < NC; ++cb) {
           const float d = z[cb] - mean;
-          t2 += (16 * cb + ri) < h2 ? d * d : 0.0f;
+          z[cb] = d;
+          if (FULL || (16 * cb + ri) < h2) t2 = __builtin_fmaf(d, d, t2);
         }
         rs = __builtin_amdgcn_rsqf(__builtin_fmaf(sum16(t2), ih2, LN_EPS));
       }
@@ -315,8 +365,7 @@ score_mlp2_kernel(EvictArgs a, uint64_t* keys, int kstride) {
 #pragma unroll
       for (int cb = 0; cb < NC; ++cb) {
         const int n = 16 * cb + ri;
-        float y = LN ? __builtin_fmaf((z[cb] - mean) * rs, sm[O_B2 + HP + n], sm[O_B2 + 2 * HP + n])
-                     : z[cb];
+        float y = LN ? __builtin_fmaf(z[cb] * rs, sm[O_B2 + HP + n], sm[O_B2 + 2 * HP + n]) : z[cb];
         o = __builtin_fmaf(sm[O_B2 + 3 * HP + n], fmaxf(y, 0.0f), o);   // padded units: wo = 0
       }
       score[i] = sum16(o) + bout;
@@ -350,24 +399,27 @@ int launch_score_mlp2(const EvictArgs& a, uint64_t* keys, int kstride, void* str
   gx = gx < nblk ? gx : nblk;
   gx = gx > 0 ? gx : 1;
   const bool ln = a.ln != 0;
-  const void* k = narrow ? (ln ? (const void*)score_mlp2_kernel<64, true> : (const void*)score_mlp2_kernel<64, false>)
-                         : (ln ? (const void*)score_mlp2_kernel<128, true> : (const void*)score_mlp2_kernel<128, false>);
+  const bool full = narrow ? (a.h1 == 64 && a.h2 == 64) : (a.h1 == 128 && a.h2 == 128);
   const size_t lds = (size_t)(narrow ? Lay<64>::BYTES : Lay<128>::BYTES);
-  hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  for_grid_y(a.units, [&](int y0, int ny) {
-    EvictArgs b = a;
-    b.y0 = y0;
-    const dim3 grid(gx, ny);
-    const hipStream_t st = (hipStream_t)stream;
-    if (narrow && ln)
-      hipLaunchKernelGGL((score_mlp2_kernel<64, true>), grid, dim3(Cfg<64>::MT), lds, st, b, keys, kstride);
-    else if (narrow)
-      hipLaunchKernelGGL((score_mlp2_kernel<64, false>), grid, dim3(Cfg<64>::MT), lds, st, b, keys, kstride);
-    else if (ln)
-      hipLaunchKernelGGL((score_mlp2_kernel<128, true>), grid, dim3(Cfg<128>::MT), lds, st, b, keys, kstride);
-    else
-      hipLaunchKernelGGL((score_mlp2_kernel<128, false>), grid, dim3(Cfg<128>::MT), lds, st, b, keys, kstride);
-  });
+  const int variant = (narrow ? 4 : 0) + (ln ? 2 : 0) + (full ? 1 : 0);
+  auto launch = [&](auto kern, int mt) {
+    hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    for_grid_y(a.units, [&](int y0, int ny) {
+      EvictArgs b = a;
+      b.y0 = y0;
+      hipLaunchKernelGGL(kern, dim3(gx, ny), dim3(mt), lds, (hipStream_t)stream, b, keys, kstride);
+    });
+  };
+  switch (variant) {
+    case 0: launch(score_mlp2_kernel<128, false, false>, Cfg<128>::MT); break;
+    case 1: launch(score_mlp2_kernel<128, false, true>, Cfg<128>::MT); break;
+    case 2: launch(score_mlp2_kernel<128, true, false>, Cfg<128>::MT); break;
+    case 3: launch(score_mlp2_kernel<128, true, true>, Cfg<128>::MT); break;
+    case 4: launch(score_mlp2_kernel<64, false, false>, Cfg<64>::MT); break;
+    case 5: launch(score_mlp2_kernel<64, false, true>, Cfg<64>::MT); break;
+    case 6: launch(score_mlp2_kernel<64, true, false>, Cfg<64>::MT); break;
+    default: launch(score_mlp2_kernel<64, true, true>, Cfg<64>::MT); break;
+  }
   return (int)hipGetLastError();
 }
 
