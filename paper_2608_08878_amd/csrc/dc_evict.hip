@@ -59,7 +59,7 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
       for (int r = tid; r < L; r += ENT) a.kept_out[(size_t)u * L + r] = r;
     return;
   }
-  select_compact<RegKeys<REG_KPT>, DTYPE, D>(a, u, a.L, a.budget, keys, REG_KPT, sh, dyn);
+  select_compact<RegKeys<REG_KPT>, DTYPE, D, ENT, 2, true>(a, u, a.L, a.budget, keys, REG_KPT, sh, dyn);
 }
 
 // Long caches: scores to keys in the workspace (grid over rows) ...
@@ -119,7 +119,7 @@ __global__ void __launch_bounds__(ENT) select_kernel(EvictArgs a, const uint64_t
     return;
   }
   MemKeys mk{keys + (size_t)u * kstride};
-  select_compact<MemKeys, DTYPE, D>(a, u, L, Bu, mk, (L + ENT - 1) / ENT, sh, dyn);
+  select_compact<MemKeys, DTYPE, D, ENT, 2, true>(a, u, L, Bu, mk, (L + ENT - 1) / ENT, sh, dyn);
   if (a.kept_out && a.budgets)          // slots past this unit's budget
     for (int r = Bu + threadIdx.x; r < a.ld_kept; r += ENT) a.kept_out[(size_t)u * a.ld_kept + r] = -1;
 }

@@ -312,8 +312,12 @@ __device__ __forceinline__ void block_scan2(bool f0, bool f1, int& r0, int& r1, 
 // Keep the top B of unit u's L rows (B < L) and compact; kept_out rows have
 // stride a.ld_kept.  Move j of the plan is the pair (hole, mover) at
 // mv[MS j], mv[MS j + 1] (MS = 2: a dense list; a larger stride lets the list
-// share row slots with the keys, move j beside row j's key).
-template <typename Keys, int DTYPE, int D, int NT = ENT, int MS = 2>
+// share row slots with the keys, move j beside row j's key).  BATCHED (the
+// stand-alone selection, many moves per unit): the state fields of 16
+// consecutive moves travel together, lane q of a 16-lane group carrying move
+// q's, so each field's reads and writes coalesce (the movers and the holes
+// both ascend); otherwise lane q of a group carries field q of one move.
+template <typename Keys, int DTYPE, int D, int NT = ENT, int MS = 2, bool BATCHED = false>
 __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Keys& keys, int kpt,
                                SelShared& sh, int* mv) {
   constexpr int ELT = DTYPE == 0 ? 4 : 2;
@@ -492,6 +496,59 @@ __device__ void select_compact(const EvictArgs& a, int u, int L, int B, const Ke
   const int grp = tid / 16, gl = tid % 16, ngrp = NT / 16;
   char* kb = (char*)a.k;
   char* vb = (char*)a.v;
+  if constexpr (BATCHED) {
+    for (int b0 = 16 * grp; b0 < nm; b0 += 16 * ngrp) {
+      // state of moves b0 .. b0 + 15, lane gl carrying move b0 + gl (past the
+      // list: re-read move b0, no store); requested before the rows
+      const bool sok = b0 + gl < nm;
+      const int js = sok ? b0 + gl : b0;
+      const size_t sd = ub + mv[MS * js], ss = ub + mv[MS * js + 1];
+      const float s_al = a.alpha[ss], s_vn = a.vnorm[ss];
+      const double s_nu = a.num[ss], s_de = a.den[ss];
+      const int32_t s_po = a.pos[ss];
+      const float s_sg = a.sigma ? a.sigma[ss] : 0.0f;
+      // rows: all 16 lanes per move, MB moves per trip, every load before the stores
+      const int mend = nm - b0 < 16 ? nm - b0 : 16;
+      for (int m0 = 0; m0 < mend; m0 += MB) {
+        size_t gd[MB], gs[MB];
+        uint4 kx[MB][CPL], vx[MB][CPL];
+#pragma unroll
+        for (int q = 0; q < MB; ++q) {
+          const int j = b0 + (m0 + q < mend ? m0 + q : m0);
+          gd[q] = ub + mv[MS * j];
+          gs[q] = ub + mv[MS * j + 1];
+#pragma unroll
+          for (int cc = 0; cc < CPL; ++cc) {
+            const int c = gl + 16 * cc < N16 ? gl + 16 * cc : N16 - 1;
+            kx[q][cc] = ldg16(kb + gs[q] * D * ELT + c * 16);
+            vx[q][cc] = ldg16(vb + gs[q] * D * ELT + c * 16);
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < MB; ++q) {
+          if (m0 + q >= mend) continue;
+#pragma unroll
+          for (int cc = 0; cc < CPL; ++cc) {
+            const int c = gl + 16 * cc;
+            if (c < N16) {
+              *reinterpret_cast<uint4*>(kb + gd[q] * D * ELT + c * 16) = kx[q][cc];
+              *reinterpret_cast<uint4*>(vb + gd[q] * D * ELT + c * 16) = vx[q][cc];
+            }
+          }
+        }
+      }
+      if (sok) {
+        a.alpha[sd] = s_al;
+        a.vnorm[sd] = s_vn;
+        a.num[sd] = s_nu;
+        a.den[sd] = s_de;
+        a.pos[sd] = s_po;
+        if (a.sigma) a.sigma[sd] = s_sg;
+        if (a.kept_out) a.kept_out[(size_t)u * a.ld_kept + (int)(sd - ub)] = (int)(ss - ub);
+      }
+    }
+    return;
+  }
   for (int j0 = grp; j0 < nm; j0 += MB * ngrp) {
     size_t gd[MB], gs[MB];
     bool ok[MB];
