@@ -484,7 +484,9 @@ def bench_paper_policy(args, wl, dev, log):
             "score_select_ms": round(m["score_select"], 4), "first_step_ms": round(first_ms, 3),
             "policy": "5->128->128->1 ReLU MLP with LayerNorm, features [alpha, |v|, sigma, H, pos]",
             "mlp_tflops": round(U * L * flop_row / (m["score_select"] * 1e-3) / 1e12, 2),
-            "mlp_frac_of_f32_mfma": round(U * L * flop_row / (m["score_select"] * 1e-3) / 157.3e12, 4),
+            # float32-accurate work (the scoring runs on the bf16 matrix cores with
+            # a three-part operand split) against the float32 peak
+            "mlp_frac_of_f32_peak": round(U * L * flop_row / (m["score_select"] * 1e-3) / 157.3e12, 4),
             "note": "paper-faithful state and policy; decode + separate scoring pass, timed apart"}
 
 
