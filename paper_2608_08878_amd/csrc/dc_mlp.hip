@@ -6,11 +6,13 @@
 // instructions run at the float32 vector rate and do not overlap the vector
 // work around them, so the contraction runs on the bf16 matrix cores instead,
 // at float32 accuracy: every float32 operand x is split exactly into three
-// bf16 parts x = xh + xm + xl (8 significand bits each: 24 in all), and the
-// product of an activation h and a weight w keeps the six part products down
-// to 2^-24 relative, hl wh + hm wm + hh wl + hm wh + hh wm + hh wh (each exact
-// in float32, accumulated in float32 by v_mfma_f32_16x16x32_bf16); the three
-// dropped ones are below 2^-31 relative.  The hidden widths are padded to
+// bf16 parts x = xh + xm + xl (8 significand bits each: 24 in all; |xm| and
+// |xl| about 2^-8 and 2^-16 of |x|), and the product of an activation h and a
+// weight w keeps the six part products down to about 2^-16 of it,
+// hl wh + hm wm + hh wl + hm wh + hh wm + hh wh (each exact in float32,
+// accumulated in float32 by v_mfma_f32_16x16x32_bf16); the three dropped ones
+// (hm wl, hl wm, hl wl) come to about 2^-23 of the product, one float32
+// rounding.  The hidden widths are padded to
 // HP = 64 (both at most 64) or 128.  One wave takes 16 rows at a time:
 //   layer 1 (MFMA, the same split, inputs padded to 32): per 16-unit block b,
 //     W1 (16 units x 32 inputs) times the rows' features (32 x 16 rows), so
