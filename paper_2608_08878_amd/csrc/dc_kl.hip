@@ -10,9 +10,10 @@
 // answer to the rounding of the two log-sum-exps), and identical rows give
 // exactly 0.  Q's normaliser never appears.
 //
-// Kernel 1 (one workgroup per 64 vocabulary columns): MFMA 16x16x32 bf16 over
-// the hidden dimension for a 16-row A = [8 full rows; the 8 matching compressed
-// rows], then per (row, tile) the local statistics
+// Kernel 1 (under 16 rows: kl_tile_kernel, one workgroup per 64 vocabulary
+// columns; 16 rows and more: the blocked GEMMs below, same arithmetic): MFMA
+// 16x16x32 bf16 over the hidden dimension for a 16-row A = [8 full rows; the 8
+// matching compressed rows], then per (row, 64-column tile) the local statistics
 //     m_t = max l,  s_t = sum e^{l - m_t},  mu_t = E_{P_t}[delta],
 //     A_t = E_{P_t}[g(mu_t - delta)]
 // where P_t is P restricted to the tile.  Kernel 2 merges the tiles exactly:

@@ -1,10 +1,10 @@
 // Two-hidden-layer policy on matrix cores (Sec. 3.1.2 scoring with the App. D
 // network: n_in -> h1 -> h2 -> 1, optional LayerNorm, widths up to 128), gfx950.
 //
-// Scoring every cached row with a wide second hidden layer is a dense
-// contraction, [rows x h1] x [h1 x h2].  On this part the float32 matrix
+// Scoring every cached row is two dense contractions, [rows x n_in] x
+// [n_in x h1] and [rows x h1] x [h1 x h2].  On this part the float32 matrix
 // instructions run at the float32 vector rate and do not overlap the vector
-// work around them, so the contraction runs on the bf16 matrix cores instead,
+// work around them, so both run on the bf16 matrix cores instead,
 // at float32 accuracy: every float32 operand x is split exactly into three
 // bf16 parts x = xh + xm + xl (8 significand bits each: 24 in all; |xm| and
 // |xl| about 2^-8 and 2^-16 of |x|), and the product of an activation h and a
@@ -12,8 +12,8 @@
 // hl wh + hm wm + hh wl + hm wh + hh wm + hh wh (each exact in float32,
 // accumulated in float32 by v_mfma_f32_16x16x32_bf16); the three dropped ones
 // (hm wl, hl wm, hl wl) come to about 2^-23 of the product, one float32
-// rounding.  The hidden widths are padded to
-// HP = 64 (both at most 64) or 128.  One wave takes 16 rows at a time:
+// rounding.  The hidden widths are padded to HP = 64 (both at most 64) or
+// 128.  One wave takes 16 rows at a time:
 //   layer 1 (MFMA, the same split, inputs padded to 32): per 16-unit block b,
 //     W1 (16 units x 32 inputs) times the rows' features (32 x 16 rows), so
 //     lane (i, g) receives units 16 b + 4 g + r (r < 4) of row i, with
@@ -42,7 +42,7 @@ namespace dc {
 
 namespace {
 
-constexpr int NX = 5;                // padded input width
+constexpr int NX = 5;                // features per row (the fifth is 0 for four-input policies)
 typedef float f32x4_v __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) const char lchar;
 
