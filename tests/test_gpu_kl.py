@@ -60,10 +60,11 @@ def test_kl_reward_full_size(which):
 
 
 # row counts below 16 take the per-step kernel, 16 and more the blocked GEMM
-# (partial row blocks, vocabularies that end inside a 256-column block)
+# (partial row blocks, vocabularies that end inside a 256-column block, a
+# 128k-token vocabulary: 2048 tiles per row in the merge)
 @pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (13, 256, 1024), (15, 128, 4160),
                                           (16, 128, 256), (64, 512, 4096), (100, 256, 4160),
-                                          (523, 128, 640)])
+                                          (523, 128, 640), (4, 128, 131072)])
 def test_kl_reward_shapes(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 7 + hid)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
