@@ -323,6 +323,20 @@ def bench_teacher_student_kl(args, wl, dev, log):
     rows, hid, voc = wl.batch, wl.kl_hidden, wl.kl_vocab
     w = torch.empty((voc, hid), dtype=torch.bfloat16, device=dev)
     sg.fill_normal(w, wl, W.S_WLM, 0, 0.02)
+    sh = stream_handle()
+    # the lm head is laid out once, as a model's weights are at load time, in
+    # the tile layout the per-step reward streams fastest (same results)
+    kl_fn = B.dc_kl_reward
+    pack_ms = None
+    if not args.kl_row_major:
+        wp = torch.empty_like(w)
+        ev = _events(2)
+        ev[0].record()
+        B.dc_kl_pack_lm_head(hid, voc, w, wp, sh)
+        ev[1].record()
+        torch.cuda.synchronize()
+        pack_ms = ev[0].elapsed_time(ev[1])
+        w, kl_fn = wp, B.dc_kl_reward_packed
     hf = torch.empty((nsteps, rows, hid), dtype=torch.bfloat16, device=dev)
     hc = torch.empty_like(hf)
     for t in range(nsteps):
@@ -334,7 +348,6 @@ def bench_teacher_student_kl(args, wl, dev, log):
     kn = torch.empty((U, D), dtype=torch.bfloat16, device=dev)
     vn = torch.empty_like(kn)
     o_t, o_s = torch.empty_like(q), torch.empty_like(q)
-    sh = stream_handle()
     parts = {"teacher": [], "student": [], "kl": [], "step": []}
     first_ms = None
     train = args.train_select
@@ -349,7 +362,7 @@ def bench_teacher_student_kl(args, wl, dev, log):
     one_t = DecodeBuffers(nt, 1, G, 1, D, wl.n0 + 2, wl.dtype, wl.ent_window, features=False)
     one_t.kv.len = wl.n0
     one_t.decode_step(q[:nt], kn[:nt], vn[:nt], features=False)
-    B.dc_kl_reward(rows, hid, voc, hf[0], hc[0], w, kl, ws, ws.numel(), sh)
+    kl_fn(rows, hid, voc, hf[0], hc[0], w, kl, ws, ws.numel(), sh)
     torch.cuda.synchronize()
     del one_t
     for t in range(nsteps):
@@ -366,7 +379,7 @@ def bench_teacher_student_kl(args, wl, dev, log):
         else:
             stu.decode_evict(pol, wl.budget, q, kn, vn, o_s)
         ev[2].record()
-        B.dc_kl_reward(rows, hid, voc, hf[t], hc[t], w, kl, ws, ws.numel(), sh)
+        kl_fn(rows, hid, voc, hf[t], hc[t], w, kl, ws, ws.numel(), sh)
         ev[3].record()
         torch.cuda.synchronize()
         if t == 0:
@@ -379,19 +392,20 @@ def bench_teacher_student_kl(args, wl, dev, log):
             parts["kl"].append(ev[2].elapsed_time(ev[3]))
             parts["step"].append(ev[0].elapsed_time(ev[3]))
     m = {k: float(np.mean(v)) for k, v in parts.items()}
-    extra = {}
+    extra = {"kl_lm_head_layout": "row-major" if args.kl_row_major else "packed 64x64 tiles",
+             "kl_pack_ms": None if pack_ms is None else round(pack_ms, 4)}
     # the same rewards deferred to the end of the rollout: one call over all
     # steps x batch rows reads the lm head once
     Td = nsteps
     wsd = torch.empty(B.dc_workspace_bytes(stu.dims, 0, Td * rows, voc), dtype=torch.uint8, device=dev)
     kld = torch.empty(Td * rows, dtype=torch.float32, device=dev)
     hfv, hcv = hf.view(Td * rows, hid), hc.view(Td * rows, hid)
-    B.dc_kl_reward(Td * rows, hid, voc, hfv, hcv, w, kld, wsd, wsd.numel(), sh)
+    kl_fn(Td * rows, hid, voc, hfv, hcv, w, kld, wsd, wsd.numel(), sh)
     torch.cuda.synchronize()
     ev = _events(2)
     ev[0].record()
     for _ in range(3):
-        B.dc_kl_reward(Td * rows, hid, voc, hfv, hcv, w, kld, wsd, wsd.numel(), sh)
+        kl_fn(Td * rows, hid, voc, hfv, hcv, w, kld, wsd, wsd.numel(), sh)
     ev[1].record()
     torch.cuda.synchronize()
     kd_ms = ev[0].elapsed_time(ev[1]) / 3
@@ -698,6 +712,9 @@ def main():
     ap.add_argument("--train-select", action="store_true",
                     help="workload 5: the student keeps a Gumbel-sampled top-B and computes "
                          "log pi (training mode) instead of the deterministic selection")
+    ap.add_argument("--kl-row-major", action="store_true",
+                    help="workload 5: read the lm head row-major instead of in the packed "
+                         "tile layout")
     ap.add_argument("--cpu-units", type=int, default=128)
     ap.add_argument("--cpu-steps", type=int, default=64)
     ap.add_argument("--calib-copy-mib", type=int, default=1024,

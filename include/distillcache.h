@@ -378,6 +378,33 @@ dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void *
                        const void *h_comp, const void *w_lm, float *kl_out, void *ws,
                        size_t ws_bytes, void *hip_stream);
 
+/* Lays the lm-head weight out for dc_kl_reward_packed (the weight of the
+ * Sec. 3.1.4 reward's output distribution; a once-per-model copy, not a
+ * per-step operation):
+ *   w_lm      [vocab][hidden] bfloat16, as for dc_kl_reward (read only)
+ *   w_packed  vocab * hidden bfloat16 (caller-allocated, the same size as
+ *             w_lm, not overlapping it), written as 64 x 64 blocks: block
+ *             (t, k) holds vocabulary rows 64 t .. 64 t + 63, hidden elements
+ *             64 k .. 64 k + 63, row-major (128 bytes per row), at element
+ *             offset (t * (hidden / 64) + k) * 4096.
+ * The packed weight is read as one contiguous run per vocabulary tile, which
+ * the per-step (few-row) reward streams faster than 64 rows of the row-major
+ * weight; the values and the results are the same.  Asynchronous on
+ * hip_stream.
+ * Supported: hidden % 128 == 0, vocab % 64 == 0.
+ * Errors: DC_ERR_NULL, DC_ERR_SHAPE (hidden or vocab < 1), DC_ERR_UNSUPPORTED
+ * (sizes, or w_packed overlapping w_lm), DC_ERR_HIP. */
+dc_status dc_kl_pack_lm_head(int32_t hidden, int32_t vocab, const void *w_lm, void *w_packed,
+                             void *hip_stream);
+
+/* dc_kl_reward (Sec. 3.1.4) reading the lm head as dc_kl_pack_lm_head laid it
+ * out.  Arguments, workspace (dc_workspace_bytes with kl_rows, kl_vocab),
+ * limits and errors as dc_kl_reward; kl_out is bit-identical to
+ * dc_kl_reward's on the row-major weight the packed one was made from. */
+dc_status dc_kl_reward_packed(int32_t rows, int32_t hidden, int32_t vocab, const void *h_full,
+                              const void *h_comp, const void *w_packed, float *kl_out, void *ws,
+                              size_t ws_bytes, void *hip_stream);
+
 /* Largest rows * (vocab / 64) of one dc_kl_reward_static call. */
 #define DC_KL_STATIC_MAX_PAIRS 524288
 

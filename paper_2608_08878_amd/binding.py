@@ -64,7 +64,8 @@ EXPORTS = ("dc_workspace_bytes", "dc_feat_init", "dc_decode_step", "dc_score_evi
            "dc_decode_evict", "dc_sample_evict", "dc_decode_sample_evict", "dc_score_evict_units",
            "dc_decode_evict_units",
            "dc_subset_log_prob",
-           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_kl_reward_static",
+           "dc_subset_log_prob_workspace_bytes", "dc_kl_reward", "dc_kl_pack_lm_head",
+           "dc_kl_reward_packed", "dc_kl_reward_static",
            "dc_reinforce_terms",
            "dc_dynamic_budget", "dc_global_alpha", "dc_global_alpha_workspace_bytes",
            "dc_status_str")
@@ -120,6 +121,10 @@ def lib() -> ctypes.CDLL:
         L.dc_subset_log_prob_workspace_bytes.restype = sz
         L.dc_kl_reward.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
         L.dc_kl_reward.restype = ctypes.c_int
+        L.dc_kl_pack_lm_head.argtypes = [i32, i32, vp, vp, vp]
+        L.dc_kl_pack_lm_head.restype = ctypes.c_int
+        L.dc_kl_reward_packed.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.dc_kl_reward_packed.restype = ctypes.c_int
         L.dc_kl_reward_static.argtypes = [i32, i32, i32, vp, vp, vp, vp, vp]
         L.dc_kl_reward_static.restype = ctypes.c_int
         L.dc_reinforce_terms.argtypes = [i32, i32, ctypes.POINTER(dc_reinforce_cfg), vp, vp, vp,
@@ -207,6 +212,16 @@ def dc_kl_reward(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_ou
                  ws_bytes: int = 0, stream=None) -> None:
     _check(lib().dc_kl_reward(rows, hidden, vocab, _ptr(h_full), _ptr(h_comp), _ptr(w_lm),
                               _ptr(kl_out), _ptr(ws), ws_bytes, stream))
+
+
+def dc_kl_pack_lm_head(hidden: int, vocab: int, w_lm, w_packed, stream=None) -> None:
+    _check(lib().dc_kl_pack_lm_head(hidden, vocab, _ptr(w_lm), _ptr(w_packed), stream))
+
+
+def dc_kl_reward_packed(rows: int, hidden: int, vocab: int, h_full, h_comp, w_packed, kl_out,
+                        ws=None, ws_bytes: int = 0, stream=None) -> None:
+    _check(lib().dc_kl_reward_packed(rows, hidden, vocab, _ptr(h_full), _ptr(h_comp),
+                                     _ptr(w_packed), _ptr(kl_out), _ptr(ws), ws_bytes, stream))
 
 
 def dc_kl_reward_static(rows: int, hidden: int, vocab: int, h_full, h_comp, w_lm, kl_out,

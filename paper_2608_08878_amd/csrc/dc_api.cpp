@@ -418,7 +418,7 @@ dc_status kl_check(int32_t rows, int32_t hidden, int32_t vocab, const void* h_fu
 // part: rows * (vocab / 64) * 4 floats of per-(row, tile) statistics.
 dc_status kl_launch(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
                     const void* h_comp, const void* w_lm, float* kl_out, float* part,
-                    void* hip_stream) {
+                    void* hip_stream, bool packed = false) {
   dc::KLArgs a;
   a.h_full = h_full;
   a.h_comp = h_comp;
@@ -429,6 +429,9 @@ dc_status kl_launch(int32_t rows, int32_t hidden, int32_t vocab, const void* h_f
   a.hidden = hidden;
   a.vocab = vocab;
   a.ntiles = vocab / dc::kl_tile_cols();
+  // where a vocabulary row and a 64-element stage of it sit in the lm head
+  a.w_row = packed ? 128 : 2 * hidden;
+  a.w_stage = packed ? 128 * dc::kl_tile_cols() : 128;
   return dc::launch_kl(a, hip_stream) == 0 ? DC_OK : DC_ERR_HIP;
 }
 
@@ -740,6 +743,27 @@ dc_status dc_kl_reward(int32_t rows, int32_t hidden, int32_t vocab, const void* 
   if (st != DC_OK) return st;
   if (!ws || ws_bytes < kl_bytes(rows, vocab)) return DC_ERR_WORKSPACE;
   return kl_launch(rows, hidden, vocab, h_full, h_comp, w_lm, kl_out, (float*)ws, hip_stream);
+}
+
+dc_status dc_kl_pack_lm_head(int32_t hidden, int32_t vocab, const void* w_lm, void* w_packed,
+                             void* hip_stream) {
+  if (!w_lm || !w_packed) return DC_ERR_NULL;
+  if (hidden < 1 || vocab < 1) return DC_ERR_SHAPE;
+  if (hidden % 128 || vocab % dc::kl_tile_cols()) return DC_ERR_UNSUPPORTED;
+  const size_t bytes = (size_t)hidden * (size_t)vocab * 2;
+  const uintptr_t s = (uintptr_t)w_lm, d = (uintptr_t)w_packed;
+  if (s < d + bytes && d < s + bytes) return DC_ERR_UNSUPPORTED;    // in place / overlapping
+  return dc::launch_kl_pack(w_lm, w_packed, hidden, vocab, hip_stream) == 0 ? DC_OK : DC_ERR_HIP;
+}
+
+dc_status dc_kl_reward_packed(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,
+                              const void* h_comp, const void* w_packed, float* kl_out, void* ws,
+                              size_t ws_bytes, void* hip_stream) {
+  const dc_status st = kl_check(rows, hidden, vocab, h_full, h_comp, w_packed, kl_out);
+  if (st != DC_OK) return st;
+  if (!ws || ws_bytes < kl_bytes(rows, vocab)) return DC_ERR_WORKSPACE;
+  return kl_launch(rows, hidden, vocab, h_full, h_comp, w_packed, kl_out, (float*)ws, hip_stream,
+                   true);
 }
 
 dc_status dc_kl_reward_static(int32_t rows, int32_t hidden, int32_t vocab, const void* h_full,

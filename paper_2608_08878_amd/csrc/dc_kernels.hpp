@@ -124,6 +124,11 @@ struct KLArgs {
   float* out;
   float* part;          // [rows][ntiles][4]
   int rows, hidden, vocab, ntiles;
+  // lm-head addressing: vocabulary row v, hidden elements 64 k .. 64 k + 63 sit at
+  // byte (v / 64) 128 hidden + (v mod 64) w_row + k w_stage.  Row-major
+  // [vocab][hidden]: w_row = 2 hidden, w_stage = 128; the packed tile layout of
+  // dc_kl_pack_lm_head: w_row = 128, w_stage = 8192.
+  int w_row, w_stage;
 };
 
 // The cross-unit alpha average of one decode step (dc_alpha.hip).
@@ -168,6 +173,7 @@ int evict_max_len();
 size_t evict_ws_bytes(int units, int L);
 size_t evict_ext_ws_bytes(int units, int L);
 int launch_kl(const KLArgs& a, void* stream);
+int launch_kl_pack(const void* w, void* packed, int hidden, int vocab, void* stream);
 // Device address of the allocation-free KL entry point's scratch on the current
 // device (looked up once per device); 0 on success.
 int kl_static_scratch(float** out);

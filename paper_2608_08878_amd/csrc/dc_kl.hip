@@ -47,6 +47,22 @@ __device__ __forceinline__ void load_to_lds16(const void* g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                : : "v"(g), "s"(lds) : "memory", "m0");
 }
+// The same with the non-temporal hint: for data read once per call (the
+// per-step kernel's lm head), which then does not displace cached lines --
+// dirty lines of earlier kernels among them, whose write-back would otherwise
+// share the HBM with the stream.
+__device__ __forceinline__ void load_to_lds16_nt(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off nt"
+               : : "v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Byte offset of vocabulary row v's first hidden element in the lm head: the
+// row-major weight and the packed tile layout differ only in where a 64-row
+// tile's rows and 64-element stages sit (KLArgs::w_row, w_stage).
+static_assert(KL_TILE == 64, "lm-head tiles of 64 vocabulary rows");
+__device__ __forceinline__ size_t w_row_off(const KLArgs& a, int v) {
+  return (size_t)(v >> 6) * 128 * (size_t)a.hidden + (size_t)(v & 63) * (size_t)a.w_row;
+}
 
 // g(y) = e^y - 1 - y without cancellation.
 __device__ __forceinline__ float gfun(float y) {
@@ -106,7 +122,11 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   // c ^ (r mod 8) of its 128 LDS bytes (lane j loads the chunk that lands at
   // byte 16 j), so the operand reads hit eight bank groups per eight lanes.
   // MFMA t of a stage takes chunk 4t + kg of both operands: the blocks feed
-  // the matrix cores in hidden order, as in the GEMM kernels.  Every load is
+  // the matrix cores in hidden order, as in the GEMM kernels.  The lm-head
+  // loads are non-temporal (at most two row blocks read a slab, back to back
+  // on one XCD); the hidden-state rows, which every tile reads, are not.
+  // Where a row's stage sits in the lm head (row-major or packed tiles) is
+  // KLArgs::w_row / w_stage.  Every load is
   // unconditional (past the end a stage re-reads the last one), so each wave
   // issues three loads per stage and a wait counts stages exactly.
   const int lrow = lane >> 3;
@@ -118,16 +138,17 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   const char* wsrc[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j)
-    wsrc[j] = (const char*)a.w + ((size_t)(tile * KL_TILE + 8 * (2 * wave + j) + lrow) * a.hidden +
-                                  8 * ((lane & 7) ^ lrow)) * 2;
+    wsrc[j] = (const char*)a.w + w_row_off(a, tile * KL_TILE + 8 * (2 * wave + j) + lrow) +
+              16 * ((lane & 7) ^ lrow);
   const int S = a.hidden / KL_BK;
   const uint32_t ring_lds = (uint32_t)(size_t)(lds_char_t*)ring;
   auto issue = [&](int st) {
-    const int off = 2 * KL_BK * (st < S ? st : S - 1);
+    const int sc = st < S ? st : S - 1;
     const uint32_t base = ring_lds + (st % KL_NS) * KL_STG;
-    if (lane < 32) load_to_lds16(asrc + off, base + wave * 512);
-    load_to_lds16(wsrc[0] + off, base + 2048 + (2 * wave) * 1024);
-    load_to_lds16(wsrc[1] + off, base + 2048 + (2 * wave + 1) * 1024);
+    const size_t offw = (size_t)a.w_stage * sc;
+    if (lane < 32) load_to_lds16(asrc + 2 * KL_BK * sc, base + wave * 512);
+    load_to_lds16_nt(wsrc[0] + offw, base + 2048 + (2 * wave) * 1024);
+    load_to_lds16_nt(wsrc[1] + offw, base + 2048 + (2 * wave + 1) * 1024);
   };
   f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
   auto mma = [&](const char* X) {
@@ -247,7 +268,7 @@ constexpr int KG_MIN_ROWS = 16;                 // fewer rows: kl_tile_kernel
 template <int TW>
 constexpr int kg_lds() { return (KG_M + 2 * TW) * KG_RS; }
 
-template <int TW, int PF>
+template <int TW, int PF, bool PK>
 __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
   constexpr int NT = 2 * TW;            // vocabulary columns per workgroup
   constexpr int CB = TW / 16;           // 16-column MFMA blocks per wave
@@ -274,13 +295,24 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
     const int v = nt * NT + lr + 32 * j;
     vrow[j] = v < a.vocab ? v : a.vocab - 1;
   }
+  static_assert(NT % 64 == 0, "whole lm-head tiles per workgroup");
+  const int wlane = lr * a.w_row + 16 * lc;       // packed layout: this lane's bytes of a block
   uint4 ra[PF][4], rb[PF][BJ];
   auto gload = [&](int k0, uint4 (&xa)[4], uint4 (&xb)[BJ]) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) xa[j] = ldg16(hsrc + ((size_t)arow[j] * a.hidden + k0 + 8 * lc) * 2);
 #pragma unroll
     for (int j = 0; j < BJ; ++j)
-      xb[j] = ldg16((const char*)a.w + ((size_t)vrow[j] * a.hidden + k0 + 8 * lc) * 2);
+      if constexpr (PK) {
+        // packed: chunk j is row lr + 32 (j mod 2) of tile nt NT / 64 + j / 2 (a tile
+        // past the vocabulary re-reads the last one; its columns are dropped)
+        int t = nt * (NT / 64) + j / 2;
+        t = t < a.ntiles ? t : a.ntiles - 1;
+        xb[j] = ldg16((const char*)a.w + ((size_t)t * (a.hidden / KG_BK) + k0 / KG_BK) * a.w_stage +
+                      (size_t)(32 * (j & 1)) * a.w_row + wlane);
+      } else {
+        xb[j] = ldg16((const char*)a.w + ((size_t)vrow[j] * a.hidden + k0 + 8 * lc) * 2);
+      }
   };
   auto sstore = [&](const uint4 (&xa)[4], const uint4 (&xb)[BJ]) {
 #pragma unroll
@@ -384,12 +416,13 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
   epilogue(acc[3], 3);
 }
 
-template <int TW, int PF>
+template <int TW, int PF, bool PK>
 static void launch_kl_gemm(const KLArgs& a, hipStream_t s) {
   const int nM = (a.rows + 63) / 64, nN = (a.vocab + 2 * TW - 1) / (2 * TW);
-  hipFuncSetAttribute((const void*)kl_gemm_kernel<TW, PF>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                      kg_lds<TW>());
-  hipLaunchKernelGGL((kl_gemm_kernel<TW, PF>), dim3(8 * nM * ((nN + 7) / 8)), dim3(256), kg_lds<TW>(), s, a);
+  hipFuncSetAttribute((const void*)kl_gemm_kernel<TW, PF, PK>,
+                      hipFuncAttributeMaxDynamicSharedMemorySize, kg_lds<TW>());
+  hipLaunchKernelGGL((kl_gemm_kernel<TW, PF, PK>), dim3(8 * nM * ((nN + 7) / 8)), dim3(256),
+                     kg_lds<TW>(), s, a);
 }
 
 // Many rows, the larger shape: a 256 x 256 block of logits per workgroup (128
@@ -447,7 +480,7 @@ __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
     hsrc[q] = (const char*)((R & 15) < 8 ? a.h_full : a.h_comp) + ((size_t)r * a.hidden + 8 * lchunk) * 2;
     int v = nt * KM_N + R;
     v = v < a.vocab ? v : a.vocab - 1;
-    wsrc[q] = (const char*)a.w + ((size_t)v * a.hidden + 8 * lchunk) * 2;
+    wsrc[q] = (const char*)a.w + w_row_off(a, v) + 16 * lchunk;
   }
   const int NW = a.hidden / KM_BK;
   const uint32_t ring_lds = (uint32_t)(size_t)(lds_char_t*)ring;
@@ -458,7 +491,7 @@ __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
     const uint32_t dst = ring_lds + (t % KM_SLOTS) * KM_STG + KM_LPW * wave * 1024;
     if (t & 1) {
 #pragma unroll
-      for (int q = 0; q < KM_LPW; ++q) load_to_lds16(wsrc[q] + 2 * KM_BK * w, dst + q * 1024);
+      for (int q = 0; q < KM_LPW; ++q) load_to_lds16(wsrc[q] + (size_t)a.w_stage * w, dst + q * 1024);
     } else {
 #pragma unroll
       for (int q = 0; q < KM_LPW; ++q) load_to_lds16(hsrc[q] + 2 * KM_BK * w, dst + q * 1024);
@@ -635,6 +668,33 @@ __global__ void __launch_bounds__(256) kl_merge_kernel(KLArgs a) {
   if (t == 0) a.out[row] = log1pf(red[0]);
 }
 
+// The packed lm-head layout: the 64 x 64 block of tile t (vocabulary rows
+// 64 t .. 64 t + 63) and stage k (hidden elements 64 k .. 64 k + 63) is one
+// contiguous 8 KB run, its 64 rows of 128 bytes in order; a tile's blocks
+// follow each other in k, and the tiles in t.  A workgroup of kl_tile_kernel
+// then reads one contiguous slab (512 KB at hidden 4096) instead of 64 rows
+// 2 hidden bytes apart.  One thread per 16-byte chunk of the output (stores
+// coalesced; each load instruction reads whole 128-byte row pieces).
+__global__ void __launch_bounds__(256) kl_pack_kernel(const uint4* __restrict__ w,
+                                                      uint4* __restrict__ out, int hidden,
+                                                      size_t n16) {
+  const size_t S = (size_t)hidden / KL_BK, cpr = (size_t)hidden / 8;
+  for (size_t d = (size_t)blockIdx.x * 256 + threadIdx.x; d < n16; d += (size_t)gridDim.x * 256) {
+    const size_t c = d & 7, r = (d >> 3) & 63, blk = d >> 9;
+    const size_t t = blk / S, k = blk - t * S;
+    out[d] = w[(t * KL_TILE + r) * cpr + 8 * k + c];
+  }
+}
+
+int launch_kl_pack(const void* w, void* packed, int hidden, int vocab, void* stream) {
+  const size_t n16 = (size_t)vocab * (size_t)hidden / 8;
+  const size_t want = (n16 + 255) / 256;
+  const unsigned blocks = (unsigned)(want < 16384 ? want : 16384);
+  hipLaunchKernelGGL(kl_pack_kernel, dim3(blocks), dim3(256), 0, (hipStream_t)stream,
+                     (const uint4*)w, (uint4*)packed, hidden, n16);
+  return (int)hipGetLastError();
+}
+
 int kl_tile_cols() { return KL_TILE; }
 
 int launch_kl(const KLArgs& a, void* stream) {
@@ -642,7 +702,10 @@ int launch_kl(const KLArgs& a, void* stream) {
   if (a.rows >= KM_MIN_ROWS) {
     launch_kl_mm(a, s);
   } else if (a.rows >= KG_MIN_ROWS) {
-    launch_kl_gemm<64, 2>(a, s);
+    // (the packed layout's stages are 64 rows apart; the row-major weight keeps
+    // the plain row addressing, which needs two registers fewer)
+    if (a.w_stage != 128) launch_kl_gemm<64, 2, true>(a, s);
+    else launch_kl_gemm<64, 2, false>(a, s);
   } else {
     const int nrb = (a.rows + 7) / 8;
     const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;

@@ -139,6 +139,26 @@ def test_kl_reward_rejects_bad_arguments():
     assert L.dc_kl_reward(8, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == 6
 
 
+def test_kl_pack_and_packed_reward_reject_bad_arguments():
+    L = B.lib()
+    n = 4096 * 32768 * 2
+    assert L.dc_kl_pack_lm_head(4096, 32768, None, FAKE, None) == 1
+    assert L.dc_kl_pack_lm_head(4096, 32768, FAKE, None, None) == 1
+    assert L.dc_kl_pack_lm_head(0, 32768, FAKE, FAKE + 2 * n, None) == 2
+    assert L.dc_kl_pack_lm_head(4000, 32768, FAKE, FAKE + 2 * n, None) == 3
+    assert L.dc_kl_pack_lm_head(4096, 32700, FAKE, FAKE + 2 * n, None) == 3
+    # in place, or overlapping by one element either way
+    assert L.dc_kl_pack_lm_head(4096, 32768, FAKE, FAKE, None) == 3
+    assert L.dc_kl_pack_lm_head(4096, 32768, FAKE, FAKE + n - 2, None) == 3
+    assert L.dc_kl_pack_lm_head(4096, 32768, FAKE + n - 2, FAKE, None) == 3
+    assert L.dc_kl_reward_packed(8, 4096, 32768, None, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 1
+    assert L.dc_kl_reward_packed(0, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 2
+    assert L.dc_kl_reward_packed(8, 4000, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None) == 3
+    assert L.dc_kl_reward_packed(B.KL_MAX_ROWS + 1, 4096, 64, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 40,
+                                 None) == 3
+    assert L.dc_kl_reward_packed(8, 4096, 32768, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None) == 6
+
+
 def test_kl_reward_static_rejects_bad_arguments_before_any_device_work():
     L = B.lib()
     assert L.dc_kl_reward_static(8, 4096, 32768, None, FAKE, FAKE, FAKE, None) == 1
