@@ -897,6 +897,7 @@ def main():
         "kv_bytes_per_step": kvb,
         "moved_rows_per_step": moved,
         "step_kernel_ms": round(step_ms, 4),
+        "hip_graph": False,       # one launch per steady step, issued directly
         "first_step_ms": round(first_ms, 3),
         "prewindow_step_ms": round(pre_ms, 4),
         "workload_window_full_step_ms": round(full_ms, 4),

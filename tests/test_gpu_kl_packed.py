@@ -102,3 +102,20 @@ def test_packed_reward_full_size(rows):
     idx = [0, 3, rows - 1] if rows == 8 else [0, 3, 127, 128, 255, 256, 299]
     ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], w.float().cpu().numpy())
     assert np.all(np.abs(packed[idx] - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed[idx], ref)
+
+
+def test_packed_reward_at_the_maximum_row_count():
+    """DC_KL_MAX_ROWS rows (the blocked GEMM's largest grid) through the packed
+    layout: bit-identical to the row-major call, sampled rows against the oracle."""
+    rows, hid, voc = B.KL_MAX_ROWS, 256, 1024
+    g = torch.Generator(device="cpu").manual_seed(16385)
+    hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
+    hc = (hf.float() + 0.2 * torch.randn(rows, hid, generator=g)).to(torch.bfloat16)
+    w = (0.1 * torch.randn(voc, hid, generator=g)).to(torch.bfloat16).cuda()
+    hfd, hcd = hf.cuda(), hc.cuda()
+    plain = _kl(B.dc_kl_reward, rows, hid, voc, hfd, hcd, w)
+    packed = _kl(B.dc_kl_reward_packed, rows, hid, voc, hfd, hcd, _pack(w))
+    assert np.array_equal(plain.view(np.uint32), packed.view(np.uint32))
+    idx = [0, 127, 128, 9999, rows - 1]
+    ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], w.float().cpu().numpy())
+    assert np.all(np.abs(packed[idx] - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed[idx], ref)
