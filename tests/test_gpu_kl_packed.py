@@ -67,8 +67,8 @@ def test_pack_layout_matches_its_definition(voc, hid):
 # every kernel the reward dispatches to (per-step under 16 rows, the two GEMM
 # shapes from 16 and from 256 rows), vocabularies ending inside a GEMM block
 @pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (8, 256, 1024), (15, 128, 4160),
-                                          (16, 128, 256), (100, 256, 4160), (256, 128, 4160),
-                                          (523, 128, 640)])
+                                          (16, 128, 256), (100, 256, 4160), (255, 128, 640),
+                                          (256, 128, 4160), (523, 128, 640)])
 def test_packed_reward_is_bit_identical_and_matches_the_oracle(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 11 + voc)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
@@ -82,11 +82,12 @@ def test_packed_reward_is_bit_identical_and_matches_the_oracle(rows, hid, voc):
     assert np.all(np.abs(packed - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed, ref)
 
 
-@pytest.mark.parametrize("rows", [8, 300])
+@pytest.mark.parametrize("rows", [8, 100, 300])
 def test_packed_reward_full_size(rows):
-    """hidden 4096, vocab 32768: the per-step call (8 rows) and a deferred one
-    (300 rows, both GEMM shapes' row blocks) bit-identical to the row-major
-    weight; sampled rows against the oracle; an unpruned row exactly 0."""
+    """hidden 4096, vocab 32768: the per-step call (8 rows), the blocked GEMM
+    (100 rows) and the large-tile GEMM (300 rows, a partial last row block),
+    bit-identical to the row-major weight; sampled rows against the oracle;
+    an unpruned row exactly 0."""
     wl = W.WORKLOADS[5]
     hid, voc = wl.kl_hidden, wl.kl_vocab
     w = _full_size_head()
@@ -99,7 +100,7 @@ def test_packed_reward_full_size(rows):
     packed = _kl(B.dc_kl_reward_packed, rows, hid, voc, hfd, hcd, _pack(w))
     assert np.array_equal(plain.view(np.uint32), packed.view(np.uint32))
     assert packed[3] == 0.0
-    idx = [0, 3, rows - 1] if rows == 8 else [0, 3, 127, 128, 255, 256, 299]
+    idx = {8: [0, 3, 7], 100: [0, 3, 63, 64, 99], 300: [0, 3, 127, 128, 255, 256, 299]}[rows]
     ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], w.float().cpu().numpy())
     assert np.all(np.abs(packed[idx] - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed[idx], ref)
 
