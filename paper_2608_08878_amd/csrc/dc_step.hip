@@ -754,8 +754,10 @@ __device__ __forceinline__ void chunk_max(const DecodeArgs& a, int u, int D, flo
 // Passes A, P and B of one chunk in one workgroup: K streamed once (logits and
 // retired pairs to the workspace), p = exp(s - m_c) against the chunk maximum,
 // then V streamed once.  The chunk's logits come back from the workspace
-// while still in L2 (this workgroup stored them moments before).
-template <int D, int G, bool FEAT>
+// while still in L2 (this workgroup stored them moments before).  RET: the
+// step retires a step leaving the window; without one no retired pair is
+// stored (the feature pass reads them only when the step retires).
+template <int D, int G, bool FEAT, bool RET>
 __global__ void __launch_bounds__(SNT) stepc_ab_kernel(DecodeArgs a) {
   constexpr int LPR = MG<D>::LPR;
   __shared__ float pbuf[SCHUNK * G];
@@ -772,16 +774,17 @@ __global__ void __launch_bounds__(SNT) stepc_ab_kernel(DecodeArgs a) {
     for (int t = tid; t < 3 * G + G * D; t += SNT) part[t] = t < G ? NEG_BIG : 0.0f;
     return;
   }
-  const bool retire = FEAT && a.retire;
+  constexpr bool FR = FEAT && RET;
+  const bool retire = FR && a.retire;
   uint4 qa[MG<D>::NT];
   load_qfrag<D, G>(qa, a, u, retire);
   RetStats<G> rs;
   if (retire) load_ret<G>(rs, a, u);
   float mrun[4];
   float zr[S_GMAX], nr[S_GMAX];   // unused on this path
-  pass_a<D, G, FEAT, false>(a, u, r0, r1, a.ws_s + (size_t)u * a.lmax * G,
-                            FEAT ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr, 0, qa, retire, rs,
-                            mrun, zr, nr);
+  pass_a<D, G, FR, false>(a, u, r0, r1, a.ws_s + (size_t)u * a.lmax * G,
+                          FR ? a.ws_r + (size_t)u * a.lmax * 2 : nullptr, 0, qa, retire, rs,
+                          mrun, zr, nr);
   float M[G];
   block_max<G>(mrun, stat, M);    // (its barriers also order the logit stores before the reads)
   const float* src = a.ws_s + ((size_t)u * a.lmax + r0) * G;
@@ -967,8 +970,12 @@ static int launch_step_t(const DecodeArgs& a, const EvictArgs* e, bool feat, boo
     for_grid_y(a.units, [&](int y0, int ny) {
       DecodeArgs b = a;
       b.y0 = y0;
-      if (feat) hipLaunchKernelGGL((stepc_ab_kernel<D, G, true>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
-      else hipLaunchKernelGGL((stepc_ab_kernel<D, G, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      if (feat && a.retire)
+        hipLaunchKernelGGL((stepc_ab_kernel<D, G, true, true>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      else if (feat)
+        hipLaunchKernelGGL((stepc_ab_kernel<D, G, true, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
+      else
+        hipLaunchKernelGGL((stepc_ab_kernel<D, G, false, false>), dim3(a.nchunks, ny), dim3(SNT), 0, s, b);
     });
     for_grid_y(a.units, [&](int y0, int ny) {
       DecodeArgs b = a;
