@@ -37,6 +37,12 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Units below which one workgroup per unit leaves most of the chip idle.
 constexpr int FEW_UNITS = 128;
+// bf16 caches of more than one chunk of rows on this many units or fewer take
+// the chunked decode as well: measured for 1-32 units, 37.6-40.1 us against
+// 41.9-43.7 us per step at 2049 rows and 40.9-44.9 us against 58.4-60.8 us at
+// 3073 rows (decode, scoring, selection and compaction), while 1025 rows still
+// favour the single launch (27-28 us against 33-36 us).
+constexpr int VERY_FEW_UNITS = 32;
 constexpr int MIN_CHUNK = 512;   // rows per workgroup on the chunked path, at least
 
 // Rows per workgroup on the chunked path.  Many units (or fp32): full chunks.
@@ -226,7 +232,8 @@ dc_status prep_decode(const dc_dims* dims, const dc_kv* kv, const dc_feat* feat,
   if (ragged && dims->dtype != DC_BF16) return DC_ERR_UNSUPPORTED;
   if (dims->dtype == DC_BF16)
     split = ragged || !dc::step_fits(L, G, D, feat != nullptr, 0) ||
-            (U < FEW_UNITS && L > 2 * dc::step_chunk_rows());
+            (U < FEW_UNITS && L > 2 * dc::step_chunk_rows()) ||
+            (U <= VERY_FEW_UNITS && L > dc::step_chunk_rows());
   else
     split = use_split(dims, L, feat != nullptr);
   // the matrix-core unit path parks each row's retired (cz, cn) in the workspace
