@@ -38,11 +38,12 @@ size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // Units below which one workgroup per unit leaves most of the chip idle.
 constexpr int FEW_UNITS = 128;
 // bf16 caches of more than one chunk of rows on this many units or fewer take
-// the chunked decode as well: measured for 1-32 units, 37.6-40.1 us against
-// 41.9-43.7 us per step at 2049 rows and 40.9-44.9 us against 58.4-60.8 us at
-// 3073 rows (decode, scoring, selection and compaction), while 1025 rows still
-// favour the single launch (27-28 us against 33-36 us).
-constexpr int VERY_FEW_UNITS = 32;
+// the chunked decode as well.  Measured per step (decode, scoring, selection
+// and compaction), single launch -> chunked: 8 units 43.5 -> 39.0 us at 2049
+// rows and 59.6 -> 42.3 us at 3073 rows, 48 units 45.9 -> 42.1 and
+// 61.5 -> 55.6 us; at 64 units 2049 rows favour the single launch (45.7
+// against 51.9 us), and 1025 rows always do (28 us against 33-36 us).
+constexpr int VERY_FEW_UNITS = 48;
 constexpr int MIN_CHUNK = 512;   // rows per workgroup on the chunked path, at least
 
 // Rows per workgroup on the chunked path.  Many units (or fp32): full chunks.
