@@ -10,8 +10,8 @@
 // answer to the rounding of the two log-sum-exps), and identical rows give
 // exactly 0.  Q's normaliser never appears.
 //
-// Kernel 1 (under 16 rows: kl_tile_kernel, one workgroup per 64 vocabulary
-// columns; 16 rows and more: the blocked GEMMs below, same arithmetic): MFMA
+// Kernel 1 (up to 24 rows: kl_tile_kernel, one workgroup per 64 vocabulary
+// columns and 8 rows; more rows: the blocked GEMMs below, same arithmetic): MFMA
 // 16x16x32 bf16 over the hidden dimension for a 16-row A = [8 full rows; the 8
 // matching compressed rows], then per (row, 64-column tile) the local statistics
 //     m_t = max l,  s_t = sum e^{l - m_t},  mu_t = E_{P_t}[delta],
@@ -258,12 +258,16 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
 // whichever kernel and row count served it.  Workgroup g runs on
 // XCD g mod 8; the row blocks of one vocabulary block are consecutive on one
 // XCD, so its lm-head slab comes from HBM once and then from that XCD's L2.
-// Used from 16 to 255 rows with TW = 64 and two stages in flight; from 256
+// Used from 25 to 128 rows with TW = 64 and two stages in flight; from 129
 // rows on kl_mm_kernel below serves the call.
 constexpr int KG_M = 128;                       // logit rows per workgroup (64 kl rows)
 constexpr int KG_BK = 64;                       // hidden elements per stage
 constexpr int KG_RS = KG_BK * 2 + 16;           // LDS row stride (bytes)
-constexpr int KG_MIN_ROWS = 16;                 // fewer rows: kl_tile_kernel
+// Fewer rows take kl_tile_kernel, whose 8-row blocks each stream the lm head:
+// measured per call (hidden 4096, vocab 32768, packed lm head), three blocks
+// (17-24 rows) 92-94 us against 112 us here, four (25-32 rows) 117-123 us
+// against 113 us.
+constexpr int KG_MIN_ROWS = 25;
 
 template <int TW>
 constexpr int kg_lds() { return (KG_M + 2 * TW) * KG_RS; }
@@ -455,7 +459,9 @@ constexpr int KM_STG = 256 * KM_BK * 2;         // LDS bytes of one stage (one o
 constexpr int KM_SLOTS = 5;                     // stage buffers
 constexpr int KM_WAVES = 8;
 constexpr int KM_LPW = 256 / 8 / KM_WAVES;      // 8-row load instructions per wave and stage
-constexpr int KM_MIN_ROWS = 256;                // from here on this kernel
+// From here on this kernel: its 128-row blocks against the blocked GEMM's 64,
+// measured 144 rows 142 us against 159 us, 128 rows 141 us against 133 us.
+constexpr int KM_MIN_ROWS = 129;
 
 __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
   __shared__ __attribute__((aligned(1024))) char ring[KM_SLOTS * KM_STG];

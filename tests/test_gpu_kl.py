@@ -59,12 +59,14 @@ def test_kl_reward_full_size(which):
     assert np.all(got >= 0)
 
 
-# row counts below 16 take the per-step kernel, 16 and more the blocked GEMM
-# (partial row blocks, vocabularies that end inside a 256-column block, a
-# 128k-token vocabulary: 2048 tiles per row in the merge)
+# up to 24 rows take the per-step kernel (8-row blocks), 25-128 the blocked
+# GEMM, more the large-tile GEMM (partial row blocks, vocabularies that end
+# inside a 256-column block, a 128k-token vocabulary: 2048 tiles per row in
+# the merge)
 @pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (13, 256, 1024), (15, 128, 4160),
-                                          (16, 128, 256), (64, 512, 4096), (100, 256, 4160),
-                                          (523, 128, 640), (4, 128, 131072)])
+                                          (16, 128, 256), (24, 256, 4160), (25, 128, 640),
+                                          (64, 512, 4096), (100, 256, 4160), (128, 128, 640),
+                                          (129, 256, 4160), (523, 128, 640), (4, 128, 131072)])
 def test_kl_reward_shapes(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 7 + hid)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
@@ -97,8 +99,8 @@ def test_kl_reward_deferred_rollout_full_size():
 
 
 def test_kl_reward_does_not_depend_on_the_rows_per_call():
-    """The per-step kernel (under 16 rows) and both GEMM shapes (16..255 rows,
-    256 and more) give every row the same bits."""
+    """The per-step kernel (up to 24 rows) and both GEMM shapes (25..128 rows,
+    129 and more) give every row the same bits."""
     wl = W.WORKLOADS[5]
     hid, voc = wl.kl_hidden, wl.kl_vocab
     w = torch.empty((voc, hid), dtype=torch.bfloat16, device="cuda")

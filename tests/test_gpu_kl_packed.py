@@ -64,11 +64,12 @@ def test_pack_layout_matches_its_definition(voc, hid):
                                                 .manual_seed(voc + hid)).to(torch.bfloat16))
 
 
-# every kernel the reward dispatches to (per-step under 16 rows, the two GEMM
-# shapes from 16 and from 256 rows), vocabularies ending inside a GEMM block
+# every kernel the reward dispatches to (per-step up to 24 rows, the two GEMM
+# shapes from 25 and from 129 rows) on both sides of each boundary,
+# vocabularies ending inside a GEMM block
 @pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (8, 256, 1024), (15, 128, 4160),
-                                          (16, 128, 256), (100, 256, 4160), (255, 128, 640),
-                                          (256, 128, 4160), (523, 128, 640)])
+                                          (24, 128, 256), (25, 128, 4160), (100, 256, 4160),
+                                          (128, 128, 640), (129, 128, 4160), (523, 128, 640)])
 def test_packed_reward_is_bit_identical_and_matches_the_oracle(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 11 + voc)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
