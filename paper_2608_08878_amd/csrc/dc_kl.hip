@@ -10,8 +10,9 @@
 // answer to the rounding of the two log-sum-exps), and identical rows give
 // exactly 0.  Q's normaliser never appears.
 //
-// Kernel 1 (up to 24 rows: kl_tile_kernel, one workgroup per 64 vocabulary
-// columns and 8 rows; more rows: the blocked GEMMs below, same arithmetic): MFMA
+// Kernel 1 (up to 64 rows: kl_tile_kernel, one workgroup per 64 vocabulary
+// columns and 8, 16 or 32 rows; more rows: the blocked GEMMs below, same
+// arithmetic): MFMA
 // 16x16x32 bf16 over the hidden dimension for a 16-row A = [8 full rows; the 8
 // matching compressed rows], then per (row, 64-column tile) the local statistics
 //     m_t = max l,  s_t = sum e^{l - m_t},  mu_t = E_{P_t}[delta],
@@ -32,7 +33,6 @@ namespace dc {
 constexpr int KL_WAVES = 4;
 constexpr int KL_TILE = 16 * KL_WAVES;   // vocabulary columns per workgroup
 constexpr int KL_BK = 64;                // hidden elements per stage (128 bytes of a row)
-constexpr int KL_STG = (16 + KL_TILE) * KL_BK * 2;   // one stage: 16 hidden-state rows, then the lm-head rows
 constexpr int KL_NS = 5;                 // stage buffers (50 KB: two workgroups per CU)
 
 typedef __attribute__((address_space(3))) char lds_char_t;
@@ -96,45 +96,62 @@ __device__ __forceinline__ float max16(float x) {
   return x;
 }
 
-// grid: 8 ceil(tiles / 8) ceil(rows / 8) workgroups of 256 threads (4 waves).
-// Workgroups are dealt to the 8 XCDs round-robin by index, so index g runs on
-// XCD g mod 8; every 8-row block of one 64-column vocabulary tile is given to
-// the same XCD back to back, and the tile's lm-head slab (64 x hidden bf16) is
-// fetched from HBM once and then served from that XCD's L2 to the other row
-// blocks (many rows: the deferred reward of a whole rollout in one call).
+// A workgroup serves RB blocks of 8 kl rows (1, 2 or 4): each block is its
+// own 16-row A operand (8 full, then the 8 compressed hidden states), and
+// every lm-head stage in LDS feeds the matrix cores for all of them, so a
+// call of up to 8 RB rows streams the lm head once.  The stage ring is five
+// deep, four for RB = 4 (two workgroups per CU either way).
+template <int RB>
+struct KLT {
+  static constexpr int NS = RB == 4 ? 4 : KL_NS;                 // stage buffers
+  static constexpr int AB = 16 * RB * KL_BK * 2;                 // A bytes of a stage
+  static constexpr int STG = AB + KL_TILE * KL_BK * 2;           // bytes of a stage
+};
+
+// grid: 8 ceil(tiles / 8) ceil(rows / (8 RB)) workgroups of 256 threads (4
+// waves).  Workgroups are dealt to the 8 XCDs round-robin by index, so index
+// g runs on XCD g mod 8; every row group of one 64-column vocabulary tile is
+// given to the same XCD back to back.
+template <int RB>
 __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
+  constexpr int NS = KLT<RB>::NS, AB = KLT<RB>::AB, STG = KLT<RB>::STG;
   __shared__ float red[KL_WAVES][8][4];
-  __shared__ __attribute__((aligned(1024))) char ring[KL_NS * KL_STG];
+  __shared__ __attribute__((aligned(1024))) char ring[NS * STG];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int nrb = (a.rows + 7) / 8;
+  const int nrb = (a.rows + 8 * RB - 1) / (8 * RB);
   const int slot = blockIdx.x >> 3;
   const int tile = (blockIdx.x & 7) + 8 * (slot / nrb), rb = slot % nrb;
   if (tile >= a.ntiles) return;      // whole workgroup: no barrier is skipped
   const int i = lane & 15, kg = lane >> 4;        // MFMA row/col index, k group
   // The hidden dimension goes in stages of 64 elements, every row read as one
-  // 128-byte line: a stage holds the 16 A rows (rows 0..7 the full, 8..15 the
-  // compressed hidden states of kl rows rb*8 + 0..7) and the workgroup's 64
-  // lm-head rows, loaded straight into LDS (global_load_lds_dwordx4) through a
-  // ring of KL_NS stage buffers, KL_NS - 2 stages in flight while one feeds
-  // the matrix cores.  A load instruction covers 8 rows x 128 bytes (the A
-  // rows: 4 rows, half a wave); row r's 16-byte chunk c sits at position
-  // c ^ (r mod 8) of its 128 LDS bytes (lane j loads the chunk that lands at
-  // byte 16 j), so the operand reads hit eight bank groups per eight lanes.
-  // MFMA t of a stage takes chunk 4t + kg of both operands: the blocks feed
-  // the matrix cores in hidden order, as in the GEMM kernels.  The lm-head
-  // loads are non-temporal (at most two row blocks read a slab, back to back
-  // on one XCD); the hidden-state rows, which every tile reads, are not.
-  // Where a row's stage sits in the lm head (row-major or packed tiles) is
-  // KLArgs::w_row / w_stage.  Every load is
-  // unconditional (past the end a stage re-reads the last one), so each wave
-  // issues three loads per stage and a wait counts stages exactly.
+  // 128-byte line: a stage holds the 16 RB A rows (block b: rows 16 b .. 16 b
+  // + 7 the full, 16 b + 8 .. 16 b + 15 the compressed hidden states of kl
+  // rows (rb RB + b) 8 + 0..7) and the workgroup's 64 lm-head rows, loaded
+  // straight into LDS (global_load_lds_dwordx4) through a ring of NS stage
+  // buffers, NS - 2 stages in flight while one feeds the matrix cores.  A
+  // load instruction covers 8 rows x 128 bytes (the A rows: 4 rows, half a
+  // wave); row r's 16-byte chunk c sits at position c ^ (r mod 8) of its 128
+  // LDS bytes (lane j loads the chunk that lands at byte 16 j), so the
+  // operand reads hit eight bank groups per eight lanes.  MFMA t of a stage
+  // takes chunk 4t + kg of both operands: the blocks feed the matrix cores in
+  // hidden order, as in the GEMM kernels.  The lm-head loads are non-temporal
+  // (each slab is read by a tile's row groups back to back on one XCD); the
+  // hidden-state rows, which every tile reads, are not.  Where a row's stage
+  // sits in the lm head (row-major or packed tiles) is KLArgs::w_row /
+  // w_stage.  Every load is unconditional (past the end a stage re-reads the
+  // last one), so each wave issues RB + 2 loads per stage and a wait counts
+  // stages exactly.
   const int lrow = lane >> 3;
-  const int ar = 4 * wave + lrow;                  // A row of this lane's load (lanes 0..31)
-  int kr = rb * 8 + (ar & 7);
-  kr = kr < a.rows ? kr : a.rows - 1;              // past the end: re-read, unused
-  const char* asrc = (const char*)(ar < 8 ? a.h_full : a.h_comp) +
-                     ((size_t)kr * a.hidden + 8 * ((lane & 7) ^ (ar & 7))) * 2;
+  const char* asrc[RB];
+#pragma unroll
+  for (int q = 0; q < RB; ++q) {
+    const int ar = 4 * (wave + 4 * q) + lrow;      // A row of this lane's load q (lanes 0..31)
+    int kr = (rb * RB + (ar >> 4)) * 8 + (ar & 7);
+    kr = kr < a.rows ? kr : a.rows - 1;            // past the end: re-read, unused
+    asrc[q] = (const char*)((ar & 15) < 8 ? a.h_full : a.h_comp) +
+              ((size_t)kr * a.hidden + 8 * ((lane & 7) ^ (ar & 7))) * 2;
+  }
   const char* wsrc[2];
 #pragma unroll
   for (int j = 0; j < 2; ++j)
@@ -144,103 +161,117 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   const uint32_t ring_lds = (uint32_t)(size_t)(lds_char_t*)ring;
   auto issue = [&](int st) {
     const int sc = st < S ? st : S - 1;
-    const uint32_t base = ring_lds + (st % KL_NS) * KL_STG;
+    const uint32_t base = ring_lds + (st % NS) * STG;
     const size_t offw = (size_t)a.w_stage * sc;
-    if (lane < 32) load_to_lds16(asrc + 2 * KL_BK * sc, base + wave * 512);
-    load_to_lds16_nt(wsrc[0] + offw, base + 2048 + (2 * wave) * 1024);
-    load_to_lds16_nt(wsrc[1] + offw, base + 2048 + (2 * wave + 1) * 1024);
+#pragma unroll
+    for (int q = 0; q < RB; ++q)
+      if (lane < 32) load_to_lds16(asrc[q] + 2 * KL_BK * sc, base + (wave + 4 * q) * 512);
+    load_to_lds16_nt(wsrc[0] + offw, base + AB + (2 * wave) * 1024);
+    load_to_lds16_nt(wsrc[1] + offw, base + AB + (2 * wave + 1) * 1024);
   };
-  f32x4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  f32x4_t acc[RB];
+#pragma unroll
+  for (int b = 0; b < RB; ++b) acc[b] = (f32x4_t){0.0f, 0.0f, 0.0f, 0.0f};
   auto mma = [&](const char* X) {
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       const int pos = ((4 * t + kg) ^ (i & 7)) << 4;
-      const uint4 av = *reinterpret_cast<const uint4*>(X + i * 128 + pos);
-      const uint4 bv = *reinterpret_cast<const uint4*>(X + 2048 + (16 * wave + i) * 128 + pos);
-      acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
-                                                    __builtin_bit_cast(bf16x8_t, bv), acc, 0, 0, 0);
+      const uint4 bv = *reinterpret_cast<const uint4*>(X + AB + (16 * wave + i) * 128 + pos);
+#pragma unroll
+      for (int b = 0; b < RB; ++b) {
+        const uint4 av = *reinterpret_cast<const uint4*>(X + (16 * b + i) * 128 + pos);
+        acc[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av),
+                                                         __builtin_bit_cast(bf16x8_t, bv), acc[b],
+                                                         0, 0, 0);
+      }
     }
   };
-  for (int st = 0; st < KL_NS - 1; ++st) issue(st);
+  for (int st = 0; st < NS - 1; ++st) issue(st);
   for (int st = 0; st < S; ++st) {
-    // this wave's loads of stage st have landed (KL_NS - 2 later stages may be
+    // this wave's loads of stage st have landed (NS - 2 later stages may be
     // in flight); after the barrier every wave's have, and every wave is done
     // with stage st - 1, whose buffer the next issue refills
-    asm volatile("s_waitcnt vmcnt(%0)" : : "n"(3 * (KL_NS - 2)) : "memory");
+    asm volatile("s_waitcnt vmcnt(%0)" : : "n"((RB + 2) * (NS - 2)) : "memory");
     __builtin_amdgcn_s_barrier();
     compiler_fence();
-    issue(st + KL_NS - 1);
-    mma(ring + (st % KL_NS) * KL_STG);
+    issue(st + NS - 1);
+    mma(ring + (st % NS) * STG);
   }
   asm volatile("s_waitcnt vmcnt(0)" : : : "memory");   // no load into LDS outlives the loop
   compiler_fence();
-  // lane holds C[4*kg + r][i] for r < 4: kg 0,1 full rows 0..7, kg 2,3 compressed rows 0..7
-  float lf[4], lc[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const float x = acc[r];
-    const float y = __shfl_xor(x, 32);
-    lf[r] = x;   // meaningful in lanes 0..31
-    lc[r] = y;
-  }
-  // per kl row rho = 4*kg + r (lanes 0..31): statistics over this workgroup's 64 columns
-  float m[4], s[4], mu[4], At[4];
-#pragma unroll
-  for (int r = 0; r < 4; ++r) m[r] = max16(lf[r]);
-  if (lane < 32 && i == 0)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][0] = m[r];
-  __syncthreads();
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int rho = 4 * (kg & 1) + r;
-    float M = red[0][rho][0];
-    for (int w = 1; w < KL_WAVES; ++w) M = fmaxf(M, red[w][rho][0]);
-    m[r] = M;
-    const float p = __expf(lf[r] - M);
-    s[r] = sum16(p);
-    mu[r] = sum16(p * (lf[r] - lc[r]));
-  }
-  if (lane < 32 && i == 0)
+  // block b's statistics: lane holds C[4*kg + r][i] for r < 4: kg 0,1 full
+  // rows 0..7, kg 2,3 compressed rows 0..7
+  auto epilogue = [&](const f32x4_t& c, int blk) {
+    float lf[4], lc[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      red[wave][4 * kg + r][1] = s[r];
-      red[wave][4 * kg + r][2] = mu[r];
+      const float x = c[r];
+      const float y = __shfl_xor(x, 32);
+      lf[r] = x;   // meaningful in lanes 0..31
+      lc[r] = y;
     }
-  __syncthreads();
+    // per kl row rho = 4*kg + r (lanes 0..31): statistics over this workgroup's 64 columns
+    float m[4], s[4], mu[4], At[4];
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int rho = 4 * (kg & 1) + r;
-    float S = 0.0f, T = 0.0f;
-    for (int w = 0; w < KL_WAVES; ++w) {
-      S = S + red[w][rho][1];
-      T = T + red[w][rho][2];
-    }
-    s[r] = S;
-    mu[r] = T / S;
-    const float p = __expf(lf[r] - m[r]);
-    At[r] = sum16(p * gfun(mu[r] - (lf[r] - lc[r])));
-  }
-  if (lane < 32 && i == 0)
+    for (int r = 0; r < 4; ++r) m[r] = max16(lf[r]);
+    if (lane < 32 && i == 0)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][3] = At[r];
-  __syncthreads();
-  if (wave == 0 && lane < 32 && i == 0) {
+      for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][0] = m[r];
+    __syncthreads();
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int rho = 4 * kg + r;
-      const int row = rb * 8 + rho;
-      if (row < a.rows) {
-        float A = 0.0f;
-        for (int w = 0; w < KL_WAVES; ++w) A = A + red[w][rho][3];
-        float* p = a.part + ((size_t)row * a.ntiles + tile) * 4;
-        p[0] = m[r];
-        p[1] = s[r];
-        p[2] = mu[r];
-        p[3] = A / s[r];
+      const int rho = 4 * (kg & 1) + r;
+      float M = red[0][rho][0];
+      for (int w = 1; w < KL_WAVES; ++w) M = fmaxf(M, red[w][rho][0]);
+      m[r] = M;
+      const float p = __expf(lf[r] - M);
+      s[r] = sum16(p);
+      mu[r] = sum16(p * (lf[r] - lc[r]));
+    }
+    if (lane < 32 && i == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        red[wave][4 * kg + r][1] = s[r];
+        red[wave][4 * kg + r][2] = mu[r];
+      }
+    __syncthreads();
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int rho = 4 * (kg & 1) + r;
+      float Ssum = 0.0f, T = 0.0f;
+      for (int w = 0; w < KL_WAVES; ++w) {
+        Ssum = Ssum + red[w][rho][1];
+        T = T + red[w][rho][2];
+      }
+      s[r] = Ssum;
+      mu[r] = T / Ssum;
+      const float p = __expf(lf[r] - m[r]);
+      At[r] = sum16(p * gfun(mu[r] - (lf[r] - lc[r])));
+    }
+    if (lane < 32 && i == 0)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][3] = At[r];
+    __syncthreads();
+    if (wave == 0 && lane < 32 && i == 0) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int rho = 4 * kg + r;
+        const int row = blk * 8 + rho;
+        if (row < a.rows) {
+          float A = 0.0f;
+          for (int w = 0; w < KL_WAVES; ++w) A = A + red[w][rho][3];
+          float* p = a.part + ((size_t)row * a.ntiles + tile) * 4;
+          p[0] = m[r];
+          p[1] = s[r];
+          p[2] = mu[r];
+          p[3] = A / s[r];
+        }
       }
     }
-  }
+    __syncthreads();      // red is free for the next block
+  };
+#pragma unroll
+  for (int b = 0; b < RB; ++b) epilogue(acc[b], rb * RB + b);
 }
 
 // Many rows (a rollout's deferred rewards): a blocked GEMM.  A workgroup of 4
@@ -258,16 +289,16 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
 // whichever kernel and row count served it.  Workgroup g runs on
 // XCD g mod 8; the row blocks of one vocabulary block are consecutive on one
 // XCD, so its lm-head slab comes from HBM once and then from that XCD's L2.
-// Used from 25 to 128 rows with TW = 64 and two stages in flight; from 129
+// Used from 65 to 128 rows with TW = 64 and two stages in flight; from 129
 // rows on kl_mm_kernel below serves the call.
 constexpr int KG_M = 128;                       // logit rows per workgroup (64 kl rows)
 constexpr int KG_BK = 64;                       // hidden elements per stage
 constexpr int KG_RS = KG_BK * 2 + 16;           // LDS row stride (bytes)
-// Fewer rows take kl_tile_kernel, whose 8-row blocks each stream the lm head:
-// measured per call (hidden 4096, vocab 32768, packed lm head), three blocks
-// (17-24 rows) 92-94 us against 112 us here, four (25-32 rows) 117-123 us
-// against 113 us.
-constexpr int KG_MIN_ROWS = 25;
+// Fewer rows take kl_tile_kernel, each of whose row groups (up to 32 rows)
+// streams the lm head once: measured per call (hidden 4096, vocab 32768,
+// packed lm head) 50-53 us up to 16 rows, 60-63 us for 17-32, 104-107 us for
+// 33-64 (two groups), against 107-113 us here for up to 64 rows.
+constexpr int KG_MIN_ROWS = 65;
 
 template <int TW>
 constexpr int kg_lds() { return (KG_M + 2 * TW) * KG_RS; }
@@ -713,9 +744,14 @@ int launch_kl(const KLArgs& a, void* stream) {
     if (a.w_stage != 128) launch_kl_gemm<64, 2, true>(a, s);
     else launch_kl_gemm<64, 2, false>(a, s);
   } else {
-    const int nrb = (a.rows + 7) / 8;
-    const int g1 = 8 * ((a.ntiles + 7) / 8) * nrb;
-    hipLaunchKernelGGL(kl_tile_kernel, dim3(g1), dim3(64 * KL_WAVES), 0, s, a);
+    // 8-row blocks per workgroup: one, two or four (up to 32 rows, the lm head
+    // streams once per row group)
+    const int rb = a.rows <= 8 ? 1 : a.rows <= 16 ? 2 : 4;
+    const int nrb = (a.rows + 8 * rb - 1) / (8 * rb);
+    const dim3 g1(8 * ((a.ntiles + 7) / 8) * nrb), blk(64 * KL_WAVES);
+    if (rb == 1) hipLaunchKernelGGL(kl_tile_kernel<1>, g1, blk, 0, s, a);
+    else if (rb == 2) hipLaunchKernelGGL(kl_tile_kernel<2>, g1, blk, 0, s, a);
+    else hipLaunchKernelGGL(kl_tile_kernel<4>, g1, blk, 0, s, a);
   }
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();

@@ -59,14 +59,15 @@ def test_kl_reward_full_size(which):
     assert np.all(got >= 0)
 
 
-# up to 24 rows take the per-step kernel (8-row blocks), 25-128 the blocked
-# GEMM, more the large-tile GEMM (partial row blocks, vocabularies that end
-# inside a 256-column block, a 128k-token vocabulary: 2048 tiles per row in
-# the merge)
+# up to 64 rows take the per-step kernel (workgroups of 8, 16 or 32 rows),
+# 65-128 the blocked GEMM, more the large-tile GEMM (partial row blocks,
+# vocabularies that end inside a 256-column block, a 128k-token vocabulary:
+# 2048 tiles per row in the merge)
 @pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (13, 256, 1024), (15, 128, 4160),
-                                          (16, 128, 256), (24, 256, 4160), (25, 128, 640),
-                                          (64, 512, 4096), (100, 256, 4160), (128, 128, 640),
-                                          (129, 256, 4160), (523, 128, 640), (4, 128, 131072)])
+                                          (16, 128, 256), (17, 256, 4160), (32, 128, 640),
+                                          (33, 128, 4160), (64, 512, 4096), (65, 128, 640),
+                                          (100, 256, 4160), (128, 128, 640), (129, 256, 4160),
+                                          (523, 128, 640), (4, 128, 131072)])
 def test_kl_reward_shapes(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 7 + hid)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
@@ -99,8 +100,9 @@ def test_kl_reward_deferred_rollout_full_size():
 
 
 def test_kl_reward_does_not_depend_on_the_rows_per_call():
-    """The per-step kernel (up to 24 rows) and both GEMM shapes (25..128 rows,
-    129 and more) give every row the same bits."""
+    """The per-step kernel (up to 64 rows, 8, 16 or 32 rows per workgroup) and
+    both GEMM shapes (65..128 rows, 129 and more) give every row the same
+    bits."""
     wl = W.WORKLOADS[5]
     hid, voc = wl.kl_hidden, wl.kl_vocab
     w = torch.empty((voc, hid), dtype=torch.bfloat16, device="cuda")
@@ -111,8 +113,12 @@ def test_kl_reward_does_not_depend_on_the_rows_per_call():
     wide = _kl_gpu(300, hid, voc, hf, hc, w)
     narrow = _kl_gpu(100, hid, voc, hf[:100], hc[:100], w)
     step = _kl_gpu(8, hid, voc, hf[96:104].contiguous(), hc[96:104].contiguous(), w)
+    step16 = _kl_gpu(13, hid, voc, hf[40:53].contiguous(), hc[40:53].contiguous(), w)
+    step32 = _kl_gpu(29, hid, voc, hf[200:229].contiguous(), hc[200:229].contiguous(), w)
     assert np.array_equal(wide[:100], narrow)
     assert np.array_equal(wide[96:104], step)
+    assert np.array_equal(wide[40:53], step16)
+    assert np.array_equal(wide[200:229], step32)
 
 
 def test_kl_reward_at_the_maximum_row_count():

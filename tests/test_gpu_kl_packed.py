@@ -64,12 +64,13 @@ def test_pack_layout_matches_its_definition(voc, hid):
                                                 .manual_seed(voc + hid)).to(torch.bfloat16))
 
 
-# every kernel the reward dispatches to (per-step up to 24 rows, the two GEMM
-# shapes from 25 and from 129 rows) on both sides of each boundary,
-# vocabularies ending inside a GEMM block
-@pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (8, 256, 1024), (15, 128, 4160),
-                                          (24, 128, 256), (25, 128, 4160), (100, 256, 4160),
-                                          (128, 128, 640), (129, 128, 4160), (523, 128, 640)])
+# every kernel the reward dispatches to (per-step up to 64 rows in workgroups
+# of 8, 16 or 32, the two GEMM shapes from 65 and from 129 rows) on both
+# sides of each boundary, vocabularies ending inside a GEMM block
+@pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (8, 256, 1024), (9, 128, 640),
+                                          (16, 128, 4160), (17, 128, 256), (32, 256, 4160),
+                                          (64, 128, 640), (65, 128, 4160), (128, 128, 640),
+                                          (129, 128, 4160), (523, 128, 640)])
 def test_packed_reward_is_bit_identical_and_matches_the_oracle(rows, hid, voc):
     g = torch.Generator(device="cpu").manual_seed(rows * 11 + voc)
     hf = torch.randn(rows, hid, generator=g).to(torch.bfloat16)
@@ -83,10 +84,11 @@ def test_packed_reward_is_bit_identical_and_matches_the_oracle(rows, hid, voc):
     assert np.all(np.abs(packed - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed, ref)
 
 
-@pytest.mark.parametrize("rows", [8, 100, 300])
+@pytest.mark.parametrize("rows", [8, 32, 100, 300])
 def test_packed_reward_full_size(rows):
-    """hidden 4096, vocab 32768: the per-step call (8 rows), the blocked GEMM
-    (100 rows) and the large-tile GEMM (300 rows, a partial last row block),
+    """hidden 4096, vocab 32768: the per-step call (8 rows; 32 rows, four 8-row
+    blocks per workgroup), the blocked GEMM (100 rows) and the large-tile GEMM
+    (300 rows, a partial last row block),
     bit-identical to the row-major weight; sampled rows against the oracle;
     an unpruned row exactly 0."""
     wl = W.WORKLOADS[5]
@@ -101,7 +103,8 @@ def test_packed_reward_full_size(rows):
     packed = _kl(B.dc_kl_reward_packed, rows, hid, voc, hfd, hcd, _pack(w))
     assert np.array_equal(plain.view(np.uint32), packed.view(np.uint32))
     assert packed[3] == 0.0
-    idx = {8: [0, 3, 7], 100: [0, 3, 63, 64, 99], 300: [0, 3, 127, 128, 255, 256, 299]}[rows]
+    idx = {8: [0, 3, 7], 32: [0, 3, 15, 16, 31], 100: [0, 3, 63, 64, 99],
+           300: [0, 3, 127, 128, 255, 256, 299]}[rows]
     ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], w.float().cpu().numpy())
     assert np.all(np.abs(packed[idx] - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed[idx], ref)
 
