@@ -11,7 +11,7 @@
 // exactly 0.  Q's normaliser never appears.
 //
 // Kernel 1 (up to 64 rows: kl_tile_kernel, one workgroup per 64 vocabulary
-// columns and 8, 16 or 32 rows; more rows: the blocked GEMMs below, same
+// columns and 8, 16, 32 or 64 rows; more rows: the blocked GEMMs below, same
 // arithmetic): MFMA
 // 16x16x32 bf16 over the hidden dimension for a 16-row A = [8 full rows; the 8
 // matching compressed rows], then per (row, 64-column tile) the local statistics
@@ -96,14 +96,14 @@ __device__ __forceinline__ float max16(float x) {
   return x;
 }
 
-// A workgroup serves RB blocks of 8 kl rows (1, 2 or 4): each block is its
-// own 16-row A operand (8 full, then the 8 compressed hidden states), and
+// A workgroup serves RB blocks of 8 kl rows (1, 2, 4 or 8): each block is
+// its own 16-row A operand (8 full, then the 8 compressed hidden states), and
 // every lm-head stage in LDS feeds the matrix cores for all of them, so a
 // call of up to 8 RB rows streams the lm head once.  The stage ring is five
-// deep, four for RB = 4 (two workgroups per CU either way).
+// deep, four for RB = 4 and three for RB = 8 (two workgroups per CU).
 template <int RB>
 struct KLT {
-  static constexpr int NS = RB == 4 ? 4 : KL_NS;                 // stage buffers
+  static constexpr int NS = RB == 8 ? 3 : RB == 4 ? 4 : KL_NS;    // stage buffers
   static constexpr int AB = 16 * RB * KL_BK * 2;                 // A bytes of a stage
   static constexpr int STG = AB + KL_TILE * KL_BK * 2;           // bytes of a stage
 };
@@ -161,7 +161,8 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   const uint32_t ring_lds = (uint32_t)(size_t)(lds_char_t*)ring;
   auto issue = [&](int st) {
     const int sc = st < S ? st : S - 1;
-    const uint32_t base = ring_lds + (st % NS) * STG;
+    // (uniform: the LDS address goes to M0 through a scalar register)
+    const uint32_t base = __builtin_amdgcn_readfirstlane(ring_lds + (st % NS) * STG);
     const size_t offw = (size_t)a.w_stage * sc;
 #pragma unroll
     for (int q = 0; q < RB; ++q)
@@ -294,10 +295,10 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
 constexpr int KG_M = 128;                       // logit rows per workgroup (64 kl rows)
 constexpr int KG_BK = 64;                       // hidden elements per stage
 constexpr int KG_RS = KG_BK * 2 + 16;           // LDS row stride (bytes)
-// Fewer rows take kl_tile_kernel, each of whose row groups (up to 32 rows)
-// streams the lm head once: measured per call (hidden 4096, vocab 32768,
-// packed lm head) 50-53 us up to 16 rows, 60-63 us for 17-32, 104-107 us for
-// 33-64 (two groups), against 107-113 us here for up to 64 rows.
+// Fewer rows take kl_tile_kernel, whose workgroups stream the lm head once
+// for up to 64 rows: measured per call (hidden 4096, vocab 32768, packed lm
+// head) 50-53 us up to 16 rows, 60-66 us for 17-32, 92-96 us for 33-64,
+// against 107-113 us here for up to 64 rows.
 constexpr int KG_MIN_ROWS = 65;
 
 template <int TW>
@@ -744,14 +745,15 @@ int launch_kl(const KLArgs& a, void* stream) {
     if (a.w_stage != 128) launch_kl_gemm<64, 2, true>(a, s);
     else launch_kl_gemm<64, 2, false>(a, s);
   } else {
-    // 8-row blocks per workgroup: one, two or four (up to 32 rows, the lm head
-    // streams once per row group)
-    const int rb = a.rows <= 8 ? 1 : a.rows <= 16 ? 2 : 4;
+    // 8-row blocks per workgroup: one, two, four or eight (the lm head streams
+    // once per row group)
+    const int rb = a.rows <= 8 ? 1 : a.rows <= 16 ? 2 : a.rows <= 32 ? 4 : 8;
     const int nrb = (a.rows + 8 * rb - 1) / (8 * rb);
     const dim3 g1(8 * ((a.ntiles + 7) / 8) * nrb), blk(64 * KL_WAVES);
     if (rb == 1) hipLaunchKernelGGL(kl_tile_kernel<1>, g1, blk, 0, s, a);
     else if (rb == 2) hipLaunchKernelGGL(kl_tile_kernel<2>, g1, blk, 0, s, a);
-    else hipLaunchKernelGGL(kl_tile_kernel<4>, g1, blk, 0, s, a);
+    else if (rb == 4) hipLaunchKernelGGL(kl_tile_kernel<4>, g1, blk, 0, s, a);
+    else hipLaunchKernelGGL(kl_tile_kernel<8>, g1, blk, 0, s, a);
   }
   hipLaunchKernelGGL(kl_merge_kernel, dim3(a.rows), dim3(256), 0, s, a);
   return (int)hipGetLastError();

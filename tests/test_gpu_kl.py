@@ -59,7 +59,7 @@ def test_kl_reward_full_size(which):
     assert np.all(got >= 0)
 
 
-# up to 64 rows take the per-step kernel (workgroups of 8, 16 or 32 rows),
+# up to 64 rows take the per-step kernel (workgroups of 8, 16, 32 or 64 rows),
 # 65-128 the blocked GEMM, more the large-tile GEMM (partial row blocks,
 # vocabularies that end inside a 256-column block, a 128k-token vocabulary:
 # 2048 tiles per row in the merge)
@@ -100,7 +100,7 @@ def test_kl_reward_deferred_rollout_full_size():
 
 
 def test_kl_reward_does_not_depend_on_the_rows_per_call():
-    """The per-step kernel (up to 64 rows, 8, 16 or 32 rows per workgroup) and
+    """The per-step kernel (up to 64 rows, 8, 16, 32 or 64 rows per workgroup) and
     both GEMM shapes (65..128 rows, 129 and more) give every row the same
     bits."""
     wl = W.WORKLOADS[5]
@@ -115,10 +115,12 @@ def test_kl_reward_does_not_depend_on_the_rows_per_call():
     step = _kl_gpu(8, hid, voc, hf[96:104].contiguous(), hc[96:104].contiguous(), w)
     step16 = _kl_gpu(13, hid, voc, hf[40:53].contiguous(), hc[40:53].contiguous(), w)
     step32 = _kl_gpu(29, hid, voc, hf[200:229].contiguous(), hc[200:229].contiguous(), w)
+    step64 = _kl_gpu(50, hid, voc, hf[250:300].contiguous(), hc[250:300].contiguous(), w)
     assert np.array_equal(wide[:100], narrow)
     assert np.array_equal(wide[96:104], step)
     assert np.array_equal(wide[40:53], step16)
     assert np.array_equal(wide[200:229], step32)
+    assert np.array_equal(wide[250:300], step64)
 
 
 def test_kl_reward_at_the_maximum_row_count():

@@ -65,7 +65,7 @@ def test_pack_layout_matches_its_definition(voc, hid):
 
 
 # every kernel the reward dispatches to (per-step up to 64 rows in workgroups
-# of 8, 16 or 32, the two GEMM shapes from 65 and from 129 rows) on both
+# of 8, 16, 32 or 64, the two GEMM shapes from 65 and from 129 rows) on both
 # sides of each boundary, vocabularies ending inside a GEMM block
 @pytest.mark.parametrize("rows,hid,voc", [(1, 128, 64), (8, 256, 1024), (9, 128, 640),
                                           (16, 128, 4160), (17, 128, 256), (32, 256, 4160),
@@ -84,10 +84,10 @@ def test_packed_reward_is_bit_identical_and_matches_the_oracle(rows, hid, voc):
     assert np.all(np.abs(packed - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed, ref)
 
 
-@pytest.mark.parametrize("rows", [8, 32, 100, 300])
+@pytest.mark.parametrize("rows", [8, 32, 64, 100, 300])
 def test_packed_reward_full_size(rows):
-    """hidden 4096, vocab 32768: the per-step call (8 rows; 32 rows, four 8-row
-    blocks per workgroup), the blocked GEMM (100 rows) and the large-tile GEMM
+    """hidden 4096, vocab 32768: the per-step call (8 rows; 32 and 64 rows, four
+    and eight 8-row blocks per workgroup), the blocked GEMM (100 rows) and the large-tile GEMM
     (300 rows, a partial last row block),
     bit-identical to the row-major weight; sampled rows against the oracle;
     an unpruned row exactly 0."""
@@ -103,7 +103,7 @@ def test_packed_reward_full_size(rows):
     packed = _kl(B.dc_kl_reward_packed, rows, hid, voc, hfd, hcd, _pack(w))
     assert np.array_equal(plain.view(np.uint32), packed.view(np.uint32))
     assert packed[3] == 0.0
-    idx = {8: [0, 3, 7], 32: [0, 3, 15, 16, 31], 100: [0, 3, 63, 64, 99],
+    idx = {8: [0, 3, 7], 32: [0, 3, 15, 16, 31], 64: [0, 3, 31, 32, 63], 100: [0, 3, 63, 64, 99],
            300: [0, 3, 127, 128, 255, 256, 299]}[rows]
     ref = okl.kl_reward(hf.float().numpy()[idx], hc.float().numpy()[idx], w.float().cpu().numpy())
     assert np.all(np.abs(packed[idx] - ref) <= 1e-3 * np.abs(ref) + 1e-6), (packed[idx], ref)
