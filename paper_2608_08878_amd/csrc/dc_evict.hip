@@ -23,31 +23,34 @@
 
 namespace dc {
 
-// Caches up to ENT * REG_KPT rows: scores in registers, one workgroup per unit.
-template <int DTYPE, int D>
-__global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
+// Caches up to NT * KPT rows: scores in registers, one workgroup of NT
+// threads per unit.  Up to 4608 rows (the steady step of a 4096-row budget
+// and more) 512 threads of 9 rows, two workgroups per CU, so one unit's
+// scoring overlaps another's selection; up to 8192 rows 1024 threads of 8.
+template <int DTYPE, int D, int NT, int KPT>
+__global__ void __launch_bounds__(NT, 4) score_select_kernel(EvictArgs a) {
   extern __shared__ int dyn[];
   __shared__ SelShared sh;
   const int u = blockIdx.x, tid = threadIdx.x, wave = tid >> 6;
   const size_t ub = (size_t)u * a.cap;
   const float invT = 1.0f / (float)a.T;
   const int L = a.L;
-  const int kact = L > wave * 64 ? (L - wave * 64 + ENT - 1) / ENT : 0;
-  float x[REG_KPT][4];
-  int32_t pk[REG_KPT];
+  const int kact = L > wave * 64 ? (L - wave * 64 + NT - 1) / NT : 0;
+  float x[KPT][4];
+  int32_t pk[KPT];
 #pragma unroll
-  for (int k = 0; k < REG_KPT; ++k) {
+  for (int k = 0; k < KPT; ++k) {
     if (k < kact) {
-      const int r = k * ENT + tid;
+      const int r = k * NT + tid;
       load_features(a, ub + (r < L ? r : L - 1), invT, x[k], pk[k]);
     }
   }
-  float sc[REG_KPT];
-  policy_scores<REG_KPT>(a, x, sc, kact);
-  RegKeys<REG_KPT> keys;
+  float sc[KPT];
+  policy_scores<KPT>(a, x, sc, kact);
+  RegKeys<KPT> keys;
 #pragma unroll
-  for (int k = 0; k < REG_KPT; ++k) {
-    const int r = k * ENT + tid;
+  for (int k = 0; k < KPT; ++k) {
+    const int r = k * NT + tid;
     keys.key[k] = ~0ull;
     if (k < kact && r < L) {
       if (a.scores_out) a.scores_out[(size_t)u * L + r] = sc[k];
@@ -56,10 +59,10 @@ __global__ void __launch_bounds__(ENT) score_select_kernel(EvictArgs a) {
   }
   if (!a.evict) {
     if (a.kept_out)
-      for (int r = tid; r < L; r += ENT) a.kept_out[(size_t)u * L + r] = r;
+      for (int r = tid; r < L; r += NT) a.kept_out[(size_t)u * L + r] = r;
     return;
   }
-  select_compact<RegKeys<REG_KPT>, DTYPE, D, ENT, 2, true>(a, u, a.L, a.budget, keys, REG_KPT, sh, dyn);
+  select_compact<RegKeys<KPT>, DTYPE, D, NT, 2, true>(a, u, a.L, a.budget, keys, KPT, sh, dyn);
 }
 
 // Long caches: scores to keys in the workspace (grid over rows) ...
@@ -146,9 +149,10 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
   const bool ragged = a.unit_len || a.budgets;
   if (!a.ext && !ragged && a.L <= ENT * REG_KPT) {
     // the one-hidden-layer policy on a short cache: scores in registers
-    auto k = score_select_kernel<DTYPE, D>;
+    const bool half = a.L <= 512 * 9;
+    auto k = half ? score_select_kernel<DTYPE, D, 512, 9> : score_select_kernel<DTYPE, D, ENT, REG_KPT>;
     hipFuncSetAttribute((const void*)k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)dyn);
-    hipLaunchKernelGGL(k, dim3(a.units), dim3(ENT), dyn, s, b);
+    hipLaunchKernelGGL(k, dim3(a.units), dim3(half ? 512 : ENT), dyn, s, b);
     return (int)hipGetLastError();
   }
   // scores to row keys in the workspace (grid over rows), then one select per
