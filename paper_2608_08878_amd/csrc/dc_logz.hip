@@ -145,6 +145,9 @@ __device__ UnitStats unit_stats(const LogzArgs& a, const UnitDims& d, const floa
                                 const int32_t* kept, int lane) {
   double mx = -INFINITY, sum = 0.0, ks = 0.0;
   int bad = 0;
+  // (unrolled so that eight iterations' loads are in flight together; the
+  // sums keep their order)
+#pragma unroll 8
   for (int i = lane; i < d.L; i += 64) {
     const double r = r_of(a, s[i]);
     bad |= !isfinite(r);
@@ -153,6 +156,7 @@ __device__ UnitStats unit_stats(const LogzArgs& a, const UnitDims& d, const floa
     sum += r;
   }
   if (kept) {
+#pragma unroll 8
     for (int t = lane; t < d.nk; t += 64) {
       const int idx = kept[t];
       if (idx < 0 || idx >= d.L) bad = 1;
@@ -229,6 +233,7 @@ __global__ void __launch_bounds__(64) logz_rows_kernel(LogzArgs a) {
   }
   for (int i0 = 0; i0 < d.L; i0 += 64 * RENORM) {
     const int iend = d.L < i0 + 64 * RENORM ? d.L : i0 + 64 * RENORM;
+#pragma unroll 8
     for (int i = i0 + lane; i < iend; i += 64) {
       float xm;
       int xk;
