@@ -169,10 +169,12 @@ static int launch_evict_t(const EvictArgs& a, uint64_t* ws_keys, hipStream_t s) 
     for_grid_y(a.units, [&](int y0, int ny) {
       EvictArgs c = b;
       c.y0 = y0;
-      // ragged caches: a quarter of the row blocks, each workgroup striding over
-      // up to four (most units are far shorter than the longest one, whose
-      // length sizes the grid)
-      const dim3 grid(ragged ? (a.L + 1023) / 1024 : (a.L + 255) / 256, ny);
+      // a quarter of the 256-row blocks, each workgroup striding over up to
+      // four: ragged caches leave most workgroups of the longest unit's grid
+      // idle otherwise, and uniform ones launch a quarter of the workgroups
+      // (workload 3's compression step, 4096 units of 16385 rows: 784-832 ->
+      // 746-750 us)
+      const dim3 grid((a.L + 1023) / 1024, ny);
       if (a.ext) hipLaunchKernelGGL(score_ext_kernel, grid, dim3(256), 0, s, c, ws_keys, kstride);
       else hipLaunchKernelGGL(score_kernel, grid, dim3(256), 0, s, c, ws_keys, kstride);
     });
