@@ -68,15 +68,15 @@ __device__ __forceinline__ size_t w_row_off(const KLArgs& a, int v) {
 __device__ __forceinline__ float gfun(float y) {
   const float ay = fabsf(y);
   if (ay < 0.5f) {
-    // y^2/2 * (1 + y/3 (1 + y/4 (1 + y/5 (1 + y/6 (1 + y/7 (1 + y/8 (1 + y/9)))))))
-    float t = 1.0f + y * (1.0f / 9.0f);
-    t = 1.0f + (y * (1.0f / 8.0f)) * t;
-    t = 1.0f + (y * (1.0f / 7.0f)) * t;
-    t = 1.0f + (y * (1.0f / 6.0f)) * t;
-    t = 1.0f + (y * (1.0f / 5.0f)) * t;
-    t = 1.0f + (y * (1.0f / 4.0f)) * t;
-    t = 1.0f + (y * (1.0f / 3.0f)) * t;
-    return (0.5f * y * y) * t;
+    // y^2 (1/2! + y (1/3! + ... + y / 9!)), Horner with fused multiply-adds
+    float t = fmaf(y, 1.0f / 362880.0f, 1.0f / 40320.0f);
+    t = fmaf(y, t, 1.0f / 5040.0f);
+    t = fmaf(y, t, 1.0f / 720.0f);
+    t = fmaf(y, t, 1.0f / 120.0f);
+    t = fmaf(y, t, 1.0f / 24.0f);
+    t = fmaf(y, t, 1.0f / 6.0f);
+    t = fmaf(y, t, 0.5f);
+    return (y * y) * t;
   }
   return expm1f(y) - y;
 }
@@ -115,8 +115,9 @@ struct KLT {
 template <int RB>
 __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
   constexpr int NS = KLT<RB>::NS, AB = KLT<RB>::AB, STG = KLT<RB>::STG;
-  __shared__ float red[KL_WAVES][8][4];
+  __shared__ float red[KL_WAVES][8];        // per-wave row maxima
   __shared__ __attribute__((aligned(1024))) char ring[NS * STG];
+  __shared__ float4 xp[KL_WAVES][32], xd[KL_WAVES][32], xg[KL_WAVES][32];
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int nrb = (a.rows + 8 * RB - 1) / (8 * RB);
@@ -211,65 +212,69 @@ __global__ void __launch_bounds__(64 * KL_WAVES) kl_tile_kernel(KLArgs a) {
       lf[r] = x;   // meaningful in lanes 0..31
       lc[r] = y;
     }
-    // per kl row rho = 4*kg + r (lanes 0..31): statistics over this workgroup's 64 columns
-    float m[4], s[4], mu[4], At[4];
+    // per kl row rho = 4*kg + r (lanes 0..31): statistics over this workgroup's
+    // 64 columns, wave w holding columns 16 w .. 16 w + 15.  The maximum goes
+    // through red; every sum adds the four waves' terms of a column lane by
+    // lane in column order, then the 16 lanes (the blocked GEMMs' order, where
+    // one lane holds all four blocks).
+    float m[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) m[r] = max16(lf[r]);
     if (lane < 32 && i == 0)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][0] = m[r];
+      for (int r = 0; r < 4; ++r) red[wave][4 * kg + r] = m[r];
     __syncthreads();
+    float p[4], d[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int rho = 4 * (kg & 1) + r;
-      float M = red[0][rho][0];
-      for (int w = 1; w < KL_WAVES; ++w) M = fmaxf(M, red[w][rho][0]);
+      float M = red[0][rho];
+      for (int w = 1; w < KL_WAVES; ++w) M = fmaxf(M, red[w][rho]);
       m[r] = M;
-      const float p = __expf(lf[r] - M);
-      s[r] = sum16(p);
-      mu[r] = sum16(p * (lf[r] - lc[r]));
+      p[r] = __expf(lf[r] - M);
+      d[r] = lf[r] - lc[r];
     }
-    if (lane < 32 && i == 0)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        red[wave][4 * kg + r][1] = s[r];
-        red[wave][4 * kg + r][2] = mu[r];
-      }
-    __syncthreads();
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int rho = 4 * (kg & 1) + r;
-      float Ssum = 0.0f, T = 0.0f;
-      for (int w = 0; w < KL_WAVES; ++w) {
-        Ssum = Ssum + red[w][rho][1];
-        T = T + red[w][rho][2];
-      }
-      s[r] = Ssum;
-      mu[r] = T / Ssum;
-      const float p = __expf(lf[r] - m[r]);
-      At[r] = sum16(p * gfun(mu[r] - (lf[r] - lc[r])));
+    if (lane < 32) {
+      xp[wave][lane] = make_float4(p[0], p[1], p[2], p[3]);
+      xd[wave][lane] = make_float4(p[0] * d[0], p[1] * d[1], p[2] * d[2], p[3] * d[3]);
     }
-    if (lane < 32 && i == 0)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) red[wave][4 * kg + r][3] = At[r];
     __syncthreads();
-    if (wave == 0 && lane < 32 && i == 0) {
+    float s[4], mu[4];
+    {
+      const int l = lane & 31;
+      const float4 p0 = xp[0][l], p1 = xp[1][l], p2 = xp[2][l], p3 = xp[3][l];
+      const float4 d0 = xd[0][l], d1 = xd[1][l], d2 = xd[2][l], d3 = xd[3][l];
+      s[0] = sum16(((p0.x + p1.x) + p2.x) + p3.x);
+      s[1] = sum16(((p0.y + p1.y) + p2.y) + p3.y);
+      s[2] = sum16(((p0.z + p1.z) + p2.z) + p3.z);
+      s[3] = sum16(((p0.w + p1.w) + p2.w) + p3.w);
+      mu[0] = sum16(((d0.x + d1.x) + d2.x) + d3.x) / s[0];
+      mu[1] = sum16(((d0.y + d1.y) + d2.y) + d3.y) / s[1];
+      mu[2] = sum16(((d0.z + d1.z) + d2.z) + d3.z) / s[2];
+      mu[3] = sum16(((d0.w + d1.w) + d2.w) + d3.w) / s[3];
+    }
+    if (lane < 32)
+      xg[wave][lane] = make_float4(p[0] * gfun(mu[0] - d[0]), p[1] * gfun(mu[1] - d[1]),
+                                   p[2] * gfun(mu[2] - d[2]), p[3] * gfun(mu[3] - d[3]));
+    __syncthreads();
+    if (wave == 0 && lane < 32) {
+      const float4 g0 = xg[0][lane], g1 = xg[1][lane], g2 = xg[2][lane], g3 = xg[3][lane];
+      const float At[4] = {sum16(((g0.x + g1.x) + g2.x) + g3.x), sum16(((g0.y + g1.y) + g2.y) + g3.y),
+                           sum16(((g0.z + g1.z) + g2.z) + g3.z), sum16(((g0.w + g1.w) + g2.w) + g3.w)};
+      if (i == 0)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int rho = 4 * kg + r;
-        const int row = blk * 8 + rho;
-        if (row < a.rows) {
-          float A = 0.0f;
-          for (int w = 0; w < KL_WAVES; ++w) A = A + red[w][rho][3];
-          float* p = a.part + ((size_t)row * a.ntiles + tile) * 4;
-          p[0] = m[r];
-          p[1] = s[r];
-          p[2] = mu[r];
-          p[3] = A / s[r];
+        for (int r = 0; r < 4; ++r) {
+          const int row = blk * 8 + 4 * kg + r;
+          if (row < a.rows) {
+            float* q = a.part + ((size_t)row * a.ntiles + tile) * 4;
+            q[0] = m[r];
+            q[1] = s[r];
+            q[2] = mu[r];
+            q[3] = At[r] / s[r];
+          }
         }
-      }
     }
-    __syncthreads();      // red is free for the next block
+    __syncthreads();      // red and the exchange arrays are free for the next block
   };
 #pragma unroll
   for (int b = 0; b < RB; ++b) epilogue(acc[b], rb * RB + b);
@@ -407,8 +412,8 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
   // lanes kg = 0, 1 the full rows 4 kg + r of block b, lanes kg = 2, 3 the same
   // rows compressed.  Lanes 0..31 form the statistics of kl row 8 b + 4 kg + r
   // over each 64-column tile g (blocks c = 4 g .. 4 g + 3), in the per-step
-  // kernel's reduction order (16-lane sums per 16-column block, then the blocks
-  // in column order), so a row's statistics, and its KL, do not depend on how
+  // kernel's reduction order (the four 16-column blocks' terms added lane by
+  // lane in column order, then the 16 lanes), so a row's statistics, and its KL, do not depend on how
   // many rows share the call.  One call per row block b, so that every index
   // into the accumulators is a constant.
   auto epilogue = [&](const f32x4_t (&ab)[CB], int b) {
@@ -427,17 +432,16 @@ __global__ void __launch_bounds__(256, 2) kl_gemm_kernel(KLArgs a) {
       for (int r = 0; r < 4; ++r) {
         float m = fmaxf(fmaxf(lf[0][r], lf[1][r]), fmaxf(lf[2][r], lf[3][r]));
         m = max16(m);
-        float p[4], S = 0.0f, T = 0.0f;
+        float p[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          p[c] = __expf(lf[c][r] - m);
-          S = S + sum16(p[c]);
-          T = T + sum16(p[c] * dl[c][r]);
-        }
+        for (int c = 0; c < 4; ++c) p[c] = __expf(lf[c][r] - m);
+        const float S = sum16(((p[0] + p[1]) + p[2]) + p[3]);
+        const float T = sum16(((p[0] * dl[0][r] + p[1] * dl[1][r]) + p[2] * dl[2][r]) + p[3] * dl[3][r]);
         const float mu = T / S;
-        float A = 0.0f;
+        float pg[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c) A = A + sum16(p[c] * gfun(mu - dl[c][r]));
+        for (int c = 0; c < 4; ++c) pg[c] = p[c] * gfun(mu - dl[c][r]);
+        const float A = sum16(((pg[0] + pg[1]) + pg[2]) + pg[3]);
         const int row = mt * 64 + 32 * wm + 8 * b + 4 * kg + r;
         const int tile = (nt * NT + TW * wn) / 64 + g;
         if (lane < 32 && i == 0 && row < a.rows && tile < a.ntiles)
@@ -618,17 +622,16 @@ __global__ void __launch_bounds__(64 * KM_WAVES) kl_mm_kernel(KLArgs a) {
     for (int r = 0; r < 4; ++r) {
       float m = fmaxf(fmaxf(lf[0][r], lf[1][r]), fmaxf(lf[2][r], lf[3][r]));
       m = max16(m);
-      float p[4], S = 0.0f, T = 0.0f;
+      float p[4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        p[c] = __expf(lf[c][r] - m);
-        S = S + sum16(p[c]);
-        T = T + sum16(p[c] * dl[c][r]);
-      }
+      for (int c = 0; c < 4; ++c) p[c] = __expf(lf[c][r] - m);
+      const float S = sum16(((p[0] + p[1]) + p[2]) + p[3]);
+      const float T = sum16(((p[0] * dl[0][r] + p[1] * dl[1][r]) + p[2] * dl[2][r]) + p[3] * dl[3][r]);
       const float mu = T / S;
-      float A = 0.0f;
+      float pg[4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c) A = A + sum16(p[c] * gfun(mu - dl[c][r]));
+      for (int c = 0; c < 4; ++c) pg[c] = p[c] * gfun(mu - dl[c][r]);
+      const float A = sum16(((pg[0] + pg[1]) + pg[2]) + pg[3]);
       const int row = mt * 128 + 64 * wm + 8 * bb + 4 * (kg & 1) + r;
       const int tile = (nt * KM_N + 64 * wn) / 64;
       if (i == 0 && row < a.rows && tile < a.ntiles)
