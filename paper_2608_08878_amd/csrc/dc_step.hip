@@ -508,8 +508,8 @@ __device__ __forceinline__ void append_rows(const DecodeArgs& a, int u) {
 // One workgroup per unit, sized so that two fit on a CU (one computes while the
 // other streams).  Dynamic LDS: [L * RS floats: logits -> weights -> u64 keys]
 // [SNW/2 * G * D output partials][2 ints per compaction move]; the retired
-// contributions (cz, cn) of pass A go to the workspace (ws_r) and come back in
-// the feature pass.
+// contributions (cz, cn) of pass A stay in registers (lane l holds those of
+// row l of each of its wave's 64-row groups) until the feature pass.
 template <int G>
 struct RowStride {
   static constexpr int RS = G < 2 ? 2 : G;     // floats per row in LDS (a u64 key must fit)
